@@ -1,0 +1,211 @@
+/*
+ * vp.h -- C ABI of the MI355X (gfx950) video-frame preprocessing library.
+ *
+ * The library computes, on one GPU, the per-frame preprocessing of a
+ * Qwen-VL-style vision input that EasyVideoR1 (arXiv 2604.16893) caches
+ * offline so that it leaves the RL loop (Section 3.1.1, "Efficient RL with
+ * Video Caching"): temporal frame-index sampling, smart_resize to multiples
+ * of 32 under a per-modality pixel budget (Section 3.1.2, "Independent
+ * Resolution Budgets"; Section 4.1, "Training Configuration"), separable
+ * antialiased bicubic resampling of decoded uint8 RGB frames, rescale by
+ * 1/255 and per-channel mean/std normalisation (Section 1 names sampling,
+ * resizing and normalisation as the costly steps), and patchification into
+ * merge-window rows of 3 * 2 * 16 * 16 = 1536 values with the per-item grid
+ * (t, h/16, w/16) -- the video_grid_thw that every stage must reproduce
+ * identically (Section 3.1.1) -- and a row-offset table for ragged mixed
+ * image/video batches (Section 3.2.2, "Joint Image-Video Training").
+ *
+ * Conventions shared by every entry point:
+ *  - Return value: a vp_status code; VP_OK (0) on success.  No function
+ *    throws, aborts or prints.  On any non-OK status nothing has been
+ *    enqueued on the stream and no output buffer has been written, except
+ *    that *out_count / *workspace_bytes style size outputs report the size
+ *    that would have been needed (strict failure: never truncate or pad,
+ *    Section 3.2.2).
+ *  - vp_last_error_message() returns a thread-local, human-readable detail
+ *    of the last non-OK status on the calling thread.
+ *  - All functions are thread-safe.  Calls that enqueue work on the same
+ *    stream execute in stream order.
+ *  - "HOST" pointers are ordinary CPU memory, read or written before the
+ *    function returns.  "DEVICE" pointers are GPU memory of the current HIP
+ *    device, owned by the caller, and must stay valid until the stream has
+ *    reached the work the call enqueued.
+ */
+#ifndef VP_H
+#define VP_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define VP_OK 0
+#define VP_ERR_NULL 1       /* a required pointer is NULL                         */
+#define VP_ERR_ARG 2        /* an argument is out of its documented range         */
+#define VP_ERR_ASPECT 3     /* smart_resize: longer/shorter side ratio above 200  */
+#define VP_ERR_DIMS 4       /* a size is non-positive or not a multiple of 32     */
+#define VP_ERR_INDEX 5      /* a frame index lies outside [0, n_src)              */
+#define VP_ERR_FRAMES 6     /* a frame count is impossible (n < 1, n > N, ...)    */
+#define VP_ERR_CAPACITY 7   /* an output or workspace buffer is too small         */
+#define VP_ERR_HIP 8        /* a HIP runtime call failed (detail in the message)  */
+
+/* Geometry: patch 16, spatial merge 2, temporal patch 2. */
+#define VP_PATCH 16
+#define VP_MERGE 2
+#define VP_TEMPORAL_PATCH 2
+#define VP_FACTOR 32        /* VP_PATCH * VP_MERGE */
+#define VP_ROW 1536         /* 3 * VP_TEMPORAL_PATCH * VP_PATCH * VP_PATCH */
+
+/* Frame-index sampling modes. */
+#define VP_SAMPLE_UNIFORM 0
+#define VP_SAMPLE_FPS 1
+
+/* Output element types. */
+#define VP_OUT_F32 0
+#define VP_OUT_BF16 1
+
+/*
+ * smart_resize (Section 3.1.1: resize under max_pixels; Section 3.1.2:
+ * separate image / video budgets; Section 4.1: a per-frame budget).
+ *
+ * Target size (out_h, out_w), both positive multiples of `factor` (32 for
+ * this geometry), for a height x width source under the per-frame budget
+ * [min_pixels, max_pixels]:
+ *   h = max(F, rhe(H/F)*F), w = max(F, rhe(W/F)*F)   (rhe: round half to even);
+ *   if h*w > max_pixels: beta = sqrt(H*W/max_pixels),
+ *       h = max(F, floor(H/beta/F)*F), w = max(F, floor(W/beta/F)*F);
+ *   else if h*w < min_pixels: beta = sqrt(min_pixels/(H*W)),
+ *       h = ceil(H*beta/F)*F, w = ceil(W*beta/F)*F.
+ * Every expression is evaluated in IEEE double precision in the written
+ * order.  Applying the function to its own output returns the same size
+ * whenever that output lies inside the budget (stage consistency).
+ * Errors: VP_ERR_NULL (out pointers), VP_ERR_ARG (height, width, factor or
+ * max_pixels <= 0, min_pixels < 0 or > max_pixels), VP_ERR_ASPECT
+ * (max(H,W)/min(H,W) > 200), VP_ERR_DIMS (result above INT32_MAX).
+ */
+int32_t vp_smart_resize_dims(int32_t height, int32_t width, int32_t factor,
+                             int64_t min_pixels, int64_t max_pixels,
+                             int32_t* out_h, int32_t* out_w);
+
+/*
+ * Frame-index sampling (Section 3.1.1: cache entries keyed by fps and
+ * max_frames; Section 4.1: 2 FPS with at most 128 frames).
+ *
+ * mode VP_SAMPLE_UNIFORM: n = nframes indices,
+ *     idx_i = rhe(i * (N-1) / (n-1)) on the exact rational (idx = {0} for n = 1).
+ * mode VP_SAMPLE_FPS: n = N / video_fps * fps (double), clamped to
+ *     [ceil_even(min_frames), floor_even(max_frames)] and to N, floored to an
+ *     even count; then the uniform indices for that n.  nframes is ignored.
+ * out_idx: HOST int32[capacity], receives the n sorted indices in [0, N).
+ * out_count: HOST, receives n (also on VP_ERR_CAPACITY, so a caller can size
+ * the buffer).
+ * Errors: VP_ERR_NULL, VP_ERR_ARG (unknown mode; fps mode with
+ * video_fps or fps <= 0, min_frames < 1 or max_frames < min_frames),
+ * VP_ERR_FRAMES (N < 1; uniform n < 1 or n > N; fps count < 2),
+ * VP_ERR_CAPACITY (capacity < n).
+ */
+int32_t vp_sample_indices(int32_t total_frames, int32_t mode, int32_t nframes,
+                          double video_fps, double fps, int32_t min_frames, int32_t max_frames,
+                          int32_t* out_idx, int32_t capacity, int32_t* out_count);
+
+/*
+ * Antialiased bicubic filter of one axis resampled from n_in to n_out
+ * samples: Keys (1981) cubic convolution with a = -0.5, stretched by
+ * sigma = max(n_in/n_out, 1).  Output i is centred at c = (i + 0.5) *
+ * n_in/n_out and reads the window [max(0, floor(c - 2 sigma + 0.5)),
+ * min(n_in, floor(c + 2 sigma + 0.5))); its weights K((j + 0.5 - c)/sigma)
+ * are normalised to sum 1 (truncated and renormalised at the borders).
+ *
+ * vp_filter_taps: *max_taps = the longest window over all outputs.
+ * vp_filter_table: start[n_out], count[n_out] (HOST int32) and
+ * weights[n_out][taps] (HOST float, row i zero beyond count[i]); `taps`
+ * must be >= vp_filter_taps.  The weights are computed in double precision
+ * and rounded once to float.
+ * Errors: VP_ERR_NULL, VP_ERR_ARG (n_in or n_out < 1), VP_ERR_CAPACITY
+ * (taps too small).
+ */
+int32_t vp_filter_taps(int32_t n_in, int32_t n_out, int32_t* max_taps);
+int32_t vp_filter_table(int32_t n_in, int32_t n_out, int32_t taps,
+                        int32_t* start, int32_t* count, float* weights);
+
+/*
+ * One video or image of a batch.  A video is n_src decoded frames; an image
+ * is one frame (n_src = 1, n_idx = 1) that the temporal patch of 2 turns
+ * into two identical frames (Section 3.2.2: images and videos share one
+ * field schema and one batch).
+ */
+typedef struct vp_item {
+    const uint8_t* frames;   /* DEVICE [n_src][src_h][src_w][3] packed RGB, contiguous   */
+    const int32_t* indices;  /* HOST [n_idx] frame indices in [0, n_src), any order;
+                                an odd count gets its last index repeated            */
+    int32_t n_src;           /* decoded frames available, >= 1                          */
+    int32_t src_h, src_w;    /* source size, >= 1                                       */
+    int32_t n_idx;           /* sampled frames, >= 1                                    */
+    int32_t dst_h, dst_w;    /* target size, positive multiples of 32
+                                (for instance from vp_smart_resize_dims)            */
+} vp_item;
+
+/*
+ * Batch layout (Section 3.1.1: identical video_grid_thw in every stage).
+ * grid_thw: HOST int32[n_items][3] = (t, dst_h/16, dst_w/16), t = ceil(n_idx/2).
+ * cu_seqlens: HOST int32[n_items + 1], cu[0] = 0, cu[b+1] = cu[b] + t*(h/16)*(w/16);
+ *   item b owns output rows [cu[b], cu[b+1]).
+ * total_rows: HOST, = cu[n_items].
+ * workspace_bytes: HOST, the device workspace vp_preprocess_batch needs.
+ * Any of the four output pointers may be NULL when not wanted.
+ * The items' frame pointers are not dereferenced.
+ * Errors: VP_ERR_NULL (items), VP_ERR_ARG (n_items < 1), VP_ERR_DIMS,
+ * VP_ERR_FRAMES, VP_ERR_INDEX (validated as vp_preprocess_batch does),
+ * VP_ERR_CAPACITY (more than INT32_MAX rows).
+ */
+int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw,
+                        int32_t* cu_seqlens, int64_t* total_rows, int64_t* workspace_bytes);
+
+/*
+ * Preprocess a batch on the GPU: for every item, every sampled frame is
+ * resampled from (src_h, src_w) to (dst_h, dst_w) with the filter of
+ * vp_filter_table along x then y (no clamping, no rounding in between),
+ * normalised as v = (R/255 - mean_c)/std_c, padded to an even frame count,
+ * and written as merge-window rows:
+ *   row cu[b] + ((tt*(h/32) + bh)*(w/32) + bw)*4 + mh*2 + mw,
+ *   column ((c*2 + dt)*16 + y)*16 + x  holds
+ *   v[frame 2*tt + dt][c][16*(2*bh + mh) + y][16*(2*bw + mw) + x].
+ *
+ * mean, std: HOST float[3] (std > 0, finite).
+ * out_dtype: VP_OUT_F32 or VP_OUT_BF16 (round to nearest even).
+ * out_rows: DEVICE [out_rows_capacity][1536] of out_dtype, row-major,
+ *   16-byte aligned.
+ * grid_thw, cu_seqlens: HOST outputs as in vp_batch_layout (may be NULL);
+ *   final when the call returns.
+ * workspace: DEVICE, >= the workspace_bytes of vp_batch_layout, 256-byte
+ *   aligned; the call copies its plan (item table, filter tables, indices)
+ *   there on `stream` and the kernels read it.  It may be reused by the
+ *   next call on the same stream.
+ * stream: the HIP stream all work is enqueued on (0 = the null stream).
+ * out_rows is final when `stream` reaches the end of the enqueued work.
+ * Errors: VP_ERR_NULL, VP_ERR_ARG (n_items < 1, bad dtype, std <= 0 or not
+ * finite, misaligned pointers), VP_ERR_DIMS, VP_ERR_FRAMES, VP_ERR_INDEX,
+ * VP_ERR_CAPACITY (out_rows_capacity < total rows, workspace too small, a
+ * frame of 4 GiB or more, a filter window too long for the kernels),
+ * VP_ERR_HIP.
+ */
+int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* mean,
+                            const float* std, int32_t out_dtype, void* out_rows,
+                            int64_t out_rows_capacity, int32_t* grid_thw, int32_t* cu_seqlens,
+                            void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* Static name of a status code ("VP_OK", "VP_ERR_ARG", ...). */
+const char* vp_status_string(int32_t status);
+
+/* Thread-local detail of the last non-OK status on this thread ("" if none). */
+const char* vp_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VP_H */

@@ -1,0 +1,244 @@
+"""MI355X-native video-frame preprocessing for Qwen-VL-style vision inputs.
+
+Python binding of ``libvp.so`` (C ABI in ``include/vp.h``): the per-frame
+preprocessing that EasyVideoR1 (arXiv 2604.16893, Section 3.1.1) caches
+offline -- frame-index sampling, smart_resize, antialiased bicubic
+resampling, normalisation and merge-window patchification with grid_thw and
+cu_seqlens -- runs in hand-written gfx950 HIP kernels.  This module only
+marshals arguments: torch provides device memory and the current stream.
+
+Importing never compiles anything; build with
+``python -m paper_2604_16893_amd.build``.  Every entry point raises
+``VPError`` when the native library is missing -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvp.so")
+
+VP_OK, VP_ERR_NULL, VP_ERR_ARG, VP_ERR_ASPECT, VP_ERR_DIMS, VP_ERR_INDEX, VP_ERR_FRAMES, \
+    VP_ERR_CAPACITY, VP_ERR_HIP = range(9)
+VP_SAMPLE_UNIFORM, VP_SAMPLE_FPS = 0, 1
+VP_OUT_F32, VP_OUT_BF16 = 0, 1
+VP_ROW = 1536
+VP_FACTOR = 32
+
+EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
+            "vp_batch_layout", "vp_preprocess_batch", "vp_status_string",
+            "vp_last_error_message")
+
+
+class VPError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+class vp_item(ctypes.Structure):
+    _fields_ = [("frames", ctypes.c_void_p),
+                ("indices", ctypes.POINTER(ctypes.c_int32)),
+                ("n_src", ctypes.c_int32),
+                ("src_h", ctypes.c_int32),
+                ("src_w", ctypes.c_int32),
+                ("n_idx", ctypes.c_int32),
+                ("dst_h", ctypes.c_int32),
+                ("dst_w", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded native library; raises VPError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise VPError(-1, f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2604_16893_amd.build` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        i32p, i64p, f32p = ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_float)
+        itemp = ctypes.POINTER(vp_item)
+        L.vp_smart_resize_dims.argtypes = [i32, i32, i32, i64, i64, i32p, i32p]
+        L.vp_sample_indices.argtypes = [i32, i32, i32, f64, f64, i32, i32, i32p, i32, i32p]
+        L.vp_filter_taps.argtypes = [i32, i32, i32p]
+        L.vp_filter_table.argtypes = [i32, i32, i32, i32p, i32p, f32p]
+        L.vp_batch_layout.argtypes = [itemp, i32, i32p, i32p, i64p, i64p]
+        L.vp_preprocess_batch.argtypes = [itemp, i32, f32p, f32p, i32, ctypes.c_void_p, i64,
+                                          i32p, i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
+        L.vp_status_string.argtypes = [i32]
+        L.vp_status_string.restype = ctypes.c_char_p
+        L.vp_last_error_message.argtypes = []
+        L.vp_last_error_message.restype = ctypes.c_char_p
+        for name in EXPORTED:
+            getattr(L, name).restype = getattr(L, name).restype if name in (
+                "vp_status_string", "vp_last_error_message") else i32
+        _lib = L
+    return _lib
+
+
+def _check(status: int, what: str):
+    if status != VP_OK:
+        L = lib()
+        raise VPError(status, f"{what}: {L.vp_status_string(status).decode()}: "
+                              f"{L.vp_last_error_message().decode()}")
+
+
+def _ptr(a: np.ndarray, ct):
+    return a.ctypes.data_as(ctypes.POINTER(ct))
+
+
+# --------------------------------------------------------------------------
+# Host entry points (same names as the C ABI)
+# --------------------------------------------------------------------------
+
+def vp_smart_resize_dims(height: int, width: int, factor: int = VP_FACTOR, min_pixels: int = 0,
+                         max_pixels: int = (1 << 62)) -> tuple[int, int]:
+    h, w = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().vp_smart_resize_dims(height, width, factor, min_pixels, max_pixels,
+                                      ctypes.byref(h), ctypes.byref(w)), "vp_smart_resize_dims")
+    return h.value, w.value
+
+
+def vp_sample_indices(total_frames: int, mode: int = VP_SAMPLE_UNIFORM, nframes: int = 0,
+                      video_fps: float = 0.0, fps: float = 0.0, min_frames: int = 1,
+                      max_frames: int = 1 << 30) -> np.ndarray:
+    cnt = ctypes.c_int32()
+    st = lib().vp_sample_indices(total_frames, mode, nframes, video_fps, fps, min_frames,
+                                 max_frames, None, 0, ctypes.byref(cnt))
+    if st != VP_ERR_CAPACITY:
+        _check(st, "vp_sample_indices")
+    out = np.zeros(max(cnt.value, 1), np.int32)
+    _check(lib().vp_sample_indices(total_frames, mode, nframes, video_fps, fps, min_frames,
+                                   max_frames, _ptr(out, ctypes.c_int32), len(out),
+                                   ctypes.byref(cnt)), "vp_sample_indices")
+    return out[:cnt.value]
+
+
+def vp_filter_taps(n_in: int, n_out: int) -> int:
+    k = ctypes.c_int32()
+    _check(lib().vp_filter_taps(n_in, n_out, ctypes.byref(k)), "vp_filter_taps")
+    return k.value
+
+
+def vp_filter_table(n_in: int, n_out: int, taps: Optional[int] = None):
+    """(start[n_out], count[n_out], weights[n_out][taps]) of one axis."""
+    taps = vp_filter_taps(n_in, n_out) if taps is None else taps
+    start = np.zeros(n_out, np.int32)
+    count = np.zeros(n_out, np.int32)
+    w = np.zeros((n_out, taps), np.float32)
+    _check(lib().vp_filter_table(n_in, n_out, taps, _ptr(start, ctypes.c_int32),
+                                 _ptr(count, ctypes.c_int32), _ptr(w, ctypes.c_float)),
+           "vp_filter_table")
+    return start, count, w
+
+
+# --------------------------------------------------------------------------
+# Batches
+# --------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Item:
+    """One video or image: device frames [n_src, H, W, 3] uint8, sampled
+    indices, and the target size (multiples of 32)."""
+    frames: object
+    indices: Sequence[int]
+    dst_h: int
+    dst_w: int
+
+
+class _Batch:
+    """ctypes view of a list of Items; keeps the host index arrays alive."""
+
+    def __init__(self, items: Sequence):
+        self.idx = []
+        self.arr = (vp_item * len(items))()
+        for k, it in enumerate(items):
+            fr = it.frames
+            if hasattr(fr, "data_ptr"):
+                if fr.dtype.__repr__() != "torch.uint8" or fr.dim() != 4 or fr.shape[3] != 3 \
+                        or not fr.is_contiguous():
+                    raise VPError(VP_ERR_ARG, f"item {k}: frames must be a contiguous uint8 "
+                                              "[n_src, H, W, 3] tensor")
+                ptr, (n_src, H, W, _) = fr.data_ptr(), tuple(fr.shape)
+            else:   # (device pointer, n_src, H, W) -- layout-only callers
+                ptr, n_src, H, W = fr
+            idx = np.ascontiguousarray(np.asarray(it.indices, dtype=np.int32).reshape(-1))
+            self.idx.append(idx)
+            self.arr[k] = vp_item(ptr, _ptr(idx, ctypes.c_int32), n_src, H, W, len(idx),
+                                  it.dst_h, it.dst_w)
+
+    def __len__(self):
+        return len(self.arr)
+
+
+def vp_batch_layout(items: Sequence):
+    """(grid_thw int32 [B,3], cu_seqlens int32 [B+1], total_rows, workspace_bytes)."""
+    b = _Batch(items)
+    B = len(b)
+    grid = np.zeros((B, 3), np.int32)
+    cu = np.zeros(B + 1, np.int32)
+    rows, ws = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().vp_batch_layout(b.arr, B, _ptr(grid, ctypes.c_int32), _ptr(cu, ctypes.c_int32),
+                                 ctypes.byref(rows), ctypes.byref(ws)), "vp_batch_layout")
+    return grid, cu, rows.value, ws.value
+
+
+def _stream_handle(stream) -> int:
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def vp_preprocess_batch(items: Sequence, mean, std, out_dtype: int, out_rows, workspace,
+                        stream=None):
+    """Enqueue the batch on `stream` (torch stream, raw handle, or None for the
+    current stream).  out_rows: device tensor [>= rows, 1536] of float32 or
+    bfloat16 matching out_dtype; workspace: device uint8 tensor of at least
+    the layout's workspace_bytes.  Returns (grid_thw, cu_seqlens)."""
+    import torch
+    want = torch.bfloat16 if out_dtype == VP_OUT_BF16 else torch.float32
+    if out_rows.dtype != want or out_rows.dim() != 2 or out_rows.shape[1] != VP_ROW \
+            or not out_rows.is_contiguous() or not out_rows.is_cuda:
+        raise VPError(VP_ERR_ARG, f"out_rows must be a contiguous CUDA [rows, {VP_ROW}] {want} tensor")
+    if not workspace.is_cuda or not workspace.is_contiguous():
+        raise VPError(VP_ERR_ARG, "workspace must be a contiguous CUDA tensor")
+    b = _Batch(items)
+    B = len(b)
+    m = np.ascontiguousarray(np.asarray(mean, np.float32).reshape(3))
+    s = np.ascontiguousarray(np.asarray(std, np.float32).reshape(3))
+    grid = np.zeros((B, 3), np.int32)
+    cu = np.zeros(B + 1, np.int32)
+    _check(lib().vp_preprocess_batch(
+        b.arr, B, _ptr(m, ctypes.c_float), _ptr(s, ctypes.c_float), out_dtype,
+        ctypes.c_void_p(out_rows.data_ptr()), out_rows.shape[0], _ptr(grid, ctypes.c_int32),
+        _ptr(cu, ctypes.c_int32), ctypes.c_void_p(workspace.data_ptr()),
+        workspace.numel() * workspace.element_size(), ctypes.c_void_p(_stream_handle(stream))),
+        "vp_preprocess_batch")
+    return grid, cu
+
+
+def preprocess(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None):
+    """Allocate the outputs with torch and run vp_preprocess_batch.
+
+    Returns (rows [total_rows, 1536] on the frames' device, grid_thw int32
+    [B, 3], cu_seqlens int32 [B+1]); rows are final when the stream is."""
+    import torch
+    code = VP_OUT_BF16 if out_dtype in ("bf16", VP_OUT_BF16) else VP_OUT_F32
+    grid, cu, rows, ws = vp_batch_layout(items)
+    dev = items[0].frames.device
+    out = torch.empty((rows, VP_ROW), dtype=torch.bfloat16 if code == VP_OUT_BF16 else torch.float32,
+                      device=dev)
+    work = torch.empty(ws, dtype=torch.uint8, device=dev)
+    vp_preprocess_batch(items, mean, std, code, out, work, stream)
+    return out, grid, cu

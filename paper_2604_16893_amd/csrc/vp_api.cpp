@@ -1,0 +1,499 @@
+// vp_api.cpp -- host side of the C ABI declared in include/vp.h.
+//
+// Host work per call: validate the items, derive grid_thw / cu_seqlens,
+// build the per-axis filter tables (double precision, rounded once to
+// float), pack the plan into one blob in pinned host memory, copy it into
+// the caller's workspace on the caller's stream, and launch the kernels.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "vp.h"
+#include "vp_plan.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int32_t fail(int32_t status, const std::string& msg) {
+    g_last_error = msg;
+    return status;
+}
+
+// ---------------------------------------------------------------------------
+// smart_resize and frame-index sampling
+// ---------------------------------------------------------------------------
+
+// Nearest integer of a double, ties to the even neighbour.
+double nearest_even(double v) {
+    const double lower = std::floor(v);
+    const double frac = v - lower;  // exact for |v| < 2^52
+    if (frac != 0.5) return frac < 0.5 ? lower : lower + 1.0;
+    return std::fmod(lower, 2.0) == 0.0 ? lower : lower + 1.0;
+}
+
+// Index i of n spread evenly over [0, last], rounded half to even on the
+// exact rational i * last / (n - 1).
+int32_t spread_index(int64_t i, int64_t last, int64_t n) {
+    if (n == 1) return 0;
+    const int64_t num = i * last, den = n - 1;
+    int64_t whole = num / den;
+    const int64_t twice_rem = 2 * (num - whole * den);
+    if (twice_rem > den || (twice_rem == den && (whole & 1))) ++whole;
+    return static_cast<int32_t>(whole);
+}
+
+// ---------------------------------------------------------------------------
+// Antialiased bicubic filter tables
+// ---------------------------------------------------------------------------
+
+struct AxisFilter {
+    int32_t n_in = 0, n_out = 0, taps = 0;
+    std::vector<int32_t> start, count;
+    std::vector<float> weight;  // [n_out][taps]
+};
+
+double cubic_a_half(double x) {  // Keys (1981) kernel, a = -1/2
+    const double t = std::fabs(x);
+    if (t >= 2.0) return 0.0;
+    if (t >= 1.0) return ((-0.5 * t + 2.5) * t - 4.0) * t + 2.0;
+    return (1.5 * t - 2.5) * t * t + 1.0;
+}
+
+// Window [lo, hi) of output i; the same double expressions as the documented
+// definition, in the same order, so that window bounds are reproducible.
+void window(int32_t n_in, int32_t n_out, int32_t i, double* centre, double* sigma, int32_t* lo,
+            int32_t* hi) {
+    const double scale = static_cast<double>(n_in) / static_cast<double>(n_out);
+    const double s = scale > 1.0 ? scale : 1.0;
+    const double support = 2.0 * s;
+    const double c = (static_cast<double>(i) + 0.5) * scale;
+    double a = std::floor(c - support + 0.5);
+    double b = std::floor(c + support + 0.5);
+    if (a < 0.0) a = 0.0;
+    if (b > n_in) b = n_in;
+    *centre = c;
+    *sigma = s;
+    *lo = static_cast<int32_t>(a);
+    *hi = static_cast<int32_t>(b);
+}
+
+int32_t axis_taps(int32_t n_in, int32_t n_out) {
+    int32_t best = 0;
+    for (int32_t i = 0; i < n_out; ++i) {
+        double c, s;
+        int32_t lo, hi;
+        window(n_in, n_out, i, &c, &s, &lo, &hi);
+        if (hi - lo > best) best = hi - lo;
+    }
+    return best;
+}
+
+void build_axis(int32_t n_in, int32_t n_out, int32_t taps, AxisFilter* f) {
+    f->n_in = n_in;
+    f->n_out = n_out;
+    f->taps = taps;
+    f->start.assign(n_out, 0);
+    f->count.assign(n_out, 0);
+    f->weight.assign(static_cast<size_t>(n_out) * taps, 0.0f);
+    std::vector<double> raw(taps);
+    for (int32_t i = 0; i < n_out; ++i) {
+        double c, s;
+        int32_t lo, hi;
+        window(n_in, n_out, i, &c, &s, &lo, &hi);
+        double sum = 0.0;
+        for (int32_t j = lo; j < hi; ++j) {
+            raw[j - lo] = cubic_a_half((static_cast<double>(j) + 0.5 - c) / s);
+            sum += raw[j - lo];
+        }
+        f->start[i] = lo;
+        f->count[i] = hi - lo;
+        for (int32_t j = lo; j < hi; ++j)
+            f->weight[static_cast<size_t>(i) * taps + (j - lo)] = static_cast<float>(raw[j - lo] / sum);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Plan
+// ---------------------------------------------------------------------------
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Plan {
+    std::vector<vp::DevItem> items;
+    std::vector<int32_t> prefix;
+    std::vector<int32_t> indices;
+    std::vector<int32_t> tables;
+    std::vector<int32_t> grid;  // [n][3]
+    std::vector<int32_t> cu;    // [n + 1]
+    int64_t total_rows = 0;
+    size_t off_items = 0, off_prefix = 0, off_indices = 0, off_tables = 0, bytes = 0;
+};
+
+int32_t validate_item(const vp_item& it, int32_t b) {
+    const std::string at = "item " + std::to_string(b) + ": ";
+    if (it.frames == nullptr) return fail(VP_ERR_NULL, at + "frames is NULL");
+    if (it.indices == nullptr) return fail(VP_ERR_NULL, at + "indices is NULL");
+    if (it.n_src < 1) return fail(VP_ERR_FRAMES, at + "n_src < 1");
+    if (it.src_h < 1 || it.src_w < 1) return fail(VP_ERR_DIMS, at + "source size < 1");
+    if (it.n_idx < 1) return fail(VP_ERR_FRAMES, at + "n_idx < 1");
+    if (it.dst_h < vp::kWin || it.dst_w < vp::kWin || it.dst_h % vp::kWin || it.dst_w % vp::kWin)
+        return fail(VP_ERR_DIMS, at + "target size not a positive multiple of 32");
+    for (int32_t k = 0; k < it.n_idx; ++k)
+        if (it.indices[k] < 0 || it.indices[k] >= it.n_src)
+            return fail(VP_ERR_INDEX, at + "index " + std::to_string(it.indices[k]) +
+                                          " outside [0, " + std::to_string(it.n_src) + ")");
+    const int64_t fb = int64_t(it.src_h) * it.src_w * 3;
+    if (fb >= (int64_t(1) << 32)) return fail(VP_ERR_CAPACITY, at + "a source frame of 4 GiB or more");
+    return VP_OK;
+}
+
+// Largest generic sub-tile (rh x cw output pixels) whose y-resampled column
+// tile fits the kernel's LDS buffer for every merge window of the item.
+bool generic_subtile(const AxisFilter& fx, int32_t* rh, int32_t* cw) {
+    for (int32_t r = 32; r >= 1; r /= 2) {
+        for (int32_t c = 32; c >= 1; c /= 2) {
+            int32_t worst = 0;
+            for (int32_t j0 = 0; j0 < fx.n_out; j0 += c) {
+                const int32_t span = fx.start[j0 + c - 1] + fx.count[j0 + c - 1] - fx.start[j0];
+                if (span > worst) worst = span;
+            }
+            if (int64_t(r) * worst * 3 <= vp::kGenericTCap) {
+                *rh = r;
+                *cw = c;
+                return true;
+            }
+        }
+    }
+    return false;
+}
+
+int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
+    if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
+    if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    p->items.assign(n, vp::DevItem{});
+    p->prefix.assign(n + 1, 0);
+    p->grid.assign(size_t(n) * 3, 0);
+    p->cu.assign(n + 1, 0);
+    p->indices.clear();
+    p->tables.clear();
+    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, AxisFilter>> axes;  // -> (word offset, filter)
+    auto table_for = [&](int32_t n_in, int32_t n_out, int32_t* off) -> const AxisFilter* {
+        auto key = std::make_pair(n_in, n_out);
+        auto found = axes.find(key);
+        if (found == axes.end()) {
+            AxisFilter f;
+            build_axis(n_in, n_out, axis_taps(n_in, n_out), &f);
+            const int32_t o = static_cast<int32_t>(p->tables.size());
+            p->tables.insert(p->tables.end(), f.start.begin(), f.start.end());
+            p->tables.insert(p->tables.end(), f.count.begin(), f.count.end());
+            const size_t wbase = p->tables.size();
+            p->tables.resize(wbase + f.weight.size());
+            std::memcpy(p->tables.data() + wbase, f.weight.data(), f.weight.size() * sizeof(float));
+            found = axes.emplace(key, std::make_pair(o, std::move(f))).first;
+        }
+        *off = found->second.first;
+        return &found->second.second;
+    };
+
+    int64_t rows = 0, tiles = 0;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp_item& it = items[b];
+        int32_t st = validate_item(it, b);
+        if (st != VP_OK) return st;
+        vp::DevItem& d = p->items[b];
+        d.frames = it.frames;
+        d.frame_bytes = int64_t(it.src_h) * it.src_w * 3;
+        d.H = it.src_h;
+        d.W = it.src_w;
+        d.h = it.dst_h;
+        d.w = it.dst_w;
+        d.t = (it.n_idx + 1) / 2;
+        d.hm = it.dst_h / vp::kWin;
+        d.wm = it.dst_w / vp::kWin;
+        d.idx_off = static_cast<int32_t>(p->indices.size());
+        for (int32_t k = 0; k < 2 * d.t; ++k)
+            p->indices.push_back(it.indices[k < it.n_idx ? k : it.n_idx - 1]);
+        const AxisFilter* fy = table_for(it.src_h, it.dst_h, &d.ty_off);
+        const AxisFilter* fx = table_for(it.src_w, it.dst_w, &d.tx_off);
+        d.ky = fy->taps;
+        d.kx = fx->taps;
+        if (!generic_subtile(*fx, &d.rh, &d.cw))
+            return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
+                                             ": horizontal filter window too long (downscale too large)");
+        d.route = vp::kRouteGeneric;
+        d.row_off = rows;
+        const int64_t item_rows = int64_t(d.t) * (it.dst_h / vp::kPatch) * (it.dst_w / vp::kPatch);
+        p->grid[3 * b + 0] = d.t;
+        p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
+        p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
+        rows += item_rows;
+        tiles += int64_t(d.t) * d.hm * d.wm;
+        if (rows > INT32_MAX || tiles > INT32_MAX)
+            return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 rows");
+        p->cu[b + 1] = static_cast<int32_t>(rows);
+        p->prefix[b + 1] = static_cast<int32_t>(tiles);
+    }
+    p->total_rows = rows;
+    p->off_items = 0;
+    p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
+    p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
+    p->off_tables = align_up(p->off_indices + sizeof(int32_t) * p->indices.size());
+    p->bytes = align_up(p->off_tables + sizeof(int32_t) * p->tables.size());
+    return VP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Pinned staging ring: the plan blob is written into pinned host memory and
+// copied asynchronously; a slot is reused only after the copy that read it
+// has completed.
+// ---------------------------------------------------------------------------
+
+struct Slot {
+    void* host = nullptr;
+    size_t cap = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+
+struct Ring {
+    std::mutex mu;
+    Slot slots[4];
+    int next = 0;
+};
+
+std::mutex g_rings_mu;
+std::map<int, Ring*> g_rings;
+
+Ring* ring_for_device(int dev) {
+    std::lock_guard<std::mutex> lk(g_rings_mu);
+    Ring*& r = g_rings[dev];
+    if (r == nullptr) r = new Ring();  // lives until process exit
+    return r;
+}
+
+int32_t hip_fail(hipError_t e, const char* what) {
+    return fail(VP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+int32_t upload_plan(const Plan& p, void* workspace, hipStream_t stream) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    Ring* ring = ring_for_device(dev);
+    std::lock_guard<std::mutex> lk(ring->mu);
+    Slot& s = ring->slots[ring->next];
+    ring->next = (ring->next + 1) % 4;
+    if (s.pending) {
+        e = hipEventSynchronize(s.done);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+        s.pending = false;
+    }
+    if (s.done == nullptr) {
+        e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    }
+    if (s.cap < p.bytes) {
+        if (s.host != nullptr) (void)hipHostFree(s.host);
+        s.host = nullptr;
+        s.cap = 0;
+        size_t cap = align_up(p.bytes * 2);
+        e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+        if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
+        s.cap = cap;
+    }
+    auto* base = static_cast<uint8_t*>(s.host);
+    std::memset(base, 0, p.bytes);
+    std::memcpy(base + p.off_items, p.items.data(), sizeof(vp::DevItem) * p.items.size());
+    std::memcpy(base + p.off_prefix, p.prefix.data(), sizeof(int32_t) * p.prefix.size());
+    std::memcpy(base + p.off_indices, p.indices.data(), sizeof(int32_t) * p.indices.size());
+    std::memcpy(base + p.off_tables, p.tables.data(), sizeof(int32_t) * p.tables.size());
+    e = hipMemcpyAsync(workspace, s.host, p.bytes, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+    e = hipEventRecord(s.done, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    s.pending = true;
+    return VP_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+
+extern "C" {
+
+int32_t vp_smart_resize_dims(int32_t height, int32_t width, int32_t factor, int64_t min_pixels,
+                             int64_t max_pixels, int32_t* out_h, int32_t* out_w) {
+    if (out_h == nullptr || out_w == nullptr) return fail(VP_ERR_NULL, "output pointer is NULL");
+    if (height <= 0 || width <= 0 || factor <= 0 || max_pixels <= 0 || min_pixels < 0 ||
+        min_pixels > max_pixels)
+        return fail(VP_ERR_ARG, "smart_resize: sizes, factor and max_pixels must be positive, "
+                                "0 <= min_pixels <= max_pixels");
+    const double H = height, W = width, F = factor;
+    const double ratio = height > width ? H / W : W / H;
+    if (ratio > 200.0) return fail(VP_ERR_ASPECT, "smart_resize: aspect ratio above 200");
+    int64_t h = static_cast<int64_t>(nearest_even(H / F)) * factor;
+    int64_t w = static_cast<int64_t>(nearest_even(W / F)) * factor;
+    if (h < factor) h = factor;
+    if (w < factor) w = factor;
+    if (h * w > max_pixels) {
+        const double beta = std::sqrt(static_cast<double>(int64_t(height) * width) /
+                                      static_cast<double>(max_pixels));
+        h = static_cast<int64_t>(std::floor(H / beta / F)) * factor;
+        w = static_cast<int64_t>(std::floor(W / beta / F)) * factor;
+        if (h < factor) h = factor;
+        if (w < factor) w = factor;
+    } else if (h * w < min_pixels) {
+        const double beta = std::sqrt(static_cast<double>(min_pixels) /
+                                      static_cast<double>(int64_t(height) * width));
+        h = static_cast<int64_t>(std::ceil(H * beta / F)) * factor;
+        w = static_cast<int64_t>(std::ceil(W * beta / F)) * factor;
+    }
+    if (h > INT32_MAX || w > INT32_MAX) return fail(VP_ERR_DIMS, "smart_resize: result too large");
+    *out_h = static_cast<int32_t>(h);
+    *out_w = static_cast<int32_t>(w);
+    return VP_OK;
+}
+
+int32_t vp_sample_indices(int32_t total_frames, int32_t mode, int32_t nframes, double video_fps,
+                          double fps, int32_t min_frames, int32_t max_frames, int32_t* out_idx,
+                          int32_t capacity, int32_t* out_count) {
+    if (out_count == nullptr) return fail(VP_ERR_NULL, "out_count is NULL");
+    if (total_frames < 1) return fail(VP_ERR_FRAMES, "total_frames < 1");
+    int64_t n = 0;
+    if (mode == VP_SAMPLE_UNIFORM) {
+        if (nframes < 1 || nframes > total_frames)
+            return fail(VP_ERR_FRAMES, "uniform sampling needs 1 <= nframes <= total_frames");
+        n = nframes;
+    } else if (mode == VP_SAMPLE_FPS) {
+        if (!(video_fps > 0.0) || !(fps > 0.0) || min_frames < 1 || max_frames < min_frames)
+            return fail(VP_ERR_ARG, "fps sampling needs video_fps, fps > 0 and "
+                                    "1 <= min_frames <= max_frames");
+        const double lo = static_cast<double>((int64_t(min_frames) + 1) / 2 * 2);
+        const double hi = static_cast<double>(int64_t(max_frames) / 2 * 2);
+        double want = static_cast<double>(total_frames) / video_fps * fps;
+        want = want < lo ? lo : want;
+        want = want > hi ? hi : want;
+        want = want > total_frames ? static_cast<double>(total_frames) : want;
+        n = static_cast<int64_t>(std::floor(want / 2.0)) * 2;
+        if (n < 2) return fail(VP_ERR_FRAMES, "fps sampling yields fewer than 2 frames");
+    } else {
+        return fail(VP_ERR_ARG, "unknown sampling mode");
+    }
+    *out_count = static_cast<int32_t>(n);
+    if (out_idx == nullptr || capacity < n)
+        return fail(VP_ERR_CAPACITY, "index buffer holds " + std::to_string(capacity) + " of " +
+                                         std::to_string(n) + " indices");
+    for (int64_t i = 0; i < n; ++i) out_idx[i] = spread_index(i, total_frames - 1, n);
+    return VP_OK;
+}
+
+int32_t vp_filter_taps(int32_t n_in, int32_t n_out, int32_t* max_taps) {
+    if (max_taps == nullptr) return fail(VP_ERR_NULL, "max_taps is NULL");
+    if (n_in < 1 || n_out < 1) return fail(VP_ERR_ARG, "n_in and n_out must be >= 1");
+    *max_taps = axis_taps(n_in, n_out);
+    return VP_OK;
+}
+
+int32_t vp_filter_table(int32_t n_in, int32_t n_out, int32_t taps, int32_t* start, int32_t* count,
+                        float* weights) {
+    if (start == nullptr || count == nullptr || weights == nullptr)
+        return fail(VP_ERR_NULL, "output pointer is NULL");
+    if (n_in < 1 || n_out < 1) return fail(VP_ERR_ARG, "n_in and n_out must be >= 1");
+    const int32_t need = axis_taps(n_in, n_out);
+    if (taps < need) return fail(VP_ERR_CAPACITY, "taps below the longest window");
+    AxisFilter f;
+    build_axis(n_in, n_out, taps, &f);
+    std::memcpy(start, f.start.data(), sizeof(int32_t) * n_out);
+    std::memcpy(count, f.count.data(), sizeof(int32_t) * n_out);
+    std::memcpy(weights, f.weight.data(), sizeof(float) * f.weight.size());
+    return VP_OK;
+}
+
+int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw,
+                        int32_t* cu_seqlens, int64_t* total_rows, int64_t* workspace_bytes) {
+    Plan p;
+    const int32_t st = build_plan(items, n_items, &p);
+    if (st != VP_OK) return st;
+    if (grid_thw) std::memcpy(grid_thw, p.grid.data(), sizeof(int32_t) * p.grid.size());
+    if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
+    if (total_rows) *total_rows = p.total_rows;
+    if (workspace_bytes) *workspace_bytes = static_cast<int64_t>(p.bytes);
+    return VP_OK;
+}
+
+int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* mean,
+                            const float* std, int32_t out_dtype, void* out_rows,
+                            int64_t out_rows_capacity, int32_t* grid_thw, int32_t* cu_seqlens,
+                            void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+    if (mean == nullptr || std == nullptr || out_rows == nullptr || workspace == nullptr)
+        return fail(VP_ERR_NULL, "mean, std, out_rows and workspace must be non-NULL");
+    if (out_dtype != VP_OUT_F32 && out_dtype != VP_OUT_BF16)
+        return fail(VP_ERR_ARG, "out_dtype must be VP_OUT_F32 or VP_OUT_BF16");
+    if (reinterpret_cast<uintptr_t>(out_rows) % 16 != 0)
+        return fail(VP_ERR_ARG, "out_rows must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+        return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
+    vp::Norm norm;
+    for (int c = 0; c < 3; ++c) {
+        if (!(std[c] > 0.0f) || !std::isfinite(std[c]) || !std::isfinite(mean[c]))
+            return fail(VP_ERR_ARG, "std must be positive and finite, mean finite");
+        norm.a[c] = static_cast<float>(1.0 / (255.0 * static_cast<double>(std[c])));
+        norm.b[c] = static_cast<float>(-static_cast<double>(mean[c]) / static_cast<double>(std[c]));
+    }
+    Plan p;
+    int32_t st = build_plan(items, n_items, &p);
+    if (st != VP_OK) return st;
+    if (out_rows_capacity < p.total_rows)
+        return fail(VP_ERR_CAPACITY, "out_rows holds " + std::to_string(out_rows_capacity) +
+                                         " rows, batch needs " + std::to_string(p.total_rows));
+    if (workspace_bytes < static_cast<int64_t>(p.bytes))
+        return fail(VP_ERR_CAPACITY, "workspace holds " + std::to_string(workspace_bytes) +
+                                         " bytes, plan needs " + std::to_string(p.bytes));
+    st = upload_plan(p, workspace, stream);
+    if (st != VP_OK) return st;
+    auto* ws = static_cast<uint8_t*>(workspace);
+    vp::PlanView view;
+    view.items = reinterpret_cast<const vp::DevItem*>(ws + p.off_items);
+    view.tile_prefix = reinterpret_cast<const int32_t*>(ws + p.off_prefix);
+    view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
+    view.tables = reinterpret_cast<const int32_t*>(ws + p.off_tables);
+    view.n_items = n_items;
+    view.n_tiles = p.prefix[n_items];
+    const int err = vp::launch_generic(view, out_rows, out_dtype, norm, stream);
+    if (err != 0)
+        return hip_fail(static_cast<hipError_t>(err), "kernel launch");
+    if (grid_thw) std::memcpy(grid_thw, p.grid.data(), sizeof(int32_t) * p.grid.size());
+    if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
+    g_last_error.clear();
+    return VP_OK;
+}
+
+const char* vp_status_string(int32_t status) {
+    switch (status) {
+        case VP_OK: return "VP_OK";
+        case VP_ERR_NULL: return "VP_ERR_NULL";
+        case VP_ERR_ARG: return "VP_ERR_ARG";
+        case VP_ERR_ASPECT: return "VP_ERR_ASPECT";
+        case VP_ERR_DIMS: return "VP_ERR_DIMS";
+        case VP_ERR_INDEX: return "VP_ERR_INDEX";
+        case VP_ERR_FRAMES: return "VP_ERR_FRAMES";
+        case VP_ERR_CAPACITY: return "VP_ERR_CAPACITY";
+        case VP_ERR_HIP: return "VP_ERR_HIP";
+        default: return "VP_ERR_UNKNOWN";
+    }
+}
+
+const char* vp_last_error_message(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,203 @@
+"""CPU tests of the native library's host side: symbol exports, the host
+planning functions bit-exact against the oracle, and every error path
+(validation happens on the host before anything is enqueued, so no GPU is
+needed)."""
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2604_16893_amd as vp
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_function():
+    header = open(os.path.join(ROOT, "include", "vp.h")).read()
+    declared = set(re.findall(r"^\s*(?:int32_t|const char\*)\s+(vp_\w+)\s*\(", header, re.M))
+    assert declared == set(vp.EXPORTED)
+    L = ctypes.CDLL(vp.LIB_PATH)
+    for name in declared:
+        assert hasattr(L, name), name
+    assert vp.lib().vp_status_string(vp.VP_ERR_CAPACITY) == b"VP_ERR_CAPACITY"
+
+
+def test_smart_resize_bit_exact_vs_oracle():
+    rng = np.random.default_rng(31)
+    for _ in range(5000):
+        H = int(rng.integers(1, 6000))
+        W = int(rng.integers(1, 6000))
+        B = int(rng.integers(1024, 9_000_000))
+        mn = int(rng.integers(0, 2)) * int(rng.integers(0, B))
+        try:
+            want = oracle.smart_resize(H, W, 32, mn, B)
+        except oracle.OracleError as e:
+            with pytest.raises(vp.VPError) as got:
+                vp.vp_smart_resize_dims(H, W, 32, mn, B)
+            assert got.value.status == e.code
+            continue
+        assert vp.vp_smart_resize_dims(H, W, 32, mn, B) == want, (H, W, mn, B)
+
+
+def test_sample_indices_bit_exact_vs_oracle():
+    for N in range(1, 70):
+        for n in range(1, N + 1):
+            assert vp.vp_sample_indices(N, vp.VP_SAMPLE_UNIFORM, n).tolist() == \
+                oracle.sample_uniform(N, n).tolist()
+    rng = np.random.default_rng(32)
+    for _ in range(2000):
+        N = int(rng.integers(1, 20000))
+        vf = float(rng.choice([23.976, 24.0, 25.0, 29.97, 30.0, 50.0, 60.0, 8.0, 1.0]))
+        fps = float(rng.choice([0.5, 1.0, 2.0, 3.0, 4.0]))
+        mn = int(rng.integers(1, 16))
+        mx = int(rng.integers(mn, 800))
+        try:
+            want = oracle.sample_fps(N, vf, fps, mn, mx)
+        except oracle.OracleError as e:
+            with pytest.raises(vp.VPError) as got:
+                vp.vp_sample_indices(N, vp.VP_SAMPLE_FPS, 0, vf, fps, mn, mx)
+            assert got.value.status == e.code
+            continue
+        assert vp.vp_sample_indices(N, vp.VP_SAMPLE_FPS, 0, vf, fps, mn, mx).tolist() == \
+            want.tolist()
+
+
+def test_sample_indices_capacity_reports_count():
+    L = vp.lib()
+    cnt = ctypes.c_int32()
+    out = (ctypes.c_int32 * 3)()
+    st = L.vp_sample_indices(256, vp.VP_SAMPLE_FPS, 0, 8.0, 2.0, 4, 128, out, 3, ctypes.byref(cnt))
+    assert st == vp.VP_ERR_CAPACITY and cnt.value == 64
+    assert L.vp_sample_indices(10, 7, 3, 0, 0, 1, 1, out, 3, ctypes.byref(cnt)) == vp.VP_ERR_ARG
+    assert L.vp_sample_indices(10, 0, 11, 0, 0, 1, 1, out, 3, ctypes.byref(cnt)) == vp.VP_ERR_FRAMES
+    assert L.vp_sample_indices(10, 0, 3, 0, 0, 1, 1, out, 3, None) == vp.VP_ERR_NULL
+
+
+AXES = [(320, 160), (240, 128), (854, 640), (480, 352), (1920, 800), (1080, 448), (1280, 448),
+        (720, 256), (640, 576), (360, 320), (1280, 576), (720, 320), (10, 20), (7, 13),
+        (300, 288), (1000, 32), (33, 32), (17, 64), (1024, 992), (256, 256), (3000, 96),
+        (1, 32), (2, 64)]
+
+
+@pytest.mark.parametrize("n_in,n_out", AXES)
+def test_filter_table_matches_oracle(n_in, n_out):
+    lo, cnt, w64 = oracle.filter_table(n_in, n_out)
+    assert vp.vp_filter_taps(n_in, n_out) == w64.shape[1]
+    start, count, w32 = vp.vp_filter_table(n_in, n_out)
+    assert start.tolist() == lo.tolist() and count.tolist() == cnt.tolist()
+    ref = w64.astype(np.float32)
+    # computed in double and rounded once: within one float ulp of the oracle's
+    # rounding; taps whose weight is exactly zero in exact arithmetic (the kernel
+    # at |x| = 1 or 2) may carry double-rounding residue of order 1e-16
+    tol = np.maximum(np.spacing(np.abs(ref)).astype(np.float64), 1e-15)
+    assert np.all(np.abs(w32.astype(np.float64) - ref.astype(np.float64)) <= tol)
+
+
+def _layout_items(k):
+    wl = workloads.config(k)
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "plan_configs.json")))
+    g = gold["configs"][k]
+    items = [vp.Item((0x10000, it["n_src"], it["H"], it["W"]), it["indices"], it["h"], it["w"])
+             for it in g["items"]]
+    return wl, g, items
+
+
+@pytest.mark.parametrize("k", range(5))
+def test_batch_layout_matches_golden_plan(k):
+    wl, g, items = _layout_items(k)
+    # dims from the library's own smart_resize agree with the oracle's fixture
+    for it, gi in zip(wl.items, g["items"]):
+        if it.dims is None:
+            assert vp.vp_smart_resize_dims(it.H, it.W, 32, it.min_pixels, it.max_pixels) == \
+                (gi["h"], gi["w"])
+    grid, cu, rows, ws = vp.vp_batch_layout(items)
+    assert grid.tolist() == g["grid_thw"]
+    assert cu.tolist() == g["cu_seqlens"]
+    assert rows == g["cu_seqlens"][-1]
+    assert ws > 0 and ws % 256 == 0
+
+
+def test_batch_layout_random_ragged_vs_oracle():
+    rng = np.random.default_rng(33)
+    for _ in range(50):
+        B = int(rng.integers(1, 20))
+        items, n_idx, hs, ws = [], [], [], []
+        for _ in range(B):
+            n_src = int(rng.integers(1, 40))
+            n = int(rng.integers(1, n_src + 1))
+            h = 32 * int(rng.integers(1, 20))
+            w = 32 * int(rng.integers(1, 20))
+            idx = rng.integers(0, n_src, size=n)
+            items.append(vp.Item((0x10000, n_src, int(rng.integers(1, 999)),
+                                  int(rng.integers(1, 999))), idx, h, w))
+            n_idx.append(n)
+            hs.append(h)
+            ws.append(w)
+        grid, cu, rows, _ = vp.vp_batch_layout(items)
+        og, ocu = oracle.layout(n_idx, hs, ws)
+        assert grid.tolist() == og.tolist() and cu.tolist() == ocu.tolist() and rows == ocu[-1]
+
+
+def test_layout_errors():
+    ok = vp.Item((0x10000, 4, 100, 100), [0, 3], 64, 64)
+    cases = [
+        (vp.Item((0x10000, 4, 100, 100), [0, 4], 64, 64), vp.VP_ERR_INDEX),
+        (vp.Item((0x10000, 4, 100, 100), [-1], 64, 64), vp.VP_ERR_INDEX),
+        (vp.Item((0x10000, 4, 100, 100), [0], 48, 64), vp.VP_ERR_DIMS),
+        (vp.Item((0x10000, 4, 100, 100), [0], 0, 64), vp.VP_ERR_DIMS),
+        (vp.Item((0x10000, 4, 0, 100), [0], 64, 64), vp.VP_ERR_DIMS),
+        (vp.Item((0x10000, 0, 100, 100), [0], 64, 64), vp.VP_ERR_FRAMES),
+        (vp.Item((0x10000, 4, 100, 100), [], 64, 64), vp.VP_ERR_FRAMES),
+        (vp.Item((0, 4, 100, 100), [0], 64, 64), vp.VP_ERR_NULL),
+        (vp.Item((0x10000, 1, 40000, 40000), [0], 64, 64), vp.VP_ERR_CAPACITY),  # 4.8 GB frame
+    ]
+    for bad, code in cases:
+        with pytest.raises(vp.VPError) as e:
+            vp.vp_batch_layout([ok, bad])
+        assert e.value.status == code, (bad, code)
+    L = vp.lib()
+    assert L.vp_batch_layout(None, 1, None, None, None, None) == vp.VP_ERR_NULL
+    b = vp._Batch([ok])
+    assert L.vp_batch_layout(b.arr, 0, None, None, None, None) == vp.VP_ERR_ARG
+
+
+def _raw_preprocess(items, mean=(0.5,) * 3, std=(0.5,) * 3, dtype=vp.VP_OUT_BF16,
+                    out=0x100000, cap=1 << 30, ws=0x200000, ws_bytes=1 << 30):
+    b = vp._Batch(items)
+    m = (ctypes.c_float * 3)(*mean)
+    s = (ctypes.c_float * 3)(*std)
+    return vp.lib().vp_preprocess_batch(b.arr, len(b), m, s, dtype, ctypes.c_void_p(out), cap,
+                                        None, None, ctypes.c_void_p(ws), ws_bytes, None)
+
+
+def test_preprocess_errors_before_any_gpu_work():
+    """Every failure is detected on the host before the plan is uploaded."""
+    ok = vp.Item((0x10000, 4, 100, 100), [0, 3], 64, 64)
+    _, _, rows, need = vp.vp_batch_layout([ok])
+    assert _raw_preprocess([ok], std=(0.5, 0.0, 0.5)) == vp.VP_ERR_ARG
+    assert _raw_preprocess([ok], std=(0.5, -1.0, 0.5)) == vp.VP_ERR_ARG
+    assert _raw_preprocess([ok], mean=(float("nan"), 0, 0)) == vp.VP_ERR_ARG
+    assert _raw_preprocess([ok], dtype=5) == vp.VP_ERR_ARG
+    assert _raw_preprocess([ok], out=0x100004) == vp.VP_ERR_ARG        # not 16-byte aligned
+    assert _raw_preprocess([ok], ws=0x200010) == vp.VP_ERR_ARG         # not 256-byte aligned
+    assert _raw_preprocess([ok], out=0) == vp.VP_ERR_NULL
+    assert _raw_preprocess([ok], ws=0) == vp.VP_ERR_NULL
+    assert _raw_preprocess([ok], cap=rows - 1) == vp.VP_ERR_CAPACITY
+    assert _raw_preprocess([ok], ws_bytes=need - 1) == vp.VP_ERR_CAPACITY
+    assert b"plan needs" in vp.lib().vp_last_error_message()
+    assert _raw_preprocess([vp.Item((0x10000, 4, 100, 100), [9], 64, 64)]) == vp.VP_ERR_INDEX
+    assert b"outside [0, 4)" in vp.lib().vp_last_error_message()
+
+
+def test_extreme_downscale_is_rejected_not_truncated():
+    # a 40000-pixel-wide source to 32 columns: a horizontal window of ~5000
+    # taps exceeds what the kernels stage; the call fails instead of clipping
+    it = vp.Item((0x10000, 1, 100, 40000), [0], 32, 32)
+    with pytest.raises(vp.VPError) as e:
+        vp.vp_batch_layout([it])
+    assert e.value.status == vp.VP_ERR_CAPACITY
