@@ -9,7 +9,9 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <map>
+#include <tuple>
 #include <mutex>
 #include <string>
 #include <utility>
@@ -132,10 +134,12 @@ struct Plan {
     std::vector<int32_t> prefix;
     std::vector<int32_t> indices;
     std::vector<int32_t> tables;
+    std::vector<vp::StreamUnit> units;
+    std::vector<vp::StreamLaunch> launches;
     std::vector<int32_t> grid;  // [n][3]
     std::vector<int32_t> cu;    // [n + 1]
     int64_t total_rows = 0;
-    size_t off_items = 0, off_prefix = 0, off_indices = 0, off_tables = 0, bytes = 0;
+    size_t off_items = 0, off_prefix = 0, off_indices = 0, off_tables = 0, off_units = 0, bytes = 0;
 };
 
 int32_t validate_item(const vp_item& it, int32_t b) {
@@ -176,6 +180,119 @@ bool generic_subtile(const AxisFilter& fx, int32_t* rh, int32_t* cw) {
     return false;
 }
 
+// ---------------------------------------------------------------------------
+// Streaming-kernel routing and tables
+// ---------------------------------------------------------------------------
+
+// Row-scatter view of a y axis: for every source row, the first output row
+// that reads it, how many consecutive output rows do, and their weights;
+// then the row on which each output row closes.  Returns the largest count,
+// or -1 if some source row is read by no output row or by a non-consecutive
+// set, or if two output rows would close on the same source row anywhere
+// but at the bottom border.
+int32_t build_scatter(const AxisFilter& f, std::vector<int32_t>* words) {
+    const int32_t n_in = f.n_in, n_out = f.n_out;
+    const int32_t rows = n_in + vp::kScatterMax;
+    std::vector<int32_t> first(rows, -1), count(rows, 0), close(n_out, 0);
+    std::vector<float> wt(size_t(rows) * vp::kScatterMax, 0.0f);
+    for (int32_t i = 0; i < n_out; ++i) {
+        for (int32_t k = 0; k < f.count[i]; ++k) {
+            const int32_t y = f.start[i] + k;
+            if (first[y] < 0) first[y] = i;
+            if (i != first[y] + count[y]) return -1;
+            if (count[y] >= vp::kScatterMax) return vp::kScatterMax + 1;
+            wt[size_t(y) * vp::kScatterMax + count[y]] = f.weight[size_t(i) * f.taps + k];
+            ++count[y];
+        }
+    }
+    int32_t most = 0;
+    for (int32_t y = 0; y < n_in; ++y) {
+        if (count[y] == 0) return -1;
+        most = count[y] > most ? count[y] : most;
+    }
+    // close rows: the window end, pushed past the previous output's close row
+    for (int32_t i = 0; i < n_out; ++i) {
+        int32_t c = f.start[i] + f.count[i] - 1;
+        if (i > 0 && c <= close[i - 1]) {
+            if (f.start[i] + f.count[i] != n_in) return -1;   // only at the bottom border
+            c = close[i - 1] + 1;
+        }
+        close[i] = c;
+    }
+    if (close[n_out - 1] >= rows) return vp::kScatterMax + 1;
+    // virtual rows n_in, n_in+1, ...: the rows still open, zero weights
+    for (int32_t y = n_in; y <= close[n_out - 1]; ++y) {
+        int32_t i = 0;
+        while (close[i] < y) ++i;
+        first[y] = i;
+        count[y] = n_out - i;
+    }
+    words->assign(size_t(rows) * vp::kScatterWords + n_out + 1, 0);   // +1: close_row[n_out] pad
+    for (int32_t y = 0; y < rows; ++y) {
+        int32_t* row = words->data() + size_t(y) * vp::kScatterWords;
+        row[0] = first[y] < 0 ? n_out : first[y];
+        row[1] = count[y];
+        std::memcpy(row + 2, &wt[size_t(y) * vp::kScatterMax], sizeof(float) * vp::kScatterMax);
+    }
+    std::memcpy(words->data() + size_t(rows) * vp::kScatterWords, close.data(),
+                sizeof(int32_t) * n_out);
+    return most;
+}
+
+// Column table of an x axis for the streaming kernel: start[j] with
+// start[j] + kx <= tlen, and the window's weights shifted by
+// (window start - start[j]) inside kx zero-padded taps.
+void build_columns(const AxisFilter& f, int32_t kx, int32_t tlen, std::vector<int32_t>* words) {
+    words->assign(size_t(f.n_out) * (1 + kx), 0);
+    int32_t* start = words->data();
+    float* w = reinterpret_cast<float*>(words->data() + f.n_out);
+    for (int32_t j = 0; j < f.n_out; ++j) {
+        const int32_t s = f.start[j] < tlen - kx ? f.start[j] : tlen - kx;
+        const int32_t shift = f.start[j] - s;
+        start[j] = s;
+        for (int32_t k = 0; k < f.count[j]; ++k)
+            w[size_t(j) * kx + shift + k] = f.weight[size_t(j) * f.taps + k];
+    }
+}
+
+struct StreamShape {
+    int32_t m = 0, kx = 0, threads = 0, slots = 0, ring = 0, stage = 0, n_strips = 0, tlen = 0;
+};
+
+int32_t round_up(int32_t v, int32_t q) { return (v + q - 1) / q * q; }
+
+// Whether an item can take the streaming kernel, and with which shape.
+// The LDS budget is checked with float32 staging, so the routing does not
+// depend on the output type.
+bool stream_shape(const vp_item& it, const AxisFilter& fy, const AxisFilter& fx, int32_t m,
+                  StreamShape* sh) {
+    if (it.src_h < it.dst_h) return false;                 // vertical upscale: general kernel
+    if (m < 1 || m > vp::kScatterMax) return false;
+    const int32_t kx = round_up(fx.taps, 4);
+    if (!vp::stream_shape_supported(m < 4 ? 4 : m, kx)) return false;
+    const int32_t n_strips = (it.src_w + 3) / 4;
+    const int32_t tlen = 4 * n_strips > kx ? 4 * n_strips : kx;
+    const int32_t lanes = n_strips > it.dst_w ? n_strips : (it.dst_w < vp::kStreamMaxThreads ? it.dst_w : vp::kStreamMaxThreads);
+    const int32_t threads = round_up(lanes, 64);
+    if (n_strips > vp::kStreamMaxThreads || threads > vp::kStreamMaxThreads) return false;
+    if (int64_t(it.src_h) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
+    const int64_t stage = int64_t(it.dst_w) * 12 * 4;
+    const int64_t ring = int64_t(tlen) * 16;
+    int32_t slots = 2;
+    if (2 * ring + stage > 80 * 1024) slots = 1;
+    if (slots * ring + stage > vp::kStreamLdsBudget) return false;
+    (void)fy;
+    sh->m = m < 4 ? 4 : m;
+    sh->kx = kx;
+    sh->threads = threads;
+    sh->slots = slots;
+    sh->ring = static_cast<int32_t>(slots * ring);
+    sh->stage = it.dst_w * 12;
+    sh->n_strips = n_strips;
+    sh->tlen = tlen;
+    return true;
+}
+
 int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
@@ -204,6 +321,40 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         return &found->second.second;
     };
 
+    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, int32_t>> scatters;  // -> (offset, m)
+    auto scatter_for = [&](int32_t n_in, int32_t n_out, const AxisFilter& f, int32_t* off,
+                           int32_t* m) -> const int32_t* {
+        auto key = std::make_pair(n_in, n_out);
+        auto found = scatters.find(key);
+        if (found == scatters.end()) {
+            std::vector<int32_t> words;
+            const int32_t most = n_in >= n_out ? build_scatter(f, &words) : -1;
+            int32_t o = -1;
+            if (most >= 1 && most <= vp::kScatterMax) {
+                o = static_cast<int32_t>(p->tables.size());
+                p->tables.insert(p->tables.end(), words.begin(), words.end());
+            }
+            found = scatters.emplace(key, std::make_pair(o, most)).first;
+        }
+        *off = found->second.first;
+        *m = found->second.second;
+        return found->second.first >= 0 ? p->tables.data() : nullptr;
+    };
+    std::map<std::tuple<int32_t, int32_t, int32_t, int32_t>, int32_t> column_tables;
+    auto columns_for = [&](const AxisFilter& f, int32_t kx, int32_t tlen) -> int32_t {
+        auto key = std::make_tuple(f.n_in, f.n_out, kx, tlen);
+        auto found = column_tables.find(key);
+        if (found == column_tables.end()) {
+            std::vector<int32_t> words;
+            build_columns(f, kx, tlen, &words);
+            const int32_t o = static_cast<int32_t>(p->tables.size());
+            p->tables.insert(p->tables.end(), words.begin(), words.end());
+            found = column_tables.emplace(key, o).first;
+        }
+        return found->second;
+    };
+    std::vector<StreamShape> shapes(n);
+
     int64_t rows = 0, tiles = 0;
     for (int32_t b = 0; b < n; ++b) {
         const vp_item& it = items[b];
@@ -226,28 +377,107 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         const AxisFilter* fx = table_for(it.src_w, it.dst_w, &d.tx_off);
         d.ky = fy->taps;
         d.kx = fx->taps;
-        if (!generic_subtile(*fx, &d.rh, &d.cw))
+        d.route = vp::kRouteGeneric;
+        int32_t m = 0;
+        const int32_t* scat = scatter_for(it.src_h, it.dst_h, *fy, &d.sy_off, &m);
+        StreamShape sh;
+        if (scat != nullptr && stream_shape(it, *fy, *fx, m, &sh)) {
+            d.route = vp::kRouteStream;
+            d.n_strips = sh.n_strips;
+            d.tlen = sh.tlen;
+            d.sx_off = columns_for(*fx, sh.kx, sh.tlen);
+            shapes[b] = sh;
+        } else if (!generic_subtile(*fx, &d.rh, &d.cw)) {
             return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
                                              ": horizontal filter window too long (downscale too large)");
-        d.route = vp::kRouteGeneric;
+        }
         d.row_off = rows;
         const int64_t item_rows = int64_t(d.t) * (it.dst_h / vp::kPatch) * (it.dst_w / vp::kPatch);
         p->grid[3 * b + 0] = d.t;
         p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
         p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
         rows += item_rows;
-        tiles += int64_t(d.t) * d.hm * d.wm;
+        if (d.route == vp::kRouteGeneric) tiles += int64_t(d.t) * d.hm * d.wm;
         if (rows > INT32_MAX || tiles > INT32_MAX)
             return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 rows");
         p->cu[b + 1] = static_cast<int32_t>(rows);
         p->prefix[b + 1] = static_cast<int32_t>(tiles);
     }
     p->total_rows = rows;
+
+    // Streaming units: one per (item, distinct frame of a pair, band of output
+    // rows); bands are cut so that the batch yields enough workgroups to fill
+    // the chip, in multiples of 4 rows (one 64-value run per store).
+    int64_t stream_frames = 0;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp::DevItem& d = p->items[b];
+        if (d.route != vp::kRouteStream) continue;
+        for (int32_t tt = 0; tt < d.t; ++tt)
+            stream_frames += p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1] ? 1 : 2;
+    }
+    struct Keyed {
+        std::tuple<int32_t, int32_t, int32_t, int32_t> key;
+        vp::StreamUnit unit;
+        int32_t ring, stage;
+    };
+    std::vector<Keyed> keyed;
+    constexpr int64_t kTargetUnits = 2048;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp::DevItem& d = p->items[b];
+        if (d.route != vp::kRouteStream) continue;
+        const StreamShape& sh = shapes[b];
+        int64_t band = stream_frames > 0 ? int64_t(d.h) * stream_frames / kTargetUnits : d.h;
+        band = band / 4 * 4;
+        if (band < 16) band = 16;
+        if (band > d.h) band = d.h;
+        for (int32_t tt = 0; tt < d.t; ++tt) {
+            const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
+            for (int32_t dt = 0; dt < (same ? 1 : 2); ++dt) {
+                for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
+                    const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
+                    Keyed k;
+                    k.key = std::make_tuple(sh.m, sh.kx, sh.threads, sh.slots);
+                    k.unit.item = b;
+                    k.unit.p = 2 * tt + dt;
+                    k.unit.rows = i0 | (i1 << 16);
+                    k.unit.flags = same ? 1 : 0;
+                    k.ring = sh.ring;
+                    k.stage = sh.stage;
+                    keyed.push_back(k);
+                }
+            }
+        }
+    }
+    std::stable_sort(keyed.begin(), keyed.end(),
+                     [](const Keyed& a, const Keyed& c) { return a.key < c.key; });
+    p->units.clear();
+    p->launches.clear();
+    for (size_t k = 0; k < keyed.size(); ++k) {
+        if (k == 0 || keyed[k].key != keyed[k - 1].key) {
+            vp::StreamLaunch L{};
+            L.first = static_cast<int32_t>(k);
+            L.count = 0;
+            L.m = std::get<0>(keyed[k].key);
+            L.kx = std::get<1>(keyed[k].key);
+            L.threads = std::get<2>(keyed[k].key);
+            L.slots = std::get<3>(keyed[k].key);
+            L.ring_bytes = 0;
+            L.stage_elems = 0;
+            p->launches.push_back(L);
+        }
+        vp::StreamLaunch& L = p->launches.back();
+        ++L.count;
+        if (keyed[k].ring > L.ring_bytes) L.ring_bytes = keyed[k].ring;
+        if (keyed[k].stage > L.stage_elems) L.stage_elems = keyed[k].stage;
+        p->units.push_back(keyed[k].unit);
+    }
+
     p->off_items = 0;
     p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
     p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
     p->off_tables = align_up(p->off_indices + sizeof(int32_t) * p->indices.size());
-    p->bytes = align_up(p->off_tables + sizeof(int32_t) * p->tables.size());
+    p->off_units = align_up(p->off_tables + sizeof(int32_t) * p->tables.size());
+    p->bytes = align_up(p->off_units + sizeof(vp::StreamUnit) * p->units.size());
     return VP_OK;
 }
 
@@ -316,6 +546,8 @@ int32_t upload_plan(const Plan& p, void* workspace, hipStream_t stream) {
     std::memcpy(base + p.off_prefix, p.prefix.data(), sizeof(int32_t) * p.prefix.size());
     std::memcpy(base + p.off_indices, p.indices.data(), sizeof(int32_t) * p.indices.size());
     std::memcpy(base + p.off_tables, p.tables.data(), sizeof(int32_t) * p.tables.size());
+    if (!p.units.empty())
+        std::memcpy(base + p.off_units, p.units.data(), sizeof(vp::StreamUnit) * p.units.size());
     e = hipMemcpyAsync(workspace, s.host, p.bytes, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
     e = hipEventRecord(s.done, stream);
@@ -468,11 +700,15 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
     view.tile_prefix = reinterpret_cast<const int32_t*>(ws + p.off_prefix);
     view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
     view.tables = reinterpret_cast<const int32_t*>(ws + p.off_tables);
+    view.units = reinterpret_cast<const vp::StreamUnit*>(ws + p.off_units);
     view.n_items = n_items;
     view.n_tiles = p.prefix[n_items];
-    const int err = vp::launch_generic(view, out_rows, out_dtype, norm, stream);
-    if (err != 0)
-        return hip_fail(static_cast<hipError_t>(err), "kernel launch");
+    int err = vp::launch_generic(view, out_rows, out_dtype, norm, stream);
+    if (err != 0) return hip_fail(static_cast<hipError_t>(err), "general kernel launch");
+    for (const vp::StreamLaunch& L : p.launches) {
+        err = vp::launch_stream(view, L, out_rows, out_dtype, norm, stream);
+        if (err != 0) return hip_fail(static_cast<hipError_t>(err), "streaming kernel launch");
+    }
     if (grid_thw) std::memcpy(grid_thw, p.grid.data(), sizeof(int32_t) * p.grid.size());
     if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
     g_last_error.clear();

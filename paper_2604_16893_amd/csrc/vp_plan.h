@@ -1,17 +1,33 @@
 // vp_plan.h -- device-side plan of one vp_preprocess_batch call.
 //
 // The host planner (vp_api.cpp) validates the items, computes their filter
-// tables, tile counts and row offsets, packs everything into one blob and
+// tables, work units and row offsets, packs everything into one blob and
 // copies it into the caller's workspace with a single async copy; the
 // kernels (vp_kernels.hip) read it from there.  Layout of the blob, each
 // section aligned to 256 bytes:
-//   DevItem items[n_items]
-//   int32   tile_prefix[n_items + 1]     work units of item b: [prefix[b], prefix[b+1])
-//   int32   indices[sum of padded counts] frame index of every (frame pair, dt)
-//   int32   tables[...]                  filter tables, 4-byte words
-// A filter table of one axis (n_in -> n_out, K taps) at word offset `off`:
-//   int32 start[n_out]; int32 count[n_out]; float weight[n_out][K]
-// Items with the same (n_in, n_out) share one table.
+//   DevItem    items[n_items]
+//   int32      tile_prefix[n_items + 1]   general-kernel work of item b: [prefix[b], prefix[b+1])
+//   int32      indices[sum of padded counts]  source frame of every (frame pair, dt)
+//   int32      tables[...]                filter tables, 4-byte words
+//   StreamUnit units[...]                 streaming-kernel work units, grouped per launch
+//
+// Tables (word offsets into `tables`; items with the same axis share them):
+//   window table of an axis n_in -> n_out, K taps:
+//       int32 start[n_out]; int32 count[n_out]; float weight[n_out][K]
+//   row-scatter table of a y axis n_in -> n_out (streaming kernel):
+//       [n_in + 6] rows of 16 words: int32 first; int32 count; float weight[14]
+//         -- output rows first .. first+count-1 read source row y, with the first
+//            count weights; the rest are zero (so that weight[skip + m] is zero
+//            for every m < 6 past the count)
+//       int32 close_row[n_out + 1]   (the last entry is padding)
+//         -- the row after which output row i is complete: the last row of its
+//            window, except that output rows whose windows all end at the bottom
+//            border close on consecutive rows n_in-1, n_in, n_in+1, ...; rows past
+//            n_in carry zero weights for the rows still open (one close per row)
+//   column table of an x axis (streaming kernel), KX taps:
+//       int32 start[n_out]; float weight[n_out][KX]
+//     -- start + KX never passes the streaming kernel's LDS row; weights are
+//        shifted and zero-padded to match.
 #pragma once
 
 #include <cstdint>
@@ -25,10 +41,15 @@ constexpr int kWin = 32;              // merge window edge in pixels (patch * me
 constexpr int kRow = 1536;            // 3 * 2 * 16 * 16
 constexpr int kWinElems = 4 * kRow;   // one merge window of one frame pair
 constexpr int kGenericThreads = 256;
-constexpr int kGenericTCap = 8192;    // floats of the generic kernel's LDS column tile
+constexpr int kGenericTCap = 8192;    // floats of the general kernel's LDS column tile
+constexpr int kScatterWords = 16;     // words per source row of a row-scatter table
+constexpr int kScatterMax = 6;        // weights per source row (output rows reading it)
+constexpr int kStripBytes = 12;       // bytes of a source row per streaming lane (4 pixels)
+constexpr int kStreamMaxThreads = 512;  // largest streaming block (launch bound)
+constexpr int kStreamLdsBudget = 160 * 1024;  // LDS of one gfx950 workgroup
 
-// Kernel variants an item can be routed to.
-enum Route : int32_t { kRouteGeneric = 0 };
+// Kernel an item is routed to.
+enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1 };
 
 struct DevItem {
     const uint8_t* frames;   // [n_src][H][W][3]
@@ -37,18 +58,35 @@ struct DevItem {
     int32_t H, W, h, w;      // source and target size
     int32_t t, hm, wm;       // frame pairs, merge windows along y and x
     int32_t idx_off;         // first entry of the item in `indices` (2 * t entries)
-    int32_t ty_off, tx_off;  // word offsets of the y and x filter tables
-    int32_t ky, kx;          // tap stride of the y and x tables
-    int32_t rh, cw;          // generic kernel: output rows / columns per LDS sub-tile
-    int32_t route, pad0;
+    int32_t ty_off, tx_off;  // window tables of the y and x axes
+    int32_t ky, kx;          // tap stride of those tables
+    int32_t rh, cw;          // general kernel: output rows / columns per LDS sub-tile
+    int32_t route;
+    int32_t n_strips;        // streaming kernel: lanes that read a source row, ceil(W / 4)
+    int32_t sy_off, sx_off;  // streaming kernel: row-scatter and column tables
+    int32_t tlen;            // streaming kernel: pixels of one LDS row
+    int32_t pad0;
 };
-static_assert(sizeof(DevItem) == 88, "DevItem layout");
+static_assert(sizeof(DevItem) == 104, "DevItem layout");
+
+// One streaming work unit: output rows [i0, i1) of padded frame position p
+// of an item.  flags bit 0: the pair's two frames are the same source frame
+// (an image, or an odd count padded with its last index), so the unit
+// writes both temporal halves of the rows.
+struct StreamUnit {
+    int32_t item;
+    int32_t p;
+    int32_t rows;    // i0 | (i1 << 16)
+    int32_t flags;
+};
+static_assert(sizeof(StreamUnit) == 16, "StreamUnit layout");
 
 struct PlanView {
     const DevItem* items;
     const int32_t* tile_prefix;
     const int32_t* indices;
     const int32_t* tables;
+    const StreamUnit* units;
     int32_t n_items;
     int32_t n_tiles;
 };
@@ -58,8 +96,23 @@ struct Norm {
     float b[3];   // -mean_c / std_c
 };
 
-// Kernel launchers (vp_kernels.hip).
+// One launch of the streaming kernel: units [first, first + count), all
+// with the same template shape and block size.
+struct StreamLaunch {
+    int32_t first, count;
+    int32_t m, kx;           // rotating accumulators, column taps
+    int32_t threads;         // block size, multiple of 64
+    int32_t slots;           // LDS rows handed from the y pass to the x pass (1 or 2)
+    int32_t ring_bytes;      // LDS of those rows (largest item of the launch)
+    int32_t stage_elems;     // output values staged per four rows (largest item)
+};
+
+// Kernel launchers (vp_kernels.hip).  Return a hipError_t value.
 int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
                    hipStream_t stream);
+int launch_stream(const PlanView& plan, const StreamLaunch& launch, void* out, int out_dtype,
+                  const Norm& norm, hipStream_t stream);
+// Whether a (m, kx) shape has a compiled streaming kernel.
+bool stream_shape_supported(int m, int kx);
 
 }  // namespace vp
