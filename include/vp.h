@@ -198,6 +198,19 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
                             int64_t out_rows_capacity, int32_t* grid_thw, int32_t* cu_seqlens,
                             void* workspace, int64_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Kernel timing hook (measurement only; not a step of the method).  The next
+ * vp_preprocess_batch call made on this thread records `start` on its stream
+ * immediately before its first kernel launch (after the plan upload) and
+ * `stop` immediately after its last launch, then forgets both events, so
+ * that hipEventElapsedTime(start, stop) is the device time of that call's
+ * kernels alone.  A call that fails before launching records neither.
+ * start, stop: events created by the caller (hipEventCreate or equivalent),
+ *   still owned by the caller; NULL, NULL cancels a pending request.
+ * Errors: VP_ERR_NULL (exactly one of the two is NULL).
+ */
+int32_t vp_set_kernel_events(hipEvent_t start, hipEvent_t stop);
+
 /* Static name of a status code ("VP_OK", "VP_ERR_ARG", ...). */
 const char* vp_status_string(int32_t status);
 

@@ -32,7 +32,7 @@ VP_FACTOR = 32
 
 EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
             "vp_batch_layout", "vp_preprocess_batch", "vp_status_string",
-            "vp_last_error_message")
+            "vp_last_error_message", "vp_set_kernel_events")
 
 
 class VPError(RuntimeError):
@@ -73,6 +73,7 @@ def lib() -> ctypes.CDLL:
         L.vp_batch_layout.argtypes = [itemp, i32, i32p, i32p, i64p, i64p]
         L.vp_preprocess_batch.argtypes = [itemp, i32, f32p, f32p, i32, ctypes.c_void_p, i64,
                                           i32p, i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
+        L.vp_set_kernel_events.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         L.vp_status_string.argtypes = [i32]
         L.vp_status_string.restype = ctypes.c_char_p
         L.vp_last_error_message.argtypes = []
@@ -226,6 +227,27 @@ def vp_preprocess_batch(items: Sequence, mean, std, out_dtype: int, out_rows, wo
         workspace.numel() * workspace.element_size(), ctypes.c_void_p(_stream_handle(stream))),
         "vp_preprocess_batch")
     return grid, cu
+
+
+def _event_handle(ev) -> int:
+    if ev is None:
+        return 0
+    if isinstance(ev, int):
+        return ev
+    handle = getattr(ev, "cuda_event", 0)
+    if not handle:
+        raise VPError(VP_ERR_ARG, "the event has no HIP event yet: record it once first")
+    return handle
+
+
+def vp_set_kernel_events(start, stop):
+    """Ask the next vp_preprocess_batch call on this thread to record `start`
+    before its first kernel and `stop` after its last one (torch.cuda.Event
+    objects that have been recorded at least once, raw hipEvent_t handles, or
+    None, None to cancel)."""
+    _check(lib().vp_set_kernel_events(ctypes.c_void_p(_event_handle(start)),
+                                      ctypes.c_void_p(_event_handle(stop))),
+           "vp_set_kernel_events")
 
 
 def preprocess(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None):

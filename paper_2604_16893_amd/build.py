@@ -28,7 +28,7 @@ def hipcc() -> str:
 
 
 def command(out: str = LIB) -> list:
-    return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC", "-shared",
             "-Wall", "-I", os.path.join(ROOT, "include"), "-I", CSRC, *DEVICE_FLAGS,
             "-o", out, *SOURCES]
 

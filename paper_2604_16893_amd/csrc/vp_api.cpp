@@ -23,6 +23,8 @@
 namespace {
 
 thread_local std::string g_last_error;
+thread_local hipEvent_t g_timing_start = nullptr;   // vp_set_kernel_events, one call
+thread_local hipEvent_t g_timing_stop = nullptr;
 
 int32_t fail(int32_t status, const std::string& msg) {
     g_last_error = msg;
@@ -694,6 +696,12 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
                                          " bytes, plan needs " + std::to_string(p.bytes));
     st = upload_plan(p, workspace, stream);
     if (st != VP_OK) return st;
+    hipEvent_t t_start = g_timing_start, t_stop = g_timing_stop;
+    g_timing_start = g_timing_stop = nullptr;
+    if (t_start != nullptr) {
+        const hipError_t e = hipEventRecord(t_start, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing start)");
+    }
     auto* ws = static_cast<uint8_t*>(workspace);
     vp::PlanView view;
     view.items = reinterpret_cast<const vp::DevItem*>(ws + p.off_items);
@@ -708,6 +716,10 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
     for (const vp::StreamLaunch& L : p.launches) {
         err = vp::launch_stream(view, L, out_rows, out_dtype, norm, stream);
         if (err != 0) return hip_fail(static_cast<hipError_t>(err), "streaming kernel launch");
+    }
+    if (t_stop != nullptr) {
+        const hipError_t e = hipEventRecord(t_stop, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");
     }
     if (grid_thw) std::memcpy(grid_thw, p.grid.data(), sizeof(int32_t) * p.grid.size());
     if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
@@ -728,6 +740,15 @@ const char* vp_status_string(int32_t status) {
         case VP_ERR_HIP: return "VP_ERR_HIP";
         default: return "VP_ERR_UNKNOWN";
     }
+}
+
+int32_t vp_set_kernel_events(hipEvent_t start, hipEvent_t stop) {
+    if ((start == nullptr) != (stop == nullptr))
+        return fail(VP_ERR_NULL, "vp_set_kernel_events needs both events or neither");
+    g_timing_start = start;
+    g_timing_stop = stop;
+    g_last_error.clear();
+    return VP_OK;
 }
 
 const char* vp_last_error_message(void) { return g_last_error.c_str(); }
