@@ -17,7 +17,11 @@ ARCH = "gfx950"
 
 # Packed FP32 instructions are disabled for all device code: plain float
 # code is compiled to scalar v_fma_f32 / v_add_f32 only.
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Common-code sinking is off: it would merge the streaming kernel's
+# per-slot close paths (each naming its own accumulator registers) into one
+# path over copied registers.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-simplifycfg-sink-common=false"]
 
 
 def hipcc() -> str:

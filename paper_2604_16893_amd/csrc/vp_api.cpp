@@ -186,71 +186,68 @@ bool generic_subtile(const AxisFilter& fx, int32_t* rh, int32_t* cw) {
 // Streaming-kernel routing and tables
 // ---------------------------------------------------------------------------
 
-// Row-scatter view of a y axis: for every source row, the first output row
-// that reads it, how many consecutive output rows do, and their weights;
-// then the row on which each output row closes.  Returns the largest count,
-// or -1 if some source row is read by no output row or by a non-consecutive
-// set, or if two output rows would close on the same source row anywhere
-// but at the bottom border.
-int32_t build_scatter(const AxisFilter& f, std::vector<int32_t>* words) {
+// Slot table of a y axis for the streaming kernel.  Output row i lives in
+// accumulator slot i mod M while it is open: from the first row of its
+// window to its close row.  The close row is the last row of the window,
+// except that output rows whose windows all end at the bottom border close
+// on consecutive rows n_in-1, n_in, n_in+1, ... (rows past n_in only carry
+// zero weights).  M is the most output rows open at once (at least 4), so two
+// open rows never share a slot.  For every source row y the table holds, per
+// slot s < M, the weight of y in the output row that has slot s at y (zero if
+// that row does not read y), then the close row of every output row.
+// Returns M, or -1 if the axis needs more than kSlotMax slots.
+int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
     const int32_t n_in = f.n_in, n_out = f.n_out;
-    const int32_t rows = n_in + vp::kScatterMax;
-    std::vector<int32_t> first(rows, -1), count(rows, 0), close(n_out, 0);
-    std::vector<float> wt(size_t(rows) * vp::kScatterMax, 0.0f);
-    for (int32_t i = 0; i < n_out; ++i) {
-        for (int32_t k = 0; k < f.count[i]; ++k) {
-            const int32_t y = f.start[i] + k;
-            if (first[y] < 0) first[y] = i;
-            if (i != first[y] + count[y]) return -1;
-            if (count[y] >= vp::kScatterMax) return vp::kScatterMax + 1;
-            wt[size_t(y) * vp::kScatterMax + count[y]] = f.weight[size_t(i) * f.taps + k];
-            ++count[y];
-        }
-    }
-    int32_t most = 0;
-    for (int32_t y = 0; y < n_in; ++y) {
-        if (count[y] == 0) return -1;
-        most = count[y] > most ? count[y] : most;
-    }
-    // close rows: the window end, pushed past the previous output's close row
+    const int32_t rows = n_in + vp::kSlotMax;
+    std::vector<int32_t> close(n_out, 0);
     for (int32_t i = 0; i < n_out; ++i) {
         int32_t c = f.start[i] + f.count[i] - 1;
         if (i > 0 && c <= close[i - 1]) {
             if (f.start[i] + f.count[i] != n_in) return -1;   // only at the bottom border
             c = close[i - 1] + 1;
         }
+        if (i > 0 && f.start[i] < f.start[i - 1]) return -1;
         close[i] = c;
     }
-    if (close[n_out - 1] >= rows) return vp::kScatterMax + 1;
-    // virtual rows n_in, n_in+1, ...: the rows still open, zero weights
-    for (int32_t y = n_in; y <= close[n_out - 1]; ++y) {
-        int32_t i = 0;
-        while (close[i] < y) ++i;
-        first[y] = i;
-        count[y] = n_out - i;
+    if (close[n_out - 1] >= rows) return -1;
+    // most rows open at once: a row is open on [start, close]
+    std::vector<int32_t> delta(rows + 1, 0);
+    for (int32_t i = 0; i < n_out; ++i) {
+        ++delta[f.start[i]];
+        --delta[close[i] + 1];
     }
-    words->assign(size_t(rows) * vp::kScatterWords + n_out + 1, 0);   // +1: close_row[n_out] pad
+    int32_t open = 0, most = 0;
     for (int32_t y = 0; y < rows; ++y) {
-        int32_t* row = words->data() + size_t(y) * vp::kScatterWords;
-        row[0] = first[y] < 0 ? n_out : first[y];
-        row[1] = count[y];
-        std::memcpy(row + 2, &wt[size_t(y) * vp::kScatterMax], sizeof(float) * vp::kScatterMax);
+        open += delta[y];
+        most = open > most ? open : most;
     }
-    std::memcpy(words->data() + size_t(rows) * vp::kScatterWords, close.data(),
-                sizeof(int32_t) * n_out);
-    return most;
+    if (most > vp::kSlotMax) return -1;
+    const int32_t m = most < 4 ? 4 : most;
+    words->assign(size_t(rows) * vp::kSlotWords + n_out + 1, 0);   // +1: close_row[n_out] pad
+    float* w = reinterpret_cast<float*>(words->data());
+    for (int32_t i = 0; i < n_out; ++i)
+        for (int32_t k = 0; k < f.count[i]; ++k)
+            w[size_t(f.start[i] + k) * vp::kSlotWords + i % m] = f.weight[size_t(i) * f.taps + k];
+    std::memcpy(words->data() + size_t(rows) * vp::kSlotWords, close.data(), sizeof(int32_t) * n_out);
+    return m;
 }
 
-// Column table of an x axis for the streaming kernel: start[j] with
-// start[j] + kx <= tlen, and the window's weights shifted by
-// (window start - start[j]) inside kx zero-padded taps.
-void build_columns(const AxisFilter& f, int32_t kx, int32_t tlen, std::vector<int32_t>* words) {
+// Column table of an x axis for the streaming kernel.  Output columns are
+// cut into bands of `band`; a band's source pixels start at the window start
+// of its first column, x0.  For column j: start[j] = (window start - x0),
+// lowered where needed so that start[j] + kx <= row_px, and the window's
+// weights shifted by the amount it was lowered, inside kx zero-padded taps.
+// The caller has checked that every window ends within row_px of its x0.
+void build_columns(const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px,
+                   std::vector<int32_t>* words) {
     words->assign(size_t(f.n_out) * (1 + kx), 0);
     int32_t* start = words->data();
     float* w = reinterpret_cast<float*>(words->data() + f.n_out);
     for (int32_t j = 0; j < f.n_out; ++j) {
-        const int32_t s = f.start[j] < tlen - kx ? f.start[j] : tlen - kx;
-        const int32_t shift = f.start[j] - s;
+        const int32_t x0 = f.start[j / band * band];
+        const int32_t l = f.start[j] - x0;
+        const int32_t s = l < row_px - kx ? l : row_px - kx;
+        const int32_t shift = l - s;
         start[j] = s;
         for (int32_t k = 0; k < f.count[j]; ++k)
             w[size_t(j) * kx + shift + k] = f.weight[size_t(j) * f.taps + k];
@@ -258,41 +255,58 @@ void build_columns(const AxisFilter& f, int32_t kx, int32_t tlen, std::vector<in
 }
 
 struct StreamShape {
-    int32_t m = 0, kx = 0, threads = 0, slots = 0, ring = 0, stage = 0, n_strips = 0, tlen = 0;
+    int32_t m = 0, kx = 0, px = 0, band = 0, threads = 0;
 };
 
 int32_t round_up(int32_t v, int32_t q) { return (v + q - 1) / q * q; }
 
-// Whether an item can take the streaming kernel, and with which shape.
-// The LDS budget is checked with float32 staging, so the routing does not
-// depend on the output type.
-bool stream_shape(const vp_item& it, const AxisFilter& fy, const AxisFilter& fx, int32_t m,
-                  StreamShape* sh) {
+// Widest span of source pixels that one band of output columns reads.
+int32_t band_span(const AxisFilter& fx, int32_t band) {
+    int32_t worst = 0;
+    for (int32_t j0 = 0; j0 < fx.n_out; j0 += band) {
+        const int32_t j1 = (j0 + band < fx.n_out ? j0 + band : fx.n_out) - 1;
+        const int32_t span = fx.start[j1] + fx.count[j1] - fx.start[j0];
+        worst = span > worst ? span : worst;
+    }
+    return worst;
+}
+
+// Whether an item can take the streaming kernel, and with which shape: the
+// output width is cut into bands of at most 64 columns (one wave each, one
+// lane per column in the x pass), each band's source pixels must fit 64
+// lanes of px pixels, and among the shapes that fit the one with the least
+// estimated lane work is taken.  The LDS budget is checked with float32
+// staging, so the routing does not depend on the output type.
+bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
     if (it.src_h < it.dst_h) return false;                 // vertical upscale: general kernel
-    if (m < 1 || m > vp::kScatterMax) return false;
+    if (m < 4 || m > vp::kSlotMax) return false;
+    const int32_t mm = m;
     const int32_t kx = round_up(fx.taps, 4);
-    if (!vp::stream_shape_supported(m < 4 ? 4 : m, kx)) return false;
-    const int32_t n_strips = (it.src_w + 3) / 4;
-    const int32_t tlen = 4 * n_strips > kx ? 4 * n_strips : kx;
-    const int32_t lanes = n_strips > it.dst_w ? n_strips : (it.dst_w < vp::kStreamMaxThreads ? it.dst_w : vp::kStreamMaxThreads);
-    const int32_t threads = round_up(lanes, 64);
-    if (n_strips > vp::kStreamMaxThreads || threads > vp::kStreamMaxThreads) return false;
-    if (int64_t(it.src_h) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
-    const int64_t stage = int64_t(it.dst_w) * 12 * 4;
-    const int64_t ring = int64_t(tlen) * 16;
-    int32_t slots = 2;
-    if (2 * ring + stage > 80 * 1024) slots = 1;
-    if (slots * ring + stage > vp::kStreamLdsBudget) return false;
-    (void)fy;
-    sh->m = m < 4 ? 4 : m;
-    sh->kx = kx;
-    sh->threads = threads;
-    sh->slots = slots;
-    sh->ring = static_cast<int32_t>(slots * ring);
-    sh->stage = it.dst_w * 12;
-    sh->n_strips = n_strips;
-    sh->tlen = tlen;
-    return true;
+    // every load of a frame row (up to kSlotMax + 8 rows past the last one) stays below 4 GiB
+    if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
+    int64_t best = -1;
+    for (int32_t band = 64; band >= 8; band -= 8) {
+        const int32_t waves = (it.dst_w + band - 1) / band;
+        if (waves * 64 > vp::kStreamMaxThreads) break;
+        const int32_t span = band_span(fx, band);
+        for (int32_t px = 2; px <= 4; ++px) {
+            if (!vp::stream_shape_supported(mm, kx, px)) continue;
+            if (span > 64 * px || kx > 64 * px) continue;
+            if (int64_t(waves) * vp::stream_wave_bytes(px, kx, 4) > vp::kStreamLdsBudget) continue;
+            const int64_t cost = int64_t(waves) * (int64_t(it.src_h) * px * 3 * (mm + 1) +
+                                                    int64_t(it.dst_h) * (3 * kx + 12));
+            if (best < 0 || cost < best) {
+                best = cost;
+                sh->m = mm;
+                sh->kx = kx;
+                sh->px = px;
+                sh->band = band;
+                sh->threads = waves * 64;
+            }
+            break;   // a wider px only adds idle lanes
+        }
+    }
+    return best >= 0;
 }
 
 int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
@@ -323,32 +337,31 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         return &found->second.second;
     };
 
-    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, int32_t>> scatters;  // -> (offset, m)
-    auto scatter_for = [&](int32_t n_in, int32_t n_out, const AxisFilter& f, int32_t* off,
-                           int32_t* m) -> const int32_t* {
-        auto key = std::make_pair(n_in, n_out);
-        auto found = scatters.find(key);
-        if (found == scatters.end()) {
+    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, int32_t>> slot_tables;  // -> (offset, m)
+    auto slots_for = [&](const AxisFilter& f, int32_t* off, int32_t* m) -> bool {
+        auto key = std::make_pair(f.n_in, f.n_out);
+        auto found = slot_tables.find(key);
+        if (found == slot_tables.end()) {
             std::vector<int32_t> words;
-            const int32_t most = n_in >= n_out ? build_scatter(f, &words) : -1;
+            const int32_t mm = f.n_in >= f.n_out ? build_slots(f, &words) : -1;
             int32_t o = -1;
-            if (most >= 1 && most <= vp::kScatterMax) {
+            if (mm > 0) {
                 o = static_cast<int32_t>(p->tables.size());
                 p->tables.insert(p->tables.end(), words.begin(), words.end());
             }
-            found = scatters.emplace(key, std::make_pair(o, most)).first;
+            found = slot_tables.emplace(key, std::make_pair(o, mm)).first;
         }
         *off = found->second.first;
         *m = found->second.second;
-        return found->second.first >= 0 ? p->tables.data() : nullptr;
+        return found->second.first >= 0;
     };
-    std::map<std::tuple<int32_t, int32_t, int32_t, int32_t>, int32_t> column_tables;
-    auto columns_for = [&](const AxisFilter& f, int32_t kx, int32_t tlen) -> int32_t {
-        auto key = std::make_tuple(f.n_in, f.n_out, kx, tlen);
+    std::map<std::tuple<int32_t, int32_t, int32_t, int32_t, int32_t>, int32_t> column_tables;
+    auto columns_for = [&](const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px) -> int32_t {
+        auto key = std::make_tuple(f.n_in, f.n_out, kx, band, row_px);
         auto found = column_tables.find(key);
         if (found == column_tables.end()) {
             std::vector<int32_t> words;
-            build_columns(f, kx, tlen, &words);
+            build_columns(f, kx, band, row_px, &words);
             const int32_t o = static_cast<int32_t>(p->tables.size());
             p->tables.insert(p->tables.end(), words.begin(), words.end());
             found = column_tables.emplace(key, o).first;
@@ -381,13 +394,12 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         d.kx = fx->taps;
         d.route = vp::kRouteGeneric;
         int32_t m = 0;
-        const int32_t* scat = scatter_for(it.src_h, it.dst_h, *fy, &d.sy_off, &m);
         StreamShape sh;
-        if (scat != nullptr && stream_shape(it, *fy, *fx, m, &sh)) {
+        if (slots_for(*fy, &d.sy_off, &m) && stream_shape(it, *fx, m, &sh)) {
             d.route = vp::kRouteStream;
-            d.n_strips = sh.n_strips;
-            d.tlen = sh.tlen;
-            d.sx_off = columns_for(*fx, sh.kx, sh.tlen);
+            d.band = sh.band;
+            d.row_px = 64 * sh.px;
+            d.sx_off = columns_for(*fx, sh.kx, sh.band, d.row_px);
             shapes[b] = sh;
         } else if (!generic_subtile(*fx, &d.rh, &d.cw)) {
             return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
@@ -420,7 +432,6 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     struct Keyed {
         std::tuple<int32_t, int32_t, int32_t, int32_t> key;
         vp::StreamUnit unit;
-        int32_t ring, stage;
     };
     std::vector<Keyed> keyed;
     constexpr int64_t kTargetUnits = 2048;
@@ -438,13 +449,11 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
                 for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
                     const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
                     Keyed k;
-                    k.key = std::make_tuple(sh.m, sh.kx, sh.threads, sh.slots);
+                    k.key = std::make_tuple(sh.m, sh.kx, sh.px, sh.threads);
                     k.unit.item = b;
                     k.unit.p = 2 * tt + dt;
                     k.unit.rows = i0 | (i1 << 16);
                     k.unit.flags = same ? 1 : 0;
-                    k.ring = sh.ring;
-                    k.stage = sh.stage;
                     keyed.push_back(k);
                 }
             }
@@ -461,16 +470,12 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
             L.count = 0;
             L.m = std::get<0>(keyed[k].key);
             L.kx = std::get<1>(keyed[k].key);
-            L.threads = std::get<2>(keyed[k].key);
-            L.slots = std::get<3>(keyed[k].key);
-            L.ring_bytes = 0;
-            L.stage_elems = 0;
+            L.px = std::get<2>(keyed[k].key);
+            L.threads = std::get<3>(keyed[k].key);
             p->launches.push_back(L);
         }
         vp::StreamLaunch& L = p->launches.back();
         ++L.count;
-        if (keyed[k].ring > L.ring_bytes) L.ring_bytes = keyed[k].ring;
-        if (keyed[k].stage > L.stage_elems) L.stage_elems = keyed[k].stage;
         p->units.push_back(keyed[k].unit);
     }
 

@@ -6,20 +6,21 @@
 //
 // Streaming kernel (the fast path; items whose frames are not upscaled
 // vertically and whose filters are short enough).  One workgroup streams
-// one source frame -- or a band of its output rows -- top to bottom:
-//   * y pass first, in registers: each lane owns 12 bytes (4 RGB pixels) of
-//     every source row, loads them with one buffer load (prefetched four rows
-//     ahead), converts them once, and adds them with wave-uniform scalar
-//     weights into M rotating accumulators -- one per output row that can
-//     still read the current source row.  The source is read exactly once.
-//   * when an output row is complete its accumulator is written to a
-//     double-buffered LDS row (one float4 per pixel) and the workgroup
-//     barrier hands it to the x pass: one lane per output pixel, its column
-//     weights in registers, one ds_read_b128 and three FMAs per tap, then
-//     the normalisation FMA and the bf16/f32 conversion into an LDS stage.
-//   * every four output rows the stage holds one 64-value run (four patch
-//     rows of 16) of every (patch, channel) block; those leave as 16-byte
-//     stores that fill whole 128-byte lines.
+// one source frame -- or a band of its output rows -- top to bottom, one
+// wave per band of up to 64 output columns; the waves never wait for each
+// other:
+//   * y pass first, in registers: each lane owns 2 or 3 RGB pixels of the
+//     band's source span, loads them with one buffer load per row
+//     (prefetched four rows ahead), converts them once and adds them with
+//     wave-uniform scalar weights into M accumulator slots; output row i
+//     lives in slot i mod M while it is open.  The source is read once.
+//   * when an output row is complete its slot goes to the wave's LDS row
+//     (one float4 per pixel) and the wave's x pass follows: one lane per
+//     output column, one ds_read_b128 and three FMAs per tap, then the
+//     normalisation FMA and the bf16/f32 conversion into the wave's stage.
+//   * every four output rows the stage holds the band's part of one
+//     64-value run (four patch rows of 16) of every (patch, channel) block;
+//     those leave as 16-byte stores, eight lanes per 128-byte run.
 //
 // General kernel (any scale factor): one workgroup per merge window of one
 // frame pair; y pass from global memory into an LDS column tile, x pass,
@@ -159,100 +160,88 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
 // ===========================================================================
 
 constexpr int kPrefetch = 4;           // source rows in flight per lane
-constexpr int kStreamBlock = kStreamMaxThreads;
 
-// Source row y adds to the n open output rows base .. base+n-1, which live in
-// acc[0 .. n-1] (acc[0] is always the oldest open row, `base`).
-template <int M>
-__device__ __forceinline__ void add_row(float (&acc)[M][12], const float (&v)[12], cptr<float> w,
-                                        int n) {
-#pragma unroll
-    for (int m = 0; m < M; ++m) {
-        if (m < n) {
-            const float wm = w[m];
-#pragma unroll
-            for (int q = 0; q < 12; ++q) acc[m][q] = fmaf(wm, v[q], acc[m][q]);
-        }
-    }
+using f4 = float __attribute__((ext_vector_type(4)));
+
+// Orders this wave's LDS accesses before and after it.  LDS operations of
+// one wave execute in issue order, so within a wave keeping the compiler from
+// moving them across this point is all the synchronisation needed.
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Same, for a source row that completes output row `base`: its final value
-// goes to `done`, and every other sum moves down one accumulator as it is
-// formed (the FMA writes acc[m - 1]), so no register is ever copied.  The
-// FMAs are unconditional: the table pads every row with zero weights, so an
-// output row that does not read this source row just moves down unchanged
-// (output rows not yet started hold zeros; rows past the band hold values
-// that are never stored).
-template <int M>
-__device__ __forceinline__ void add_row_and_close(float (&acc)[M][12], const float (&v)[12],
-                                                  cptr<float> w, float (&done)[12]) {
-    const float w0 = w[0];
-#pragma unroll
-    for (int q = 0; q < 12; ++q) done[q] = fmaf(w0, v[q], acc[0][q]);
-#pragma unroll
-    for (int m = 1; m < M; ++m) {
-        const float wm = w[m];
-#pragma unroll
-        for (int q = 0; q < 12; ++q) acc[m - 1][q] = fmaf(wm, v[q], acc[m][q]);
-    }
-#pragma unroll
-    for (int q = 0; q < 12; ++q) acc[M - 1][q] = 0.f;
-}
-
-__device__ __forceinline__ void put_row(const float (&done)[12], float4* dst) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-        dst[q] = make_float4(done[3 * q], done[3 * q + 1], done[3 * q + 2], 0.f);
-}
-
-template <int M, int KX, int OUT_BF16>
-__global__ __launch_bounds__(kStreamBlock) void stream_kernel(PlanView plan, int unit0, int ring_slots,
-                                                              void* out, Norm norm) {
+// One workgroup streams one source frame (or a band of its output rows) top
+// to bottom; each of its waves owns one band of up to 64 output columns and
+// works alone -- no workgroup barrier anywhere:
+//   * y pass, in registers: lane t owns PX consecutive pixels of the band's
+//     source span, reads them with one buffer load per row (prefetched four
+//     rows ahead), converts them once and adds them with wave-uniform scalar
+//     weights into M rotating accumulators, one per output row that can
+//     still read the row;
+//   * when an output row completes, each lane writes its PX pixels to the
+//     wave's LDS row (float4 per pixel, 16*PX bytes per lane: no bank
+//     conflicts), and the x pass follows at once: lane j = one output column,
+//     its KX weights in registers, one ds_read_b128 and three FMAs per tap,
+//     then the normalisation FMA and the conversion into the wave's stage;
+//   * every four output rows the stage holds, for each (patch, channel), the
+//     band's part of one 64-value run; it leaves as 16-byte stores, eight
+//     lanes per 128-byte run.
+template <int M, int KX, int PX, int OUT_BF16>
+__global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan, int unit0,
+                                                                   void* out, Norm norm) {
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
+    constexpr int kRowPx = 64 * PX;
+    constexpr int kWaveBytes = stream_wave_bytes(PX, KX, sizeof(elem_t));
+    constexpr int V = 3 * PX;                      // values per lane per source row
+    constexpr int kLoadDwords = PX == 4 ? 4 : 3;   // 3*PX bytes plus up to 3 of misalignment
+    constexpr int S = 16 / int(sizeof(elem_t));    // output columns per 16-byte store
     extern __shared__ __align__(16) unsigned char smem[];
 
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const cptr<StreamUnit> up = as_const(plan.units) + unit0 + blockIdx.x;
     const int u_item = up->item, u_p = up->p, u_rows = up->rows, u_flags = up->flags;
     const cptr<DevItem> it = as_const(plan.items) + u_item;
-    const int t = threadIdx.x;
-    const int nt = blockDim.x;
     const int i0 = u_rows & 0xffff;
     const int i1 = u_rows >> 16;
     const int w = it->w;
-    const int tlen = it->tlen;
-    const int n_strips = it->n_strips;
+    const int band = it->band;
+    const int j0 = wave * band;                    // first output column of this wave
+    const int nbw = min(band, w - j0);             // its columns
     const int tt = u_p >> 1;
     const int dt_self = u_p & 1;
     const bool both = (u_flags & 1) != 0;
 
-    float4* ring = reinterpret_cast<float4*>(smem);                               // [slots][tlen]
-    elem_t* stage = reinterpret_cast<elem_t*>(smem + size_t(ring_slots) * tlen * 16);  // [w/16][3][4][16]
+    unsigned char* wbase = smem + wave * kWaveBytes;
+    float4* row = reinterpret_cast<float4*>(wbase);                                   // [kRowPx]
+    elem_t* stage = reinterpret_cast<elem_t*>(wbase + kRowPx * 16);                   // [3][4][64]
+    float4* wxl = reinterpret_cast<float4*>(wbase + kRowPx * 16 + 3 * 4 * 64 * sizeof(elem_t));  // [KX/4][64]
 
-    // LDS pixels that no lane writes stay zero (they meet zero weights only).
-    for (int k = 4 * n_strips + t; k < tlen; k += nt) {
-        ring[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (ring_slots > 1) ring[tlen + k] = make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-
-    // x pass: output pixel j = t keeps its column weights in registers.
+    // x pass: output column j0 + lane; its KX column weights wait in the
+    // wave's LDS, four per 16-byte word, one word per lane per group.
     const cptr<int32_t> tables = as_const(plan.tables);
     const cptr<int32_t> sx_start = tables + it->sx_off;
     const cptr<float> sx_w = (cptr<float>)(sx_start + w);
-    float wx[KX];
+    const bool xlane = lane < nbw;
     int sj = 0;
-    if (t < w) {
-        sj = sx_start[t];
-        const cptr<float> src = sx_w + int64_t(t) * KX;
+    {
+        const int jx = xlane ? j0 + lane : w - 1;   // idle lanes read a valid entry, keep zeros
+        const cptr<float> src = sx_w + int64_t(jx) * KX;
+        if (xlane) sj = sx_start[jx];
 #pragma unroll
-        for (int k = 0; k < KX; ++k) wx[k] = src[k];
-    } else {
-#pragma unroll
-        for (int k = 0; k < KX; ++k) wx[k] = 0.f;
+        for (int g = 0; g < KX / 4; ++g) {
+            const float4 wv = make_float4(src[4 * g], src[4 * g + 1], src[4 * g + 2], src[4 * g + 3]);
+            wxl[g * 64 + lane] = xlane ? wv : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
 
+    const cptr<int32_t> xs = tables + it->tx_off;   // window starts of the x axis
+    const int x0 = xs[j0];                          // first source pixel of the band
     const cptr<int32_t> ys = tables + it->ty_off;
-    const cptr<int32_t> scat = tables + it->sy_off;                 // [H + extra][8]
-    const cptr<int32_t> close_row = scat + int64_t(it->H + kScatterMax) * kScatterWords;  // [h]
+    const cptr<float> slot_w = (cptr<float>)(tables + it->sy_off);             // [H + 6][8]
+    const cptr<int32_t> close_row = tables + it->sy_off + (it->H + kSlotMax) * kSlotWords;  // [h]
 
     // Source frame through a buffer resource: loads past the frame return 0.
     const int f = as_const(plan.indices)[it->idx_off + u_p];
@@ -265,148 +254,170 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(PlanView plan, int
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         reinterpret_cast<void*>(fa - lead), (short)0, static_cast<int>(range), 0x00020000);
     const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
-    const bool vlane = t < n_strips;
-    const uint32_t lane_off = lead + kStripBytes * static_cast<uint32_t>(t);
+    const uint32_t lane_off = lead + 3u * static_cast<uint32_t>(x0 + PX * lane);
 
     const float a0 = norm.a[0], a1 = norm.a[1], a2 = norm.a[2];
     const float b0 = norm.b[0], b1 = norm.b[1], b2 = norm.b[2];
 
-    float acc[M][12];
+    // acc[s][q]: the RGB sums of pixel q of the lane in slot s, as a float4
+    // (w stays zero) so that each pixel leaves with one 16-byte LDS write
+    // straight from its registers.
+    f4 acc[M][PX];
 #pragma unroll
     for (int s = 0; s < M; ++s)
 #pragma unroll
-        for (int q = 0; q < 12; ++q) acc[s][q] = 0.f;
+        for (int q = 0; q < PX; ++q) acc[s][q] = f4{0.f, 0.f, 0.f, 0.f};
 
-    int base = i0;        // oldest output row still accumulating, in acc[0]
+    // Output row i accumulates in acc[i % M].  The band starts at the first
+    // source row of output row i0; output rows before i0 that are still open
+    // there collect partial sums, which are discarded when they close.
     const int y0 = ys[i0];
     const int y1 = close_row[i1 - 1] + 1;   // past the frame: zero-weight rows, loads return 0
+    int base = i0;        // next output row to close
+    while (base > 0 && close_row[base - 1] >= y0) --base;
+    int slot = base % M;
+    int next_close = close_row[base];
 
-    auto load_row = [&](int y) __attribute__((always_inline)) -> uint4 {
+    using load_t = typename std::conditional<kLoadDwords == 4, uint4, uint3>::type;
+    auto load_row = [&](int y) __attribute__((always_inline)) -> load_t {
         const uint32_t off = (lane_off + static_cast<uint32_t>(y) * row_bytes) & ~3u;
-        const auto r = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
-        return make_uint4(r[0], r[1], r[2], r[3]);
+        if constexpr (kLoadDwords == 4) {
+            const auto r = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
+            return make_uint4(r[0], r[1], r[2], r[3]);
+        } else {
+            const auto r = __builtin_amdgcn_raw_buffer_load_b96(rsrc, off, 0, 0);
+            return make_uint3(r[0], r[1], r[2]);
+        }
     };
 
     // x pass of output row i, normalise, stage; every 4th row: store.
     auto x_pass = [&](int i) __attribute__((always_inline)) {
-        const float4* row = ring + (ring_slots > 1 ? (i & 1) : 0) * tlen;
         const int yy = i & 3;
-        for (int j = t; j < w; j += nt) {
+        if (xlane) {
             float r0 = 0.f, r1 = 0.f, r2 = 0.f;
-            if (j == t) {
-                const float4* src = row + sj;
+            const float4* src = row + sj;
 #pragma unroll
-                for (int g = 0; g < KX; g += 4) {
-                    // four taps at a time: bounds the LDS values held in registers
-                    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                    for (int k = g; k < g + 4; ++k) {
-                        const float4 q = src[k];
-                        r0 = fmaf(wx[k], q.x, r0);
-                        r1 = fmaf(wx[k], q.y, r1);
-                        r2 = fmaf(wx[k], q.z, r2);
-                    }
-                }
+            for (int g = 0; g < KX; g += 4) {
+                // four taps at a time: bounds the LDS values held in registers
                 __builtin_amdgcn_sched_barrier(0);
-            } else {   // more outputs than lanes: weights from the table
-                const float4* src = row + sx_start[j];
-                const cptr<float> wj = sx_w + int64_t(j) * KX;
+                const float4 wg = wxl[(g / 4) * 64 + lane];
+                const float wk[4] = {wg.x, wg.y, wg.z, wg.w};
 #pragma unroll
-                for (int k = 0; k < KX; ++k) {
-                    const float4 q = src[k];
-                    const float wk = wj[k];
-                    r0 = fmaf(wk, q.x, r0);
-                    r1 = fmaf(wk, q.y, r1);
-                    r2 = fmaf(wk, q.z, r2);
+                for (int k = 0; k < 4; ++k) {
+                    const float4 q = src[g + k];
+                    r0 = fmaf(wk[k], q.x, r0);
+                    r1 = fmaf(wk[k], q.y, r1);
+                    r2 = fmaf(wk[k], q.z, r2);
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);
             const float v0 = fmaf(r0, a0, b0);
             const float v1 = fmaf(r1, a1, b1);
             const float v2 = fmaf(r2, a2, b2);
-            const int e = ((j >> 4) * 3 * 4 + yy) * 16 + (j & 15);
+            elem_t* st = stage + yy * 64 + lane;
             if constexpr (OUT_BF16 != 0) {
-                stage[e] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v0));
-                stage[e + 64] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
-                stage[e + 128] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
+                st[0] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v0));
+                st[256] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
+                st[512] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
             } else {
-                stage[e] = v0;
-                stage[e + 64] = v1;
-                stage[e + 128] = v2;
+                st[0] = v0;
+                st[256] = v1;
+                st[512] = v2;
             }
         }
         if (yy == 3) {
-            __syncthreads();
-            // rows i-3 .. i hold one 64-value run of every (patch column, channel) block
-            constexpr int kChunks = OUT_BF16 ? 8 : 16;   // 16-byte pieces per run
+            wave_lds_fence();
+            // rows i-3 .. i: for each channel c and patch column touched by
+            // the band, four 16-column rows of the patch = one 64-value run;
+            // the band writes the 16-byte pieces of it that it owns
+            constexpr int kPieces = 16 / S;          // pieces per 16-column patch row
+            const int q0 = j0 >> 4;
+            const int nq = ((j0 + nbw + 15) >> 4) - q0;
             const int yq = (i & 15) >> 2;
             const int bh = i >> 5;
             const int mh = (i >> 4) & 1;
-            const int n_runs = (w >> 4) * 3;
             const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + bh) * it->wm * 4 + mh * 2;
-            const uint4* st4 = reinterpret_cast<const uint4*>(stage);
-            for (int e = t; e < n_runs * kChunks; e += nt) {
-                const int run = e / kChunks;
-                const int piece = e - run * kChunks;
-                const int pj = run / 3;
-                const int c = run - pj * 3;
-                const int64_t rho = win_row0 + (pj >> 1) * 4 + (pj & 1);
-                const uint4 val = st4[e];
-                elem_t* dst = static_cast<elem_t*>(out) + rho * kRow + yq * 64;
-                if (both) {
-                    reinterpret_cast<uint4*>(dst + (c * 2) * 256)[piece] = val;
-                    reinterpret_cast<uint4*>(dst + (c * 2 + 1) * 256)[piece] = val;
-                } else {
-                    reinterpret_cast<uint4*>(dst + (c * 2 + dt_self) * 256)[piece] = val;
+            const int n_seg = 3 * nq * 4 * kPieces;
+            for (int e = lane; e < n_seg; e += 64) {
+                const int piece = e % kPieces;
+                const int r4 = e / kPieces;
+                const int ry = r4 & 3;
+                const int cq = r4 >> 2;
+                const int c = cq / nq;
+                const int q = cq - c * nq;
+                const int jabs = (q0 + q) * 16 + piece * S;
+                const int jl = jabs - j0;
+                if (jl >= 0 && jl < nbw) {
+                    const uint4 val = *reinterpret_cast<const uint4*>(stage + (c * 4 + ry) * 64 + jl);
+                    const int64_t rho = win_row0 + ((q0 + q) >> 1) * 4 + ((q0 + q) & 1);
+                    elem_t* dst = static_cast<elem_t*>(out) + rho * kRow + (yq * 4 + ry) * 16 + piece * S;
+                    if (both) {
+                        *reinterpret_cast<uint4*>(dst + (c * 2) * 256) = val;
+                        *reinterpret_cast<uint4*>(dst + (c * 2 + 1) * 256) = val;
+                    } else {
+                        *reinterpret_cast<uint4*>(dst + (c * 2 + dt_self) * 256) = val;
+                    }
                 }
             }
+            wave_lds_fence();
         }
     };
 
-    auto process_row = [&](int y, uint4 cur) __attribute__((always_inline)) {
-        // base only changes in uniform control flow; say so, so that the
-        // table reads below stay scalar loads
-        base = __builtin_amdgcn_readfirstlane(base);
-        const cptr<int32_t> sr = scat + y * kScatterWords;
-        const int first = sr[0];
-        const int cnt = sr[1];
-        const int skip = base - first;
-        const int n = min(cnt, i1 - first) - skip;
-        const cptr<float> wr = (cptr<float>)(sr + 2) + skip;
-        const bool closes = base < i1 && y == close_row[base];
-        if (closes && ring_slots == 1) __syncthreads();   // the previous x pass has read the row
-        if (vlane) {
-            const uint32_t shift = (lead + static_cast<uint32_t>(y) * row_bytes) & 3u;
-            uint32_t d0 = cur.x, d1 = cur.y, d2 = cur.z;
-            if (shift != 0) {
-                d0 = __builtin_amdgcn_alignbyte(cur.y, cur.x, shift);
-                d1 = __builtin_amdgcn_alignbyte(cur.z, cur.y, shift);
-                d2 = __builtin_amdgcn_alignbyte(cur.w, cur.z, shift);
-            }
-            float v[12];
-            v[0] = float(d0 & 255u);
-            v[1] = float((d0 >> 8) & 255u);
-            v[2] = float((d0 >> 16) & 255u);
-            v[3] = float(d0 >> 24);
-            v[4] = float(d1 & 255u);
-            v[5] = float((d1 >> 8) & 255u);
-            v[6] = float((d1 >> 16) & 255u);
-            v[7] = float(d1 >> 24);
-            v[8] = float(d2 & 255u);
-            v[9] = float((d2 >> 8) & 255u);
-            v[10] = float((d2 >> 16) & 255u);
-            v[11] = float(d2 >> 24);
-            if (!closes) {
-                add_row<M>(acc, v, wr, n);
-            } else {
-                float done[12];
-                add_row_and_close<M>(acc, v, wr, done);
-                put_row(done, ring + (ring_slots > 1 ? (base & 1) : 0) * tlen + 4 * t);
+    auto process_row = [&](int y, load_t cur) __attribute__((always_inline)) {
+        const uint32_t shift = (lane_off + static_cast<uint32_t>(y) * row_bytes) & 3u;
+        uint32_t d[kLoadDwords];
+        d[0] = cur.x;
+        d[1] = cur.y;
+        d[2] = cur.z;
+        if constexpr (kLoadDwords == 4) d[3] = cur.w;
+        // the lane's 3*PX bytes, from byte `shift` on
+        constexpr int kWords = (V + 3) / 4;
+        uint32_t b[kWords];
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) {
+            if constexpr (true) {
+                if (k + 1 < kLoadDwords) b[k] = __builtin_amdgcn_alignbyte(d[k + 1 < kLoadDwords ? k + 1 : k], d[k], shift);
+                else b[k] = d[k] >> (8 * shift);
             }
         }
-        if (closes) {
-            __syncthreads();
-            x_pass(base);
+        float v[V];
+#pragma unroll
+        for (int q = 0; q < V; ++q) v[q] = float((b[q >> 2] >> (8 * (q & 3))) & 255u);
+        // every slot takes this row with its weight (zero where its output row does not read it)
+        const cptr<float> wr = slot_w + y * kSlotWords;
+#pragma unroll
+        for (int s = 0; s < M; ++s) {
+            const float ws = wr[s];
+#pragma unroll
+            for (int q = 0; q < PX; ++q) {
+                acc[s][q].x = fmaf(ws, v[3 * q], acc[s][q].x);
+                acc[s][q].y = fmaf(ws, v[3 * q + 1], acc[s][q].y);
+                acc[s][q].z = fmaf(ws, v[3 * q + 2], acc[s][q].z);
+            }
+        }
+        if (y == next_close) {   // wave-uniform
+            const bool keep = base >= i0;
+            if (keep) wave_lds_fence();
+            // the closing slot goes to the wave's LDS row (kept rows only) and
+            // restarts at zero; each case names its registers statically
+#pragma unroll
+            for (int s = 0; s < M; ++s) {
+                if (slot == s) {
+                    if (keep) {
+#pragma unroll
+                        for (int q = 0; q < PX; ++q) reinterpret_cast<f4*>(row)[PX * lane + q] = acc[s][q];
+                    }
+#pragma unroll
+                    for (int q = 0; q < PX; ++q) acc[s][q] = f4{0.f, 0.f, 0.f, 0.f};
+                }
+            }
+            if (keep) {
+                wave_lds_fence();
+                x_pass(base);
+            }
             ++base;
+            slot = slot + 1 == M ? 0 : slot + 1;
+            next_close = close_row[base];
         }
     };
 
@@ -414,39 +425,39 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(PlanView plan, int
     // or the frame is harmless (in-frame data that is never used, or zeros
     // from the buffer's range check), and an unconditional load keeps every
     // prefetch register in place.
-    uint4 pf[kPrefetch];
+    load_t pf[kPrefetch];
 #pragma unroll
-    for (int d = 0; d < kPrefetch; ++d) pf[d] = load_row(y0 + d);
+    for (int k = 0; k < kPrefetch; ++k) pf[k] = load_row(y0 + k);
 
     for (int yb = y0; yb < y1; yb += kPrefetch) {
 #pragma unroll
-        for (int d = 0; d < kPrefetch; ++d) {
-            const int y = yb + d;
+        for (int k = 0; k < kPrefetch; ++k) {
+            const int y = yb + k;
             if (y < y1) {
-                const uint4 cur = pf[d];
-                pf[d] = load_row(y + kPrefetch);
+                const load_t cur = pf[k];
+                pf[k] = load_row(y + kPrefetch);
                 process_row(y, cur);
             }
         }
     }
 }
 
-template <int M, int KX>
+template <int M, int KX, int PX>
 int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                         const Norm& norm, hipStream_t stream) {
-    const int slots = L.slots;
-    const int lds = L.ring_bytes + L.stage_elems * (out_dtype == 1 ? 2 : 4);
+    const int waves = L.threads / 64;
+    const int lds = waves * stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4);
     dim3 grid(L.count), block(L.threads);
     if (out_dtype == 1) {
-        auto k = stream_kernel<M, KX, 1>;
+        auto k = stream_kernel<M, KX, PX, 1>;
         if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        hipLaunchKernelGGL(k, grid, block, lds, stream, plan, L.first, slots, out, norm);
+        hipLaunchKernelGGL(k, grid, block, lds, stream, plan, L.first, out, norm);
     } else {
-        auto k = stream_kernel<M, KX, 0>;
+        auto k = stream_kernel<M, KX, PX, 0>;
         if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        hipLaunchKernelGGL(k, grid, block, lds, stream, plan, L.first, slots, out, norm);
+        hipLaunchKernelGGL(k, grid, block, lds, stream, plan, L.first, out, norm);
     }
     return static_cast<int>(hipGetLastError());
 }
@@ -464,21 +475,30 @@ int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& n
     return static_cast<int>(hipGetLastError());
 }
 
-bool stream_shape_supported(int m, int kx) {
-    return m >= 4 && m <= 6 && (kx == 4 || kx == 8 || kx == 12 || kx == 16);
+// Compiled shapes: every (M, KX) with 2 pixels per lane, and with 3 pixels
+// per lane where the accumulators still fit the registers of a 1024-thread
+// block (M <= 5).
+bool stream_shape_supported(int m, int kx, int px) {
+    if (m < 4 || m > 6 || (kx != 4 && kx != 8 && kx != 12 && kx != 16)) return false;
+    return px == 2 || (px == 3 && m <= 5);
 }
 
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream) {
     if (L.count <= 0) return 0;
-    if (L.threads <= 0 || L.threads > kStreamBlock || L.threads % 64 != 0 ||
-        (L.slots != 1 && L.slots != 2))
+    if (L.threads <= 0 || L.threads > kStreamMaxThreads || L.threads % 64 != 0)
         return static_cast<int>(hipErrorInvalidConfiguration);
-#define VP_STREAM_CASE(MM, KK) \
-    if (L.m == MM && L.kx == KK) return launch_stream_shape<MM, KK>(plan, L, out, out_dtype, norm, stream);
-    VP_STREAM_CASE(4, 4) VP_STREAM_CASE(4, 8) VP_STREAM_CASE(4, 12) VP_STREAM_CASE(4, 16)
-    VP_STREAM_CASE(5, 4) VP_STREAM_CASE(5, 8) VP_STREAM_CASE(5, 12) VP_STREAM_CASE(5, 16)
-    VP_STREAM_CASE(6, 4) VP_STREAM_CASE(6, 8) VP_STREAM_CASE(6, 12) VP_STREAM_CASE(6, 16)
+    if (!stream_shape_supported(L.m, L.kx, L.px) ||
+        L.threads / 64 * stream_wave_bytes(L.px, L.kx, 4) > kStreamLdsBudget)
+        return static_cast<int>(hipErrorInvalidConfiguration);
+#define VP_STREAM_CASE(MM, KK, PP) \
+    if (L.m == MM && L.kx == KK && L.px == PP) \
+        return launch_stream_shape<MM, KK, PP>(plan, L, out, out_dtype, norm, stream);
+#define VP_STREAM_KX(MM, PP) \
+    VP_STREAM_CASE(MM, 4, PP) VP_STREAM_CASE(MM, 8, PP) VP_STREAM_CASE(MM, 12, PP) VP_STREAM_CASE(MM, 16, PP)
+    VP_STREAM_KX(4, 2) VP_STREAM_KX(5, 2) VP_STREAM_KX(6, 2)
+    VP_STREAM_KX(4, 3) VP_STREAM_KX(5, 3)
+#undef VP_STREAM_KX
 #undef VP_STREAM_CASE
     return static_cast<int>(hipErrorInvalidValue);
 }

@@ -14,20 +14,22 @@
 // Tables (word offsets into `tables`; items with the same axis share them):
 //   window table of an axis n_in -> n_out, K taps:
 //       int32 start[n_out]; int32 count[n_out]; float weight[n_out][K]
-//   row-scatter table of a y axis n_in -> n_out (streaming kernel):
-//       [n_in + 6] rows of 16 words: int32 first; int32 count; float weight[14]
-//         -- output rows first .. first+count-1 read source row y, with the first
-//            count weights; the rest are zero (so that weight[skip + m] is zero
-//            for every m < 6 past the count)
+//   slot table of a y axis n_in -> n_out (streaming kernel), M slots:
+//       [n_in + 6] rows of 8 words: float weight[slot]   (slots >= M zero)
+//         -- output row i is accumulated in slot i mod M from the first row of
+//            its window to its close row; weight[s] is the weight of source
+//            row y in the output row that has slot s at y, or zero
 //       int32 close_row[n_out + 1]   (the last entry is padding)
 //         -- the row after which output row i is complete: the last row of its
 //            window, except that output rows whose windows all end at the bottom
 //            border close on consecutive rows n_in-1, n_in, n_in+1, ...; rows past
-//            n_in carry zero weights for the rows still open (one close per row)
-//   column table of an x axis (streaming kernel), KX taps:
+//            n_in carry zero weights (one close per row)
+//   column table of an x axis (streaming kernel), KX taps, for output bands
+//   of `band` columns whose source pixels fit an LDS row of `row_px` pixels:
 //       int32 start[n_out]; float weight[n_out][KX]
-//     -- start + KX never passes the streaming kernel's LDS row; weights are
-//        shifted and zero-padded to match.
+//     -- start is relative to the first source pixel of the output's band
+//        (the window start of the band's first column) and start + KX never
+//        passes row_px; weights are shifted and zero-padded to match.
 #pragma once
 
 #include <cstdint>
@@ -42,11 +44,17 @@ constexpr int kRow = 1536;            // 3 * 2 * 16 * 16
 constexpr int kWinElems = 4 * kRow;   // one merge window of one frame pair
 constexpr int kGenericThreads = 256;
 constexpr int kGenericTCap = 8192;    // floats of the general kernel's LDS column tile
-constexpr int kScatterWords = 16;     // words per source row of a row-scatter table
-constexpr int kScatterMax = 6;        // weights per source row (output rows reading it)
-constexpr int kStripBytes = 12;       // bytes of a source row per streaming lane (4 pixels)
-constexpr int kStreamMaxThreads = 512;  // largest streaming block (launch bound)
+constexpr int kSlotWords = 8;         // words per source row of a slot table
+constexpr int kSlotMax = 6;           // most output rows open at once (accumulator slots)
+constexpr int kStreamMaxThreads = 1024;  // largest streaming block: 16 bands of one frame
 constexpr int kStreamLdsBudget = 160 * 1024;  // LDS of one gfx950 workgroup
+
+// LDS of one streaming wave: its source row (64 * px float4 pixels), the
+// stage of four output rows (3 channels x 4 rows x 64 columns) and the
+// column weights of its lanes (kx floats each).
+constexpr int stream_wave_bytes(int px, int kx, int elem_bytes) {
+    return 64 * px * 16 + 3 * 4 * 64 * elem_bytes + 64 * kx * 4;
+}
 
 // Kernel an item is routed to.
 enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1 };
@@ -62,15 +70,15 @@ struct DevItem {
     int32_t ky, kx;          // tap stride of those tables
     int32_t rh, cw;          // general kernel: output rows / columns per LDS sub-tile
     int32_t route;
-    int32_t n_strips;        // streaming kernel: lanes that read a source row, ceil(W / 4)
-    int32_t sy_off, sx_off;  // streaming kernel: row-scatter and column tables
-    int32_t tlen;            // streaming kernel: pixels of one LDS row
+    int32_t band;            // streaming kernel: output columns per wave (multiple of 8, <= 64)
+    int32_t sy_off, sx_off;  // streaming kernel: slot and column tables
+    int32_t row_px;          // streaming kernel: source pixels per wave row (64 * px)
     int32_t pad0;
 };
 static_assert(sizeof(DevItem) == 104, "DevItem layout");
 
-// One streaming work unit: output rows [i0, i1) of padded frame position p
-// of an item.  flags bit 0: the pair's two frames are the same source frame
+// One streaming work unit (one workgroup, one wave per column band): output
+// rows [i0, i1) of padded frame position p of an item.  flags bit 0: the pair's two frames are the same source frame
 // (an image, or an odd count padded with its last index), so the unit
 // writes both temporal halves of the rows.
 struct StreamUnit {
@@ -100,11 +108,8 @@ struct Norm {
 // with the same template shape and block size.
 struct StreamLaunch {
     int32_t first, count;
-    int32_t m, kx;           // rotating accumulators, column taps
-    int32_t threads;         // block size, multiple of 64
-    int32_t slots;           // LDS rows handed from the y pass to the x pass (1 or 2)
-    int32_t ring_bytes;      // LDS of those rows (largest item of the launch)
-    int32_t stage_elems;     // output values staged per four rows (largest item)
+    int32_t m, kx, px;       // rotating accumulators, column taps, pixels per lane
+    int32_t threads;         // block size: 64 per column band
 };
 
 // Kernel launchers (vp_kernels.hip).  Return a hipError_t value.
@@ -112,7 +117,7 @@ int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& n
                    hipStream_t stream);
 int launch_stream(const PlanView& plan, const StreamLaunch& launch, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream);
-// Whether a (m, kx) shape has a compiled streaming kernel.
-bool stream_shape_supported(int m, int kx);
+// Whether a (m, kx, px) shape has a compiled streaming kernel.
+bool stream_shape_supported(int m, int kx, int px);
 
 }  // namespace vp
