@@ -272,8 +272,9 @@ int32_t band_span(const AxisFilter& fx, int32_t band) {
 }
 
 // Whether an item can take the streaming kernel, and with which shape: the
-// output width is cut into bands of at most 64 columns (one wave each, one
-// lane per column in the x pass), each band's source pixels must fit 64
+// output width is cut into bands of 16, 32, 48 or 64 columns (whole patches;
+// one wave each, one lane per column in the x pass), each band's source
+// pixels must fit 64
 // lanes of px pixels, and among the shapes that fit the one with the least
 // estimated lane work is taken.  The LDS budget is checked with float32
 // staging, so the routing does not depend on the output type.
@@ -285,7 +286,7 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShap
     // every load of a frame row (up to kSlotMax + 8 rows past the last one) stays below 4 GiB
     if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
     int64_t best = -1;
-    for (int32_t band = 64; band >= 8; band -= 8) {
+    for (int32_t band = 64; band >= 16; band -= 16) {
         const int32_t waves = (it.dst_w + band - 1) / band;
         if (waves * 64 > vp::kStreamMaxThreads) break;
         const int32_t span = band_span(fx, band);

@@ -251,8 +251,6 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
     // dword, and the dword holding the frame's last byte lies in that byte's
     // (4-byte aligned) page, so it is always readable.
     const uint32_t range = static_cast<uint32_t>((it->frame_bytes + lead + 3) & ~int64_t(3));
-    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        reinterpret_cast<void*>(fa - lead), (short)0, static_cast<int>(range), 0x00020000);
     const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
     const uint32_t lane_off = lead + 3u * static_cast<uint32_t>(x0 + PX * lane);
 
@@ -278,14 +276,39 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
     int slot = base % M;
     int next_close = close_row[base];
 
+    // Rows are visited in blocks of four starting at a multiple of 4, so
+    // that y % 4 = k is known at every step: the lane's byte offset inside
+    // row y is then voff[k] (dword aligned) + shf[k] (0..3), with the row
+    // block's own offset, a multiple of 4, added as a scalar.
     using load_t = typename std::conditional<kLoadDwords == 4, uint4, uint3>::type;
-    auto load_row = [&](int y) __attribute__((always_inline)) -> load_t {
-        const uint32_t off = (lane_off + static_cast<uint32_t>(y) * row_bytes) & ~3u;
+    uint32_t voff[kPrefetch], shf[kPrefetch];
+#pragma unroll
+    for (int k = 0; k < kPrefetch; ++k) {
+        const uint32_t c = lane_off + static_cast<uint32_t>(k) * row_bytes;
+        voff[k] = c & ~3u;
+        shf[k] = c & 3u;
+    }
+    // The block's rows get a buffer resource of their own, based at the
+    // block's first row (a multiple of 4 bytes past the frame base, since yb
+    // is a multiple of 4) with the rest of the frame as its range: all
+    // per-row address arithmetic is scalar.
+    auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> load_t {
+        // (the row block is wave-uniform; say so, or the descriptor would be
+        // built per lane)
+        const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
+        const int64_t left = int64_t(range) - int64_t(o);
+        const uint32_t n = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(left > 0 ? left : 0));
+        const uintptr_t bp = fa - lead + o;
+        const uint32_t bp_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
+        const uint32_t bp_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
+        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+            reinterpret_cast<void*>((uintptr_t(bp_hi) << 32) | bp_lo), (short)0, static_cast<int>(n),
+            0x00020000);
         if constexpr (kLoadDwords == 4) {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
+            const auto r = __builtin_amdgcn_raw_buffer_load_b128(rb, voff[k], 0, 0);
             return make_uint4(r[0], r[1], r[2], r[3]);
         } else {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b96(rsrc, off, 0, 0);
+            const auto r = __builtin_amdgcn_raw_buffer_load_b96(rb, voff[k], 0, 0);
             return make_uint3(r[0], r[1], r[2]);
         }
     };
@@ -327,58 +350,51 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
         }
         if (yy == 3) {
             wave_lds_fence();
-            // rows i-3 .. i: for each channel c and patch column touched by
-            // the band, four 16-column rows of the patch = one 64-value run;
-            // the band writes the 16-byte pieces of it that it owns
-            constexpr int kPieces = 16 / S;          // pieces per 16-column patch row
-            const int q0 = j0 >> 4;
-            const int nq = ((j0 + nbw + 15) >> 4) - q0;
+            // rows i-3 .. i: for each patch column q of the band and channel
+            // c, four 16-column rows of the patch = one 64-value run, written
+            // as 16-byte pieces, 16/S pieces per patch row
+            constexpr int kPieces = 16 / S;
+            constexpr int kPerPatch = 3 * 4 * kPieces;
             const int yq = (i & 15) >> 2;
             const int bh = i >> 5;
             const int mh = (i >> 4) & 1;
             const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + bh) * it->wm * 4 + mh * 2;
-            const int n_seg = 3 * nq * 4 * kPieces;
+            const int n_seg = (nbw >> 4) * kPerPatch;
             for (int e = lane; e < n_seg; e += 64) {
-                const int piece = e % kPieces;
-                const int r4 = e / kPieces;
-                const int ry = r4 & 3;
-                const int cq = r4 >> 2;
-                const int c = cq / nq;
-                const int q = cq - c * nq;
-                const int jabs = (q0 + q) * 16 + piece * S;
-                const int jl = jabs - j0;
-                if (jl >= 0 && jl < nbw) {
-                    const uint4 val = *reinterpret_cast<const uint4*>(stage + (c * 4 + ry) * 64 + jl);
-                    const int64_t rho = win_row0 + ((q0 + q) >> 1) * 4 + ((q0 + q) & 1);
-                    elem_t* dst = static_cast<elem_t*>(out) + rho * kRow + (yq * 4 + ry) * 16 + piece * S;
-                    if (both) {
-                        *reinterpret_cast<uint4*>(dst + (c * 2) * 256) = val;
-                        *reinterpret_cast<uint4*>(dst + (c * 2 + 1) * 256) = val;
-                    } else {
-                        *reinterpret_cast<uint4*>(dst + (c * 2 + dt_self) * 256) = val;
-                    }
+                const int q = e / kPerPatch;
+                const int r = e - q * kPerPatch;
+                const int c = r / (4 * kPieces);
+                const int ry = (r / kPieces) & 3;
+                const int piece = r % kPieces;
+                const uint4 val = *reinterpret_cast<const uint4*>(stage + (c * 4 + ry) * 64 + q * 16 + piece * S);
+                const int qa = (j0 >> 4) + q;
+                const int64_t rho = win_row0 + (qa >> 1) * 4 + (qa & 1);
+                elem_t* dst = static_cast<elem_t*>(out) + rho * kRow + (yq * 4 + ry) * 16 + piece * S;
+                if (both) {
+                    *reinterpret_cast<uint4*>(dst + (c * 2) * 256) = val;
+                    *reinterpret_cast<uint4*>(dst + (c * 2 + 1) * 256) = val;
+                } else {
+                    *reinterpret_cast<uint4*>(dst + (c * 2 + dt_self) * 256) = val;
                 }
             }
             wave_lds_fence();
         }
     };
 
-    auto process_row = [&](int y, load_t cur) __attribute__((always_inline)) {
-        const uint32_t shift = (lane_off + static_cast<uint32_t>(y) * row_bytes) & 3u;
+    auto process_row = [&](int y, load_t cur, uint32_t shift) __attribute__((always_inline)) {
         uint32_t d[kLoadDwords];
         d[0] = cur.x;
         d[1] = cur.y;
         d[2] = cur.z;
         if constexpr (kLoadDwords == 4) d[3] = cur.w;
-        // the lane's 3*PX bytes, from byte `shift` on
+        // the lane's 3*PX bytes, from byte `shift` on (the last word needs
+        // only its low byte when it has no successor: rotate it in place)
         constexpr int kWords = (V + 3) / 4;
         uint32_t b[kWords];
 #pragma unroll
         for (int k = 0; k < kWords; ++k) {
-            if constexpr (true) {
-                if (k + 1 < kLoadDwords) b[k] = __builtin_amdgcn_alignbyte(d[k + 1 < kLoadDwords ? k + 1 : k], d[k], shift);
-                else b[k] = d[k] >> (8 * shift);
-            }
+            const int hi = k + 1 < kLoadDwords ? k + 1 : k;
+            b[k] = __builtin_amdgcn_alignbyte(d[hi], d[k], shift);
         }
         float v[V];
 #pragma unroll
@@ -421,23 +437,22 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
         }
     };
 
-    // Rows are loaded kPrefetch ahead, unconditionally: a load past the band
-    // or the frame is harmless (in-frame data that is never used, or zeros
-    // from the buffer's range check), and an unconditional load keeps every
-    // prefetch register in place.
+    // Rows are loaded one block (four rows) ahead, unconditionally: a load
+    // past the band or the frame is harmless (in-frame data that is never
+    // used, or zeros from the buffer's range check), and an unconditional
+    // load keeps every prefetch register in place.
+    const int yb0 = y0 & ~3;
     load_t pf[kPrefetch];
 #pragma unroll
-    for (int k = 0; k < kPrefetch; ++k) pf[k] = load_row(y0 + k);
+    for (int k = 0; k < kPrefetch; ++k) pf[k] = load_row(yb0, k);
 
-    for (int yb = y0; yb < y1; yb += kPrefetch) {
+    for (int yb = yb0; yb < y1; yb += kPrefetch) {
 #pragma unroll
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
-            if (y < y1) {
-                const load_t cur = pf[k];
-                pf[k] = load_row(y + kPrefetch);
-                process_row(y, cur);
-            }
+            const load_t cur = pf[k];
+            pf[k] = load_row(yb + kPrefetch, k);
+            if (y >= y0 && y < y1) process_row(y, cur, shf[k]);
         }
     }
 }

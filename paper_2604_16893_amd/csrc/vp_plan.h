@@ -70,7 +70,7 @@ struct DevItem {
     int32_t ky, kx;          // tap stride of those tables
     int32_t rh, cw;          // general kernel: output rows / columns per LDS sub-tile
     int32_t route;
-    int32_t band;            // streaming kernel: output columns per wave (multiple of 8, <= 64)
+    int32_t band;            // streaming kernel: output columns per wave (16, 32, 48 or 64)
     int32_t sy_off, sx_off;  // streaming kernel: slot and column tables
     int32_t row_px;          // streaming kernel: source pixels per wave row (64 * px)
     int32_t pad0;
