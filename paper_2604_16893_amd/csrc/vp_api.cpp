@@ -255,7 +255,7 @@ void build_columns(const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px
 }
 
 struct StreamShape {
-    int32_t m = 0, kx = 0, px = 0, band = 0, threads = 0;
+    int32_t m = 0, kx = 0, px = 0, band = 0, bands = 0;
 };
 
 int32_t round_up(int32_t v, int32_t q) { return (v + q - 1) / q * q; }
@@ -273,11 +273,11 @@ int32_t band_span(const AxisFilter& fx, int32_t band) {
 
 // Whether an item can take the streaming kernel, and with which shape: the
 // output width is cut into bands of 16, 32, 48 or 64 columns (whole patches;
-// one wave each, one lane per column in the x pass), each band's source
-// pixels must fit 64
-// lanes of px pixels, and among the shapes that fit the one with the least
-// estimated lane work is taken.  The LDS budget is checked with float32
-// staging, so the routing does not depend on the output type.
+// one single-wave workgroup each, one lane per column in the x pass), each
+// band's source pixels must fit 64 lanes of px pixels, and among the shapes
+// that fit, the one with the least estimated lane work is taken.  The LDS
+// budget is checked with float32 staging, so the routing does not depend on
+// the output type.
 bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
     if (it.src_h < it.dst_h) return false;                 // vertical upscale: general kernel
     if (m < 4 || m > vp::kSlotMax) return false;
@@ -288,12 +288,11 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShap
     int64_t best = -1;
     for (int32_t band = 64; band >= 16; band -= 16) {
         const int32_t waves = (it.dst_w + band - 1) / band;
-        if (waves * 64 > vp::kStreamMaxThreads) break;
         const int32_t span = band_span(fx, band);
         for (int32_t px = 2; px <= 4; ++px) {
             if (!vp::stream_shape_supported(mm, kx, px)) continue;
             if (span > 64 * px || kx > 64 * px) continue;
-            if (int64_t(waves) * vp::stream_wave_bytes(px, kx, 4) > vp::kStreamLdsBudget) continue;
+            if (vp::stream_wave_bytes(px, kx, 4) > vp::kStreamLdsBudget) continue;
             const int64_t cost = int64_t(waves) * (int64_t(it.src_h) * px * 3 * (mm + 1) +
                                                     int64_t(it.dst_h) * (3 * kx + 12));
             if (best < 0 || cost < best) {
@@ -302,7 +301,7 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShap
                 sh->kx = kx;
                 sh->px = px;
                 sh->band = band;
-                sh->threads = waves * 64;
+                sh->bands = waves;
             }
             break;   // a wider px only adds idle lanes
         }
@@ -450,7 +449,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
                 for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
                     const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
                     Keyed k;
-                    k.key = std::make_tuple(sh.m, sh.kx, sh.px, sh.threads);
+                    k.key = std::make_tuple(sh.m, sh.kx, sh.px, sh.bands);
                     k.unit.item = b;
                     k.unit.p = 2 * tt + dt;
                     k.unit.rows = i0 | (i1 << 16);
@@ -472,7 +471,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
             L.m = std::get<0>(keyed[k].key);
             L.kx = std::get<1>(keyed[k].key);
             L.px = std::get<2>(keyed[k].key);
-            L.threads = std::get<3>(keyed[k].key);
+            L.bands = std::get<3>(keyed[k].key);
             p->launches.push_back(L);
         }
         vp::StreamLaunch& L = p->launches.back();

@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
 
 constexpr int kPrefetch = 4;           // source rows in flight per lane
 
-using f4 = float __attribute__((ext_vector_type(4)));
+using f3 = float __attribute__((ext_vector_type(3)));
 
 // Orders this wave's LDS accesses before and after it.  LDS operations of
 // one wave execute in issue order, so within a wave keeping the compiler from
@@ -189,19 +189,36 @@ __device__ __forceinline__ void wave_lds_fence() {
 //     band's part of one 64-value run; it leaves as 16-byte stores, eight
 //     lanes per 128-byte run.
 template <int M, int KX, int PX, int OUT_BF16>
-__global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan, int unit0,
-                                                                   void* out, Norm norm) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(M * PX > 12 ? 4 : 5)))
+void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out, Norm norm) {
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
     constexpr int kRowPx = 64 * PX;
-    constexpr int kWaveBytes = stream_wave_bytes(PX, KX, sizeof(elem_t));
     constexpr int V = 3 * PX;                      // values per lane per source row
     constexpr int kLoadDwords = PX == 4 ? 4 : 3;   // 3*PX bytes plus up to 3 of misalignment
     constexpr int S = 16 / int(sizeof(elem_t));    // output columns per 16-byte store
     extern __shared__ __align__(16) unsigned char smem[];
 
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const cptr<StreamUnit> up = as_const(plan.units) + unit0 + blockIdx.x;
+    const int lane = threadIdx.x;
+    // Workgroup -> (unit, column band).  Consecutive workgroups go to the
+    // eight XCDs in turn; while the unit count allows, the bands of one unit
+    // are given ids that fall on the same XCD, so that the source pixels two
+    // neighbouring bands share are fetched once into that XCD's L2.
+    int u, wave;
+    {
+        const int g = blockIdx.x;
+        const int full = (n_units >> 3) * 8 * n_bands;
+        if (g < full) {
+            const int r = g >> 3;
+            u = (r / n_bands) * 8 + (g & 7);
+            wave = r % n_bands;
+        } else {
+            u = (n_units & ~7) + (g - full) / n_bands;
+            wave = (g - full) % n_bands;
+        }
+        u = __builtin_amdgcn_readfirstlane(u);
+        wave = __builtin_amdgcn_readfirstlane(wave);
+    }
+    const cptr<StreamUnit> up = as_const(plan.units) + unit0 + u;
     const int u_item = up->item, u_p = up->p, u_rows = up->rows, u_flags = up->flags;
     const cptr<DevItem> it = as_const(plan.items) + u_item;
     const int i0 = u_rows & 0xffff;
@@ -214,7 +231,7 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
     const int dt_self = u_p & 1;
     const bool both = (u_flags & 1) != 0;
 
-    unsigned char* wbase = smem + wave * kWaveBytes;
+    unsigned char* wbase = smem;
     float4* row = reinterpret_cast<float4*>(wbase);                                   // [kRowPx]
     elem_t* stage = reinterpret_cast<elem_t*>(wbase + kRowPx * 16);                   // [3][4][64]
     float4* wxl = reinterpret_cast<float4*>(wbase + kRowPx * 16 + 3 * 4 * 64 * sizeof(elem_t));  // [KX/4][64]
@@ -257,14 +274,14 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
     const float a0 = norm.a[0], a1 = norm.a[1], a2 = norm.a[2];
     const float b0 = norm.b[0], b1 = norm.b[1], b2 = norm.b[2];
 
-    // acc[s][q]: the RGB sums of pixel q of the lane in slot s, as a float4
-    // (w stays zero) so that each pixel leaves with one 16-byte LDS write
-    // straight from its registers.
-    f4 acc[M][PX];
+    // acc[s][q]: the RGB sums of pixel q of the lane in slot s, as a float3
+    // so that each pixel leaves with one 12-byte LDS write straight from its
+    // registers.
+    f3 acc[M][PX];
 #pragma unroll
     for (int s = 0; s < M; ++s)
 #pragma unroll
-        for (int q = 0; q < PX; ++q) acc[s][q] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < PX; ++q) acc[s][q] = f3{0.f, 0.f, 0.f};
 
     // Output row i accumulates in acc[i % M].  The band starts at the first
     // source row of output row i0; output rows before i0 that are still open
@@ -421,10 +438,10 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
                 if (slot == s) {
                     if (keep) {
 #pragma unroll
-                        for (int q = 0; q < PX; ++q) reinterpret_cast<f4*>(row)[PX * lane + q] = acc[s][q];
+                        for (int q = 0; q < PX; ++q) *reinterpret_cast<f3*>(row + PX * lane + q) = acc[s][q];
                     }
 #pragma unroll
-                    for (int q = 0; q < PX; ++q) acc[s][q] = f4{0.f, 0.f, 0.f, 0.f};
+                    for (int q = 0; q < PX; ++q) acc[s][q] = f3{0.f, 0.f, 0.f};
                 }
             }
             if (keep) {
@@ -460,20 +477,14 @@ __global__ __launch_bounds__(kStreamMaxThreads) void stream_kernel(PlanView plan
 template <int M, int KX, int PX>
 int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                         const Norm& norm, hipStream_t stream) {
-    const int waves = L.threads / 64;
-    const int lds = waves * stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4);
-    dim3 grid(L.count), block(L.threads);
-    if (out_dtype == 1) {
-        auto k = stream_kernel<M, KX, PX, 1>;
-        if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        hipLaunchKernelGGL(k, grid, block, lds, stream, plan, L.first, out, norm);
-    } else {
-        auto k = stream_kernel<M, KX, PX, 0>;
-        if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        hipLaunchKernelGGL(k, grid, block, lds, stream, plan, L.first, out, norm);
-    }
+    const int lds = stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4);
+    dim3 grid(static_cast<unsigned>(L.count) * static_cast<unsigned>(L.bands)), block(64);
+    if (out_dtype == 1)
+        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1>), grid, block, lds, stream, plan, L.first, L.count,
+                           L.bands, out, norm);
+    else
+        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 0>), grid, block, lds, stream, plan, L.first, L.count,
+                           L.bands, out, norm);
     return static_cast<int>(hipGetLastError());
 }
 
@@ -501,10 +512,9 @@ bool stream_shape_supported(int m, int kx, int px) {
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream) {
     if (L.count <= 0) return 0;
-    if (L.threads <= 0 || L.threads > kStreamMaxThreads || L.threads % 64 != 0)
+    if (L.bands <= 0 || int64_t(L.count) * L.bands > INT32_MAX)
         return static_cast<int>(hipErrorInvalidConfiguration);
-    if (!stream_shape_supported(L.m, L.kx, L.px) ||
-        L.threads / 64 * stream_wave_bytes(L.px, L.kx, 4) > kStreamLdsBudget)
+    if (!stream_shape_supported(L.m, L.kx, L.px) || stream_wave_bytes(L.px, L.kx, 4) > kStreamLdsBudget)
         return static_cast<int>(hipErrorInvalidConfiguration);
 #define VP_STREAM_CASE(MM, KK, PP) \
     if (L.m == MM && L.kx == KK && L.px == PP) \

@@ -46,10 +46,9 @@ constexpr int kGenericThreads = 256;
 constexpr int kGenericTCap = 8192;    // floats of the general kernel's LDS column tile
 constexpr int kSlotWords = 8;         // words per source row of a slot table
 constexpr int kSlotMax = 6;           // most output rows open at once (accumulator slots)
-constexpr int kStreamMaxThreads = 1024;  // largest streaming block: 16 bands of one frame
-constexpr int kStreamLdsBudget = 160 * 1024;  // LDS of one gfx950 workgroup
+constexpr int kStreamLdsBudget = 64 * 1024;   // LDS of one streaming workgroup (one wave)
 
-// LDS of one streaming wave: its source row (64 * px float4 pixels), the
+// LDS of one streaming workgroup (one wave): its source row (64 * px float4 pixels), the
 // stage of four output rows (3 channels x 4 rows x 64 columns) and the
 // column weights of its lanes (kx floats each).
 constexpr int stream_wave_bytes(int px, int kx, int elem_bytes) {
@@ -77,8 +76,8 @@ struct DevItem {
 };
 static_assert(sizeof(DevItem) == 104, "DevItem layout");
 
-// One streaming work unit (one workgroup, one wave per column band): output
-// rows [i0, i1) of padded frame position p of an item.  flags bit 0: the pair's two frames are the same source frame
+// One streaming work unit: output rows [i0, i1) of padded frame position p
+// of an item; one single-wave workgroup per column band of the unit.  flags bit 0: the pair's two frames are the same source frame
 // (an image, or an odd count padded with its last index), so the unit
 // writes both temporal halves of the rows.
 struct StreamUnit {
@@ -108,8 +107,8 @@ struct Norm {
 // with the same template shape and block size.
 struct StreamLaunch {
     int32_t first, count;
-    int32_t m, kx, px;       // rotating accumulators, column taps, pixels per lane
-    int32_t threads;         // block size: 64 per column band
+    int32_t m, kx, px;       // accumulator slots, column taps, pixels per lane
+    int32_t bands;           // column bands per unit (workgroups per unit)
 };
 
 // Kernel launchers (vp_kernels.hip).  Return a hipError_t value.
