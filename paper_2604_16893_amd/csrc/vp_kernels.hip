@@ -189,7 +189,7 @@ __device__ __forceinline__ void wave_lds_fence() {
 //     band's part of one 64-value run; it leaves as 16-byte stores, eight
 //     lanes per 128-byte run.
 template <int M, int KX, int PX, int OUT_BF16>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(M * PX > 12 ? 4 : 5)))
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(M * PX > 12 || 3 * M * PX + KX >= 52 ? 4 : 5)))
 void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out, Norm norm) {
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
     constexpr int kRowPx = 64 * PX;
@@ -234,24 +234,20 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
     unsigned char* wbase = smem;
     float4* row = reinterpret_cast<float4*>(wbase);                                   // [kRowPx]
     elem_t* stage = reinterpret_cast<elem_t*>(wbase + kRowPx * 16);                   // [3][4][64]
-    float4* wxl = reinterpret_cast<float4*>(wbase + kRowPx * 16 + 3 * 4 * 64 * sizeof(elem_t));  // [KX/4][64]
 
-    // x pass: output column j0 + lane; its KX column weights wait in the
-    // wave's LDS, four per 16-byte word, one word per lane per group.
+    // x pass: output column j0 + lane keeps its KX column weights in registers.
     const cptr<int32_t> tables = as_const(plan.tables);
     const cptr<int32_t> sx_start = tables + it->sx_off;
     const cptr<float> sx_w = (cptr<float>)(sx_start + w);
     const bool xlane = lane < nbw;
     int sj = 0;
+    float wx[KX];
     {
         const int jx = xlane ? j0 + lane : w - 1;   // idle lanes read a valid entry, keep zeros
         const cptr<float> src = sx_w + int64_t(jx) * KX;
         if (xlane) sj = sx_start[jx];
 #pragma unroll
-        for (int g = 0; g < KX / 4; ++g) {
-            const float4 wv = make_float4(src[4 * g], src[4 * g + 1], src[4 * g + 2], src[4 * g + 3]);
-            wxl[g * 64 + lane] = xlane ? wv : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+        for (int k = 0; k < KX; ++k) wx[k] = xlane ? src[k] : 0.f;
     }
 
     const cptr<int32_t> xs = tables + it->tx_off;   // window starts of the x axis
@@ -340,14 +336,12 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
             for (int g = 0; g < KX; g += 4) {
                 // four taps at a time: bounds the LDS values held in registers
                 __builtin_amdgcn_sched_barrier(0);
-                const float4 wg = wxl[(g / 4) * 64 + lane];
-                const float wk[4] = {wg.x, wg.y, wg.z, wg.w};
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const float4 q = src[g + k];
-                    r0 = fmaf(wk[k], q.x, r0);
-                    r1 = fmaf(wk[k], q.y, r1);
-                    r2 = fmaf(wk[k], q.z, r2);
+                    r0 = fmaf(wx[g + k], q.x, r0);
+                    r1 = fmaf(wx[g + k], q.y, r1);
+                    r2 = fmaf(wx[g + k], q.z, r2);
                 }
             }
             __builtin_amdgcn_sched_barrier(0);

@@ -48,11 +48,10 @@ constexpr int kSlotWords = 8;         // words per source row of a slot table
 constexpr int kSlotMax = 6;           // most output rows open at once (accumulator slots)
 constexpr int kStreamLdsBudget = 64 * 1024;   // LDS of one streaming workgroup (one wave)
 
-// LDS of one streaming workgroup (one wave): its source row (64 * px float4 pixels), the
-// stage of four output rows (3 channels x 4 rows x 64 columns) and the
-// column weights of its lanes (kx floats each).
+// LDS of one streaming workgroup (one wave): its source row (64 * px float4
+// pixels) and the stage of four output rows (3 channels x 4 rows x 64 columns).
 constexpr int stream_wave_bytes(int px, int kx, int elem_bytes) {
-    return 64 * px * 16 + 3 * 4 * 64 * elem_bytes + 64 * kx * 4;
+    return (void)kx, 64 * px * 16 + 3 * 4 * 64 * elem_bytes;
 }
 
 // Kernel an item is routed to.
