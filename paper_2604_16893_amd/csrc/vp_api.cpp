@@ -689,6 +689,7 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
             return fail(VP_ERR_ARG, "std must be positive and finite, mean finite");
         norm.a[c] = static_cast<float>(1.0 / (255.0 * static_cast<double>(std[c])));
         norm.b[c] = static_cast<float>(-static_cast<double>(mean[c]) / static_cast<double>(std[c]));
+        norm.z[c] = static_cast<float>(-255.0 * static_cast<double>(mean[c]));
     }
     Plan p;
     int32_t st = build_plan(items, n_items, &p);

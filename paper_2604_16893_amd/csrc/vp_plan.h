@@ -100,6 +100,7 @@ struct PlanView {
 struct Norm {
     float a[3];   // 1 / (255 * std_c)
     float b[3];   // -mean_c / std_c
+    float z[3];   // -255 * mean_c: v = a_c * (R + z_c), the same value in pixel units
 };
 
 // One launch of the streaming kernel: units [first, first + count), all
