@@ -257,26 +257,20 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
     const cptr<int32_t> close_row = tables + it->sy_off + (it->H + kSlotMax) * kSlotWords;  // [h]
 
     // Source frame, read through buffer resources (loads past a resource's
-    // range return 0).
+    // range return 0).  Every load is dword-aligned: unaligned per-lane
+    // loads cost about a third of the read bandwidth on gfx950.
     const int f = as_const(plan.indices)[it->idx_off + u_p];
     const uintptr_t fa = reinterpret_cast<uintptr_t>(it->frames + int64_t(f) * it->frame_bytes);
-    const int H = it->H;
-    const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
-    const uint32_t frame_bytes = static_cast<uint32_t>(it->frame_bytes);
-    // The lane's first byte inside a row.  A lane wholly past the row's end
-    // reads garbage that no column weight ever touches; it is clamped to
-    // the row's end so that its reads stay inside the next row.
-    const uint32_t lane_byte = min(3u * static_cast<uint32_t>(x0 + PX * lane), row_bytes);
-    // The last row is read dword-aligned from the dword-aligned frame base,
-    // with the range rounded up to whole dwords: the range check is per
-    // dword, and the dword holding the frame's last byte lies in that
-    // byte's (4-byte aligned) page, so it is always readable.  Every other
-    // row is read at the lane's exact byte: its 12 or 16 bytes end at most a
-    // few bytes into the next row, always inside the frame.
     const uint32_t lead = static_cast<uint32_t>(fa & 3u);
-    const uint32_t last_pos = lead + static_cast<uint32_t>(H - 1) * row_bytes + lane_byte;
-    const uint32_t last_off = last_pos & ~3u;
-    const uint32_t last_shift = last_pos & 3u;
+    // Range = the frame rounded up to whole dwords: the range check is per
+    // dword, and the dword holding the frame's last byte lies in that byte's
+    // (4-byte aligned) page, so it is always readable.
+    const uint32_t range = static_cast<uint32_t>((it->frame_bytes + lead + 3) & ~int64_t(3));
+    const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
+    // The lane's first byte inside a row, from the dword-aligned frame base.
+    // A lane wholly past the row's end reads garbage that no column weight
+    // ever touches; it is clamped to the row's end.
+    const uint32_t lane_off = lead + min(3u * static_cast<uint32_t>(x0 + PX * lane), row_bytes);
     // v_c = a_c * (R_c + z_c): the x pass starts its sums at z_c, so the
     // normalisation costs one multiply per value
     const float a0 = norm.a[0], a1 = norm.a[1], a2 = norm.a[2];
@@ -301,38 +295,36 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
     int slot = base % M;
     int next_close = close_row[base];
 
+    // Rows are visited in blocks of four starting at a multiple of 4, so
+    // that y % 4 = k is known at every step: the lane's byte offset inside
+    // row y is then voff[k] (dword aligned) + shf[k] (0..3), with the row
+    // block's own offset, a multiple of 4, in the block's buffer resource.
     using load_t = typename std::conditional<kLoadDwords == 4, uint4, uint3>::type;
-    // Row y < H - 1: a resource based at the row's first byte, read at the
-    // lane's byte.  Rows from H - 1 on get an empty range here (their loads
-    // return 0); the last row is read separately, dword-aligned.
-    auto load_row = [&](int y) __attribute__((always_inline)) -> load_t {
-        y = __builtin_amdgcn_readfirstlane(y);   // wave-uniform: build the resource in scalars
-        const uintptr_t base = fa + static_cast<uintptr_t>(static_cast<uint32_t>(y) * row_bytes);
-        const uint32_t n = y < H - 1 ? frame_bytes - static_cast<uint32_t>(y) * row_bytes : 0u;
-        const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(base));
-        const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(base >> 32));
+    uint32_t voff[kPrefetch], shf[kPrefetch];
+#pragma unroll
+    for (int k = 0; k < kPrefetch; ++k) {
+        const uint32_t c = lane_off + static_cast<uint32_t>(k) * row_bytes;
+        voff[k] = c & ~3u;
+        shf[k] = c & 3u;
+    }
+    // Row yb + k of the block starting at yb: a resource based at the
+    // block's first row (a multiple of 4 bytes past the aligned frame base)
+    // with the rest of the frame as its range.
+    auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> load_t {
+        // (the block is wave-uniform; say so, or the descriptor would be built per lane)
+        const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
+        const int64_t left = int64_t(range) - int64_t(o);
+        const uint32_t n = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(left > 0 ? left : 0));
+        const uintptr_t bp = fa - lead + o;
+        const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
+        const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
         const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-            reinterpret_cast<void*>((uintptr_t(b_hi) << 32) | b_lo), (short)0,
-            static_cast<int>(__builtin_amdgcn_readfirstlane(n)), 0x00020000);
+            reinterpret_cast<void*>((uintptr_t(b_hi) << 32) | b_lo), (short)0, static_cast<int>(n), 0x00020000);
         if constexpr (kLoadDwords == 4) {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b128(rb, lane_byte, 0, 0);
+            const auto r = __builtin_amdgcn_raw_buffer_load_b128(rb, voff[k], 0, 0);
             return make_uint4(r[0], r[1], r[2], r[3]);
         } else {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b96(rb, lane_byte, 0, 0);
-            return make_uint3(r[0], r[1], r[2]);
-        }
-    };
-    auto load_last_row = [&]() __attribute__((always_inline)) -> load_t {
-        const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(fa - lead));
-        const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>((fa - lead) >> 32));
-        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-            reinterpret_cast<void*>((uintptr_t(b_hi) << 32) | b_lo), (short)0,
-            static_cast<int>((frame_bytes + lead + 3u) & ~3u), 0x00020000);
-        if constexpr (kLoadDwords == 4) {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b128(rb, last_off, 0, 0);
-            return make_uint4(r[0], r[1], r[2], r[3]);
-        } else {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b96(rb, last_off, 0, 0);
+            const auto r = __builtin_amdgcn_raw_buffer_load_b96(rb, voff[k], 0, 0);
             return make_uint3(r[0], r[1], r[2]);
         }
     };
@@ -406,22 +398,21 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
         }
     };
 
-    // The lane's 3*PX source values of a row, converted to float.
-    auto convert = [&](load_t cur, bool aligned_read, float (&v)[V]) __attribute__((always_inline)) {
-        uint32_t b[kLoadDwords];
-        b[0] = cur.x;
-        b[1] = cur.y;
-        b[2] = cur.z;
-        if constexpr (kLoadDwords == 4) b[3] = cur.w;
-        if (aligned_read) {
-            // the dword-aligned read: the lane's bytes start at last_shift
-            // (the last word needs only its low bytes when it has no
-            // successor: rotate it in place)
+    // The lane's 3*PX source values of a row, converted to float: its bytes
+    // start at byte `shift` of the loaded dwords (the last word needs only
+    // its low bytes when it has no successor: rotate it in place).
+    auto convert = [&](load_t cur, uint32_t shift, float (&v)[V]) __attribute__((always_inline)) {
+        uint32_t d[kLoadDwords];
+        d[0] = cur.x;
+        d[1] = cur.y;
+        d[2] = cur.z;
+        if constexpr (kLoadDwords == 4) d[3] = cur.w;
+        constexpr int kWords = (V + 3) / 4;
+        uint32_t b[kWords];
 #pragma unroll
-            for (int k = 0; k < kLoadDwords; ++k) {
-                const int hi = k + 1 < kLoadDwords ? k + 1 : k;
-                b[k] = __builtin_amdgcn_alignbyte(b[hi], b[k], last_shift);
-            }
+        for (int k = 0; k < kWords; ++k) {
+            const int hi = k + 1 < kLoadDwords ? k + 1 : k;
+            b[k] = __builtin_amdgcn_alignbyte(d[hi], d[k], shift);
         }
 #pragma unroll
         for (int q = 0; q < V; ++q) v[q] = float((b[q >> 2] >> (8 * (q & 3))) & 255u);
@@ -467,45 +458,36 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
         }
     };
 
-    // Rows y0 .. H-2 in the main loop, loaded four rows ahead,
-    // unconditionally: a load past the band is harmless (in-frame data that
-    // is never used, or zeros from the empty range), and an unconditional
-    // load keeps every prefetch register in place.
-    const int y_main = min(y1, H - 1);
-    // (issued in row order, as the loop issues them, so that the oldest
-    // load is always the next one needed)
+    // Rows are loaded one block (four rows) ahead, unconditionally: a load
+    // past the band or the frame is harmless (in-frame data that is never
+    // used, or zeros from the range check), and an unconditional load keeps
+    // every prefetch register in place.  The first block's loads are issued
+    // in row order, as the loop issues them, so that the oldest load is
+    // always the next one needed.
+    const int yb0 = y0 & ~3;
     load_t pf[kPrefetch];
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) {
-        pf[k] = load_row(y0 + k);
+        pf[k] = load_row(yb0, k);
         __builtin_amdgcn_sched_barrier(0);
     }
 
-    for (int yb = y0; yb < y_main; yb += kPrefetch) {
+    for (int yb = yb0; yb < y1; yb += kPrefetch) {
         const cptr<float> wblk = slot_w + yb * kSlotWords;
 #pragma unroll
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
             // convert first: the next load then reuses the same registers
             float v[V];
-            convert(pf[k], false, v);
-            // keep the conversion here, ahead of the load that reuses pf[k]'s
-            // registers (otherwise it sinks into the conditional use below and
-            // pf[k] has to be copied while its load is in flight)
+            convert(pf[k], shf[k], v);
+            // (keep the conversion here, ahead of the load that reuses
+            // pf[k]'s registers; otherwise it sinks into the conditional use
+            // below and pf[k] has to be copied while its load is in flight)
 #pragma unroll
             for (int q = 0; q < V; ++q) asm volatile("" : : "v"(v[q]));
-            pf[k] = load_row(y + kPrefetch);
-            if (y < y_main) process_row(y, v, wblk + k * kSlotWords);
+            pf[k] = load_row(yb + kPrefetch, k);
+            if (y >= y0 && y < y1) process_row(y, v, wblk + k * kSlotWords);
         }
-    }
-    // The last row, read dword-aligned, then the zero-weight rows past the
-    // frame on which the bottom output rows close.
-    for (int y = max(y0, H - 1); y < y1; ++y) {
-        load_t cur{};
-        if (y == H - 1) cur = load_last_row();
-        float v[V];
-        convert(cur, y == H - 1, v);
-        process_row(y, v, slot_w + y * kSlotWords);
     }
 }
 
