@@ -131,6 +131,14 @@ SMALL = [
     ("tall_downscale", [(2, 2400, 100, [1, 0], 64, 32)], "bf16"),
     ("ragged_mixed", [(9, 120, 200, [0, 3, 8, 5], 96, 160), (1, 333, 257, [0], 320, 256),
                       (7, 45, 80, [6], 64, 64), (3, 480, 854, [0, 1, 2], 128, 224)], "bf16"),
+    # streaming-kernel shapes: five accumulator slots with three pixels per
+    # lane; a last column band of 32 after two of 64; odd frame sizes, so
+    # that every other frame starts off a 4-byte boundary; a frame narrower
+    # than one wave's pixels (lanes past the row end)
+    ("slots5_px3", [(3, 224, 700, [2, 0], 160, 256)], "f32"),
+    ("partial_band", [(2, 300, 450, [1, 0], 128, 160)], "bf16"),
+    ("unaligned_frames", [(4, 75, 101, [1, 2, 3], 64, 96)], "f32"),
+    ("narrow_frame", [(2, 100, 40, [0, 1], 64, 32)], "f32"),
 ]
 
 
