@@ -189,7 +189,8 @@ __device__ __forceinline__ void wave_lds_fence() {
 //     band's part of one 64-value run; it leaves as 16-byte stores, eight
 //     lanes per 128-byte run.
 template <int M, int KX, int PX, int OUT_BF16>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(M * PX > 12 || 3 * M * PX + KX >= 52 ? 4 : 5)))
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
+    M * PX > 12 || 3 * M * PX + KX >= 52 || (OUT_BF16 == 0 && M * PX >= 12) ? 4 : 5)))
 void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out, Norm norm) {
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
     constexpr int kRowPx = 64 * PX;
@@ -329,6 +330,29 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
         }
     };
 
+    // Store-out pieces of this lane: piece e = lane + 64 r of the band's
+    // (patch q, channel c, row ry, piece) runs, as a stage offset (-1: none)
+    // and an output offset relative to the merge-window row block.
+    constexpr int kPieces = 16 / S;
+    constexpr int kPerPatch = 3 * 4 * kPieces;
+    constexpr int kStoreIter = (4 * kPerPatch + 63) / 64;
+    int st_off[kStoreIter], dst_off[kStoreIter];
+    {
+        const int n_seg = (nbw >> 4) * kPerPatch;
+#pragma unroll
+        for (int r = 0; r < kStoreIter; ++r) {
+            const int e = lane + 64 * r;
+            const int q = e / kPerPatch;
+            const int rr = e - q * kPerPatch;
+            const int c = rr / (4 * kPieces);
+            const int ry = (rr / kPieces) & 3;
+            const int piece = rr % kPieces;
+            const int qa = (j0 >> 4) + q;
+            st_off[r] = e < n_seg ? (c * 4 + ry) * 64 + q * 16 + piece * S : -1;
+            dst_off[r] = ((qa >> 1) * 4 + (qa & 1)) * kRow + (c * 2) * 256 + ry * 16 + piece * S;
+        }
+    }
+
     // x pass of output row i, normalise, stage; every 4th row: store.
     auto x_pass = [&](int i) __attribute__((always_inline)) {
         const int yy = i & 3;
@@ -367,31 +391,26 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
         }
         if (yy == 3) {
             wave_lds_fence();
-            // rows i-3 .. i: for each patch column q of the band and channel
-            // c, four 16-column rows of the patch = one 64-value run, written
-            // as 16-byte pieces, 16/S pieces per patch row
-            constexpr int kPieces = 16 / S;
-            constexpr int kPerPatch = 3 * 4 * kPieces;
+            // rows i-3 .. i: the lane's 16-byte pieces (precomputed below)
             const int yq = (i & 15) >> 2;
             const int bh = i >> 5;
             const int mh = (i >> 4) & 1;
             const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + bh) * it->wm * 4 + mh * 2;
-            const int n_seg = (nbw >> 4) * kPerPatch;
-            for (int e = lane; e < n_seg; e += 64) {
-                const int q = e / kPerPatch;
-                const int r = e - q * kPerPatch;
-                const int c = r / (4 * kPieces);
-                const int ry = (r / kPieces) & 3;
-                const int piece = r % kPieces;
-                const uint4 val = *reinterpret_cast<const uint4*>(stage + (c * 4 + ry) * 64 + q * 16 + piece * S);
-                const int qa = (j0 >> 4) + q;
-                const int64_t rho = win_row0 + (qa >> 1) * 4 + (qa & 1);
-                elem_t* dst = static_cast<elem_t*>(out) + rho * kRow + (yq * 4 + ry) * 16 + piece * S;
-                if (both) {
-                    *reinterpret_cast<uint4*>(dst + (c * 2) * 256) = val;
-                    *reinterpret_cast<uint4*>(dst + (c * 2 + 1) * 256) = val;
-                } else {
-                    *reinterpret_cast<uint4*>(dst + (c * 2 + dt_self) * 256) = val;
+            elem_t* const obase = static_cast<elem_t*>(out) + win_row0 * kRow + yq * 64;
+#pragma unroll
+            for (int r = 0; r < kStoreIter; ++r) {
+                if (st_off[r] >= 0) {
+                    const uint4 val = *reinterpret_cast<const uint4*>(stage + st_off[r]);
+                    elem_t* dst = obase + dst_off[r];
+                    // non-temporal: the rows are not read again here
+                    using u4v = unsigned __attribute__((ext_vector_type(4)));
+                    const u4v vv = {val.x, val.y, val.z, val.w};
+                    if (both) {
+                        __builtin_nontemporal_store(vv, reinterpret_cast<u4v*>(dst));
+                        __builtin_nontemporal_store(vv, reinterpret_cast<u4v*>(dst + 256));
+                    } else {
+                        __builtin_nontemporal_store(vv, reinterpret_cast<u4v*>(dst + dt_self * 256));
+                    }
                 }
             }
             wave_lds_fence();
