@@ -194,8 +194,12 @@ bool generic_subtile(const AxisFilter& fx, int32_t* rh, int32_t* cw) {
 // zero weights).  M is the most output rows open at once (at least 4), so two
 // open rows never share a slot.  For every source row y the table holds, per
 // slot s < M, the weight of y in the output row that has slot s at y (zero if
-// that row does not read y), then the close row of every output row.
+// that row does not read y), times 2^24 (the kernel reads byte b as the f16
+// denormal b * 2^-24; the power of two is exact both ways), then the close
+// row of every output row.
 // Returns M, or -1 if the axis needs more than kSlotMax slots.
+constexpr float kSlotScale = 16777216.0f;   // 2^24
+
 int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
     const int32_t n_in = f.n_in, n_out = f.n_out;
     const int32_t rows = n_in + vp::kSlotMax;
@@ -227,7 +231,7 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
     float* w = reinterpret_cast<float*>(words->data());
     for (int32_t i = 0; i < n_out; ++i)
         for (int32_t k = 0; k < f.count[i]; ++k)
-            w[size_t(f.start[i] + k) * vp::kSlotWords + i % m] = f.weight[size_t(i) * f.taps + k];
+            w[size_t(f.start[i] + k) * vp::kSlotWords + i % m] = f.weight[size_t(i) * f.taps + k] * kSlotScale;
     std::memcpy(words->data() + size_t(rows) * vp::kSlotWords, close.data(), sizeof(int32_t) * n_out);
     return m;
 }

@@ -11,9 +11,12 @@
 // other:
 //   * y pass first, in registers: each lane owns 2 or 3 RGB pixels of the
 //     band's source span, loads them with one buffer load per row
-//     (prefetched four rows ahead), converts them once and adds them with
-//     wave-uniform scalar weights into M accumulator slots; output row i
-//     lives in slot i mod M while it is open.  The source is read once.
+//     (prefetched four rows ahead), unpacks the bytes two at a time into
+//     f16 halves (one v_perm per pair, which also absorbs the lane's byte
+//     misalignment) and adds them with wave-uniform scalar weights into M
+//     accumulator slots through mixed-precision FMAs (f16 byte times f32
+//     weight, exact); output row i lives in slot i mod M while it is open.
+//     The source is read once.
 //   * when an output row is complete its slot goes to the wave's LDS row
 //     (one float4 per pixel) and the wave's x pass follows: one lane per
 //     output column, one ds_read_b128 and three FMAs per tap, then the
@@ -162,6 +165,7 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
 constexpr int kPrefetch = 4;           // source rows in flight per lane
 
 using f3 = float __attribute__((ext_vector_type(3)));
+using h2 = _Float16 __attribute__((ext_vector_type(2)));
 
 // Orders this wave's LDS accesses before and after it.  LDS operations of
 // one wave execute in issue order, so within a wave keeping the compiler from
@@ -177,7 +181,7 @@ __device__ __forceinline__ void wave_lds_fence() {
 // works alone -- no workgroup barrier anywhere:
 //   * y pass, in registers: lane t owns PX consecutive pixels of the band's
 //     source span, reads them with one buffer load per row (prefetched four
-//     rows ahead), converts them once and adds them with wave-uniform scalar
+//     rows ahead), unpacks them once and adds them with wave-uniform scalar
 //     weights into M rotating accumulators, one per output row that can
 //     still read the row;
 //   * when an output row completes, each lane writes its PX pixels to the
@@ -301,12 +305,15 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
     // row y is then voff[k] (dword aligned) + shf[k] (0..3), with the row
     // block's own offset, a multiple of 4, in the block's buffer resource.
     using load_t = typename std::conditional<kLoadDwords == 4, uint4, uint3>::type;
-    uint32_t voff[kPrefetch], shf[kPrefetch];
+    // sel[k]: the v_perm selector that moves bytes shift and shift + 1 of
+    // the loaded dwords (shift = the lane's byte offset mod 4 in row phase k)
+    // into the low bytes of two 16-bit halves and zeroes the high bytes.
+    uint32_t voff[kPrefetch], sel[kPrefetch];
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) {
         const uint32_t c = lane_off + static_cast<uint32_t>(k) * row_bytes;
         voff[k] = c & ~3u;
-        shf[k] = c & 3u;
+        sel[k] = 0x0C000C00u | (c & 3u) | (((c & 3u) + 1u) << 16);
     }
     // Row yb + k of the block starting at yb: a resource based at the
     // block's first row (a multiple of 4 bytes past the aligned frame base)
@@ -417,29 +424,41 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
         }
     };
 
-    // The lane's 3*PX source values of a row, converted to float: its bytes
-    // start at byte `shift` of the loaded dwords (the last word needs only
-    // its low bytes when it has no successor: rotate it in place).
-    auto convert = [&](load_t cur, uint32_t shift, float (&v)[V]) __attribute__((always_inline)) {
+    // The lane's 3*PX source bytes of a row, unpacked two at a time into
+    // 16-bit halves with zero high bytes: byte value b reads as the f16
+    // number b * 2^-24 (a denormal, exact).  The slot weights carry the
+    // factor 2^24, so the mixed-precision FMAs below form w * b exactly, as a
+    // float copy of the byte would, without a conversion per value.  Pair p
+    // (values 2p, 2p+1) starts at byte shift + 2p, inside dwords p/2 and
+    // p/2 + 1: the selector is sel, plus 2 per byte for odd p.
+    constexpr int P = (V + 1) / 2;
+    auto unpack = [&](load_t cur, uint32_t s0, uint32_t (&hv)[P]) __attribute__((always_inline)) {
         uint32_t d[kLoadDwords];
         d[0] = cur.x;
         d[1] = cur.y;
         d[2] = cur.z;
         if constexpr (kLoadDwords == 4) d[3] = cur.w;
-        constexpr int kWords = (V + 3) / 4;
-        uint32_t b[kWords];
+        // (formed here, per row: hoisted out of the row loop, the four odd
+        // selectors would hold four more registers)
+        uint32_t s1;
+        asm volatile("v_add_u32 %0, 0x20002, %1" : "=v"(s1) : "v"(s0));
 #pragma unroll
-        for (int k = 0; k < kWords; ++k) {
-            const int hi = k + 1 < kLoadDwords ? k + 1 : k;
-            b[k] = __builtin_amdgcn_alignbyte(d[hi], d[k], shift);
+        for (int p = 0; p < P; ++p) {
+            const int j = p >> 1;
+            const int hi = j + 1 < kLoadDwords ? j + 1 : j;
+            hv[p] = __builtin_amdgcn_perm(d[hi], d[j], (p & 1) ? s1 : s0);
         }
-#pragma unroll
-        for (int q = 0; q < V; ++q) v[q] = float((b[q >> 2] >> (8 * (q & 3))) & 255u);
     };
 
     // Source row y (its values in v) into the slots; closes an output row
     // when y is its close row.
-    auto process_row = [&](int y, const float (&v)[V], cptr<float> wr) __attribute__((always_inline)) {
+    auto process_row = [&](int y, const uint32_t (&hv)[P], cptr<float> wr) __attribute__((always_inline)) {
+        float v[V];
+#pragma unroll
+        for (int q = 0; q < V; ++q) {
+            const h2 pr = __builtin_bit_cast(h2, hv[q >> 1]);
+            v[q] = static_cast<float>((q & 1) ? pr.y : pr.x);   // folds into the FMAs (fma_mix)
+        }
         // every slot takes this row with its weight (zero where its output row does not read it)
 #pragma unroll
         for (int s = 0; s < M; ++s) {
@@ -496,16 +515,16 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
 #pragma unroll
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
-            // convert first: the next load then reuses the same registers
-            float v[V];
-            convert(pf[k], shf[k], v);
-            // (keep the conversion here, ahead of the load that reuses
+            // unpack first: the next load then reuses the same registers
+            uint32_t hv[P];
+            unpack(pf[k], sel[k], hv);
+            // (keep the unpacking here, ahead of the load that reuses
             // pf[k]'s registers; otherwise it sinks into the conditional use
             // below and pf[k] has to be copied while its load is in flight)
 #pragma unroll
-            for (int q = 0; q < V; ++q) asm volatile("" : : "v"(v[q]));
+            for (int q = 0; q < P; ++q) asm volatile("" : : "v"(hv[q]));
             pf[k] = load_row(yb + kPrefetch, k);
-            if (y >= y0 && y < y1) process_row(y, v, wblk + k * kSlotWords);
+            if (y >= y0 && y < y1) process_row(y, hv, wblk + k * kSlotWords);
         }
     }
 }

@@ -17,8 +17,9 @@
 //   slot table of a y axis n_in -> n_out (streaming kernel), M slots:
 //       [n_in + 6] rows of 8 words: float weight[slot]   (slots >= M zero)
 //         -- output row i is accumulated in slot i mod M from the first row of
-//            its window to its close row; weight[s] is the weight of source
-//            row y in the output row that has slot s at y, or zero
+//            its window to its close row; weight[s] is 2^24 times the weight
+//            of source row y in the output row that has slot s at y, or zero
+//            (the kernel reads source bytes as f16 denormals, b * 2^-24)
 //       int32 close_row[n_out + 1]   (the last entry is padding)
 //         -- the row after which output row i is complete: the last row of its
 //            window, except that output rows whose windows all end at the bottom
