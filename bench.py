@@ -100,8 +100,8 @@ def cpu_baseline(wl, frames_dev, planned, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=4, choices=range(5),
                     help="workload configuration (4 = 64x256 frames 720x1280, the default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -216,6 +216,7 @@ def main():
         f"kernels {mean_kern_ms:.3f} ms mean (min {min(kern_ms):.3f}, max {max(kern_ms):.3f}); "
         f"{value:,.0f} frames/s; {achieved:,.0f} GB/s algorithmic "
         f"({achieved / HBM_PEAK_GBPS:.1%} of 8 TB/s)")
+    log("kernel ms per step: " + " ".join(f"{t:.3f}" for t in kern_ms))
 
     tag = f"c{args.workload}"
     sha = kernel_source_sha()

@@ -137,11 +137,14 @@ struct Plan {
     std::vector<int32_t> indices;
     std::vector<int32_t> tables;
     std::vector<vp::StreamUnit> units;
+    std::vector<uint32_t> wgs;   // streaming workgroups: unit | band << 20, grouped per launch
     std::vector<vp::StreamLaunch> launches;
     std::vector<int32_t> grid;  // [n][3]
     std::vector<int32_t> cu;    // [n + 1]
     int64_t total_rows = 0;
-    size_t off_items = 0, off_prefix = 0, off_indices = 0, off_tables = 0, off_units = 0, bytes = 0;
+    int64_t generic_cost = 0;   // source pixels the general kernel reads, roughly
+    size_t off_items = 0, off_prefix = 0, off_indices = 0, off_tables = 0, off_units = 0, off_wgs = 0,
+           bytes = 0;
 };
 
 int32_t validate_item(const vp_item& it, int32_t b) {
@@ -188,15 +191,15 @@ bool generic_subtile(const AxisFilter& fx, int32_t* rh, int32_t* cw) {
 
 // Slot table of a y axis for the streaming kernel.  Output row i lives in
 // accumulator slot i mod M while it is open: from the first row of its
-// window to its close row.  The close row is the last row of the window,
-// except that output rows whose windows all end at the bottom border close
-// on consecutive rows n_in-1, n_in, n_in+1, ... (rows past n_in only carry
-// zero weights).  M is the most output rows open at once (at least 4), so two
-// open rows never share a slot.  For every source row y the table holds, per
-// slot s < M, the weight of y in the output row that has slot s at y (zero if
-// that row does not read y), times 2^24 (the kernel reads byte b as the f16
-// denormal b * 2^-24; the power of two is exact both ways), then the close
-// row of every output row.
+// window to its close row, the last row of its window or, if that is
+// earlier, the close row of output row i - 1 (close rows never decrease;
+// several output rows close on the same source row when the axis is
+// upscaled, and at the bottom border).  M is the most output rows open at
+// once (at least 4), so two open rows never share a slot.  For every source
+// row y the table holds, per slot s < M, the weight of y in the output row
+// that has slot s at y (zero if that row does not read y), times 2^24 (the
+// kernel reads byte b as the f16 denormal b * 2^-24; the power of two is
+// exact both ways), then the close row of every output row.
 // Returns M, or -1 if the axis needs more than kSlotMax slots.
 constexpr float kSlotScale = 16777216.0f;   // 2^24
 
@@ -206,10 +209,7 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
     std::vector<int32_t> close(n_out, 0);
     for (int32_t i = 0; i < n_out; ++i) {
         int32_t c = f.start[i] + f.count[i] - 1;
-        if (i > 0 && c <= close[i - 1]) {
-            if (f.start[i] + f.count[i] != n_in) return -1;   // only at the bottom border
-            c = close[i - 1] + 1;
-        }
+        if (i > 0 && c < close[i - 1]) c = close[i - 1];
         if (i > 0 && f.start[i] < f.start[i - 1]) return -1;
         close[i] = c;
     }
@@ -227,7 +227,8 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
     }
     if (most > vp::kSlotMax) return -1;
     const int32_t m = most < 4 ? 4 : most;
-    words->assign(size_t(rows) * vp::kSlotWords + n_out + 1, 0);   // +1: close_row[n_out] pad
+    words->assign(size_t(rows) * vp::kSlotWords + n_out + 1, 0);
+    (*words)[size_t(rows) * vp::kSlotWords + n_out] = INT32_MAX;   // close_row[n_out]: never reached
     float* w = reinterpret_cast<float*>(words->data());
     for (int32_t i = 0; i < n_out; ++i)
         for (int32_t k = 0; k < f.count[i]; ++k)
@@ -283,7 +284,6 @@ int32_t band_span(const AxisFilter& fx, int32_t band) {
 // budget is checked with float32 staging, so the routing does not depend on
 // the output type.
 bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
-    if (it.src_h < it.dst_h) return false;                 // vertical upscale: general kernel
     if (m < 4 || m > vp::kSlotMax) return false;
     const int32_t mm = m;
     const int32_t kx = round_up(fx.taps, 4);
@@ -317,6 +317,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
     p->items.assign(n, vp::DevItem{});
+    p->generic_cost = 0;
     p->prefix.assign(n + 1, 0);
     p->grid.assign(size_t(n) * 3, 0);
     p->cu.assign(n + 1, 0);
@@ -347,7 +348,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         auto found = slot_tables.find(key);
         if (found == slot_tables.end()) {
             std::vector<int32_t> words;
-            const int32_t mm = f.n_in >= f.n_out ? build_slots(f, &words) : -1;
+            const int32_t mm = build_slots(f, &words);
             int32_t o = -1;
             if (mm > 0) {
                 o = static_cast<int32_t>(p->tables.size());
@@ -415,7 +416,10 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
         p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
         rows += item_rows;
-        if (d.route == vp::kRouteGeneric) tiles += int64_t(d.t) * d.hm * d.wm;
+        if (d.route == vp::kRouteGeneric) {
+            tiles += int64_t(d.t) * d.hm * d.wm;
+            p->generic_cost += int64_t(2) * d.t * d.H * d.W;
+        }
         if (rows > INT32_MAX || tiles > INT32_MAX)
             return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 rows");
         p->cu[b + 1] = static_cast<int32_t>(rows);
@@ -424,63 +428,105 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     p->total_rows = rows;
 
     // Streaming units: one per (item, distinct frame of a pair, band of output
-    // rows); bands are cut so that the batch yields enough workgroups to fill
-    // the chip, in multiples of 4 rows (one 64-value run per store).
-    int64_t stream_frames = 0;
+    // rows).  A workgroup streams the source rows of its unit top to bottom,
+    // so its life is about proportional to those rows.  To end the batch
+    // evenly -- many kernel shapes run side by side, and a small launch lasts
+    // as long as its longest unit -- no unit reads more than an eighth of the
+    // source rows per wave slot of the whole batch (256 CUs x 20 waves), in
+    // bands of output rows that are multiples of 4 (one 64-value run per
+    // store).  A band re-reads the source rows that its first window shares
+    // with the band above, so none spans fewer than ten windows of source
+    // rows.
+    constexpr int64_t kWaveSlots = 256 * 20;
+    int64_t wave_rows = 0;   // source rows that all workgroups stream, whole frames
     for (int32_t b = 0; b < n; ++b) {
         const vp::DevItem& d = p->items[b];
         if (d.route != vp::kRouteStream) continue;
-        for (int32_t tt = 0; tt < d.t; ++tt)
-            stream_frames += p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1] ? 1 : 2;
+        for (int32_t tt = 0; tt < d.t; ++tt) {
+            const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
+            wave_rows += int64_t(same ? 1 : 2) * shapes[b].bands * d.H;
+        }
     }
+    const int64_t max_src_rows = wave_rows / (kWaveSlots * 8);
     struct Keyed {
-        std::tuple<int32_t, int32_t, int32_t, int32_t> key;
+        std::tuple<int32_t, int32_t, int32_t> key;   // kernel shape (m, kx, px)
+        int32_t bands;                               // column bands (workgroups) of the unit
         vp::StreamUnit unit;
+        int64_t cost;
     };
     std::vector<Keyed> keyed;
-    constexpr int64_t kTargetUnits = 2048;
     for (int32_t b = 0; b < n; ++b) {
         const vp::DevItem& d = p->items[b];
         if (d.route != vp::kRouteStream) continue;
         const StreamShape& sh = shapes[b];
-        int64_t band = stream_frames > 0 ? int64_t(d.h) * stream_frames / kTargetUnits : d.h;
-        band = band / 4 * 4;
-        if (band < 16) band = 16;
-        if (band > d.h) band = d.h;
+        int64_t band = max_src_rows * d.h / d.H;
+        const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
+        band = std::max(band, min_band);
+        band = std::max<int64_t>((band + 3) / 4 * 4, 16);
+        band = std::min<int64_t>(band, d.h);
         for (int32_t tt = 0; tt < d.t; ++tt) {
             const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
             for (int32_t dt = 0; dt < (same ? 1 : 2); ++dt) {
                 for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
                     const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
                     Keyed k;
-                    k.key = std::make_tuple(sh.m, sh.kx, sh.px, sh.bands);
+                    k.key = std::make_tuple(sh.m, sh.kx, sh.px);
+                    k.bands = sh.bands;
                     k.unit.item = b;
                     k.unit.p = 2 * tt + dt;
                     k.unit.rows = i0 | (i1 << 16);
                     k.unit.flags = same ? 1 : 0;
+                    k.cost = int64_t(i1 - i0) * d.H / d.h * d.W;   // source pixels read, roughly
                     keyed.push_back(k);
                 }
             }
         }
     }
-    std::stable_sort(keyed.begin(), keyed.end(),
-                     [](const Keyed& a, const Keyed& c) { return a.key < c.key; });
+    // Units of one kernel shape form one launch, whatever their widths.  Its
+    // workgroups are listed explicitly: entry g (unit index | band << 20, or
+    // kNoWork) runs as workgroup g, and consecutive workgroups go to the
+    // eight XCDs in turn.  Units are taken eight at a time, and their bands
+    // are listed round by round (band 0 of all eight, then band 1, ...), so
+    // that all bands of one unit run on one XCD and share the source pixels
+    // of neighbouring bands through its L2; a unit with fewer bands than the
+    // others of its eight leaves empty entries.  Units are sorted by band
+    // count first, which keeps those rare.
+    std::stable_sort(keyed.begin(), keyed.end(), [](const Keyed& a, const Keyed& c) {
+        return a.key != c.key ? a.key < c.key : a.bands < c.bands;
+    });
+    if (keyed.size() > vp::kWgUnitMask + 1)
+        return fail(VP_ERR_CAPACITY, "batch has more than 2^20 streaming work units");
     p->units.clear();
+    p->wgs.clear();
     p->launches.clear();
-    for (size_t k = 0; k < keyed.size(); ++k) {
-        if (k == 0 || keyed[k].key != keyed[k - 1].key) {
-            vp::StreamLaunch L{};
-            L.first = static_cast<int32_t>(k);
-            L.count = 0;
-            L.m = std::get<0>(keyed[k].key);
-            L.kx = std::get<1>(keyed[k].key);
-            L.px = std::get<2>(keyed[k].key);
-            L.bands = std::get<3>(keyed[k].key);
-            p->launches.push_back(L);
+    for (size_t k0 = 0; k0 < keyed.size();) {
+        size_t k1 = k0;
+        while (k1 < keyed.size() && keyed[k1].key == keyed[k0].key) ++k1;
+        vp::StreamLaunch L{};
+        L.first = static_cast<int32_t>(p->wgs.size());
+        L.m = std::get<0>(keyed[k0].key);
+        L.kx = std::get<1>(keyed[k0].key);
+        L.px = std::get<2>(keyed[k0].key);
+        for (size_t c0 = k0; c0 < k1; c0 += 8) {
+            const size_t c1 = std::min(c0 + 8, k1);
+            int32_t rounds = 0;
+            for (size_t k = c0; k < c1; ++k) rounds = std::max(rounds, keyed[k].bands);
+            const uint32_t u0 = static_cast<uint32_t>(p->units.size());
+            for (size_t k = c0; k < c1; ++k) {
+                p->units.push_back(keyed[k].unit);
+                L.cost += keyed[k].cost * keyed[k].bands;
+            }
+            for (int32_t r = 0; r < rounds; ++r)
+                for (size_t x = 0; x < 8; ++x) {
+                    const size_t k = c0 + x;
+                    p->wgs.push_back(k < c1 && r < keyed[k].bands
+                                         ? (u0 + static_cast<uint32_t>(x)) | (static_cast<uint32_t>(r) << vp::kWgBandShift)
+                                         : vp::kNoWork);
+                }
         }
-        vp::StreamLaunch& L = p->launches.back();
-        ++L.count;
-        p->units.push_back(keyed[k].unit);
+        L.count = static_cast<int32_t>(p->wgs.size()) - L.first;
+        p->launches.push_back(L);
+        k0 = k1;
     }
 
     p->off_items = 0;
@@ -488,7 +534,8 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
     p->off_tables = align_up(p->off_indices + sizeof(int32_t) * p->indices.size());
     p->off_units = align_up(p->off_tables + sizeof(int32_t) * p->tables.size());
-    p->bytes = align_up(p->off_units + sizeof(vp::StreamUnit) * p->units.size());
+    p->off_wgs = align_up(p->off_units + sizeof(vp::StreamUnit) * p->units.size());
+    p->bytes = align_up(p->off_wgs + sizeof(uint32_t) * p->wgs.size());
     return VP_OK;
 }
 
@@ -559,12 +606,124 @@ int32_t upload_plan(const Plan& p, void* workspace, hipStream_t stream) {
     std::memcpy(base + p.off_tables, p.tables.data(), sizeof(int32_t) * p.tables.size());
     if (!p.units.empty())
         std::memcpy(base + p.off_units, p.units.data(), sizeof(vp::StreamUnit) * p.units.size());
+    if (!p.wgs.empty())
+        std::memcpy(base + p.off_wgs, p.wgs.data(), sizeof(uint32_t) * p.wgs.size());
     e = hipMemcpyAsync(workspace, s.host, p.bytes, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
     e = hipEventRecord(s.done, stream);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
     s.pending = true;
     return VP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Side streams.  The launches of one call (one per streaming-kernel shape,
+// plus the general kernel) are independent of each other; on the caller's
+// stream alone they would run one after another, and a small launch leaves
+// most of the chip idle for the whole life of its longest workgroup.  Calls
+// with several launches therefore fork to up to kSideStreams more streams of
+// the device and join back with events, so the call stays one ordered step
+// of the caller's stream.  The streams (default priority) and events are
+// created on first use and kept until the process ends.
+// ---------------------------------------------------------------------------
+
+constexpr int kSideStreams = 3;
+
+struct Side {
+    std::mutex mu;   // held from fork to join: the events are shared by all calls
+    bool ready = false;
+    hipStream_t s[kSideStreams] = {};
+    hipEvent_t fork = nullptr;
+    hipEvent_t join[kSideStreams] = {};
+};
+
+std::mutex g_side_mu;
+std::map<int, Side*> g_side;
+
+int32_t side_for_device(int dev, Side** out) {
+    Side* side = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_side_mu);
+        Side*& r = g_side[dev];
+        if (r == nullptr) r = new Side();   // lives until process exit
+        side = r;
+    }
+    std::lock_guard<std::mutex> lk(side->mu);
+    if (!side->ready) {
+        hipError_t e = hipEventCreateWithFlags(&side->fork, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(e, "hipEventCreate (fork)");
+        for (int i = 0; i < kSideStreams; ++i) {
+            e = hipStreamCreateWithFlags(&side->s[i], hipStreamNonBlocking);
+            if (e != hipSuccess) return hip_fail(e, "hipStreamCreate (side stream)");
+            e = hipEventCreateWithFlags(&side->join[i], hipEventDisableTiming);
+            if (e != hipSuccess) return hip_fail(e, "hipEventCreate (join)");
+        }
+        side->ready = true;
+    }
+    *out = side;
+    return VP_OK;
+}
+
+// Runs the plan's launches: on the caller's stream if there is one, else
+// spread over the caller's stream and the side streams, largest estimated
+// work first onto the least loaded stream.
+int32_t run_launches(const Plan& p, const vp::PlanView& view, void* out_rows, int32_t out_dtype,
+                     const vp::Norm& norm, hipStream_t stream) {
+    struct Job {
+        int32_t launch;   // index into p.launches, or -1 for the general kernel
+        int64_t cost;
+    };
+    std::vector<Job> jobs;
+    if (view.n_tiles > 0) jobs.push_back(Job{-1, p.generic_cost});
+    for (size_t k = 0; k < p.launches.size(); ++k)
+        jobs.push_back(Job{static_cast<int32_t>(k), p.launches[k].cost});
+    auto launch = [&](const Job& j, hipStream_t st) -> int32_t {
+        if (j.launch < 0) {
+            const int err = vp::launch_generic(view, out_rows, out_dtype, norm, st);
+            if (err != 0) return hip_fail(static_cast<hipError_t>(err), "general kernel launch");
+        } else {
+            const int err = vp::launch_stream(view, p.launches[j.launch], out_rows, out_dtype, norm, st);
+            if (err != 0) return hip_fail(static_cast<hipError_t>(err), "streaming kernel launch");
+        }
+        return VP_OK;
+    };
+    if (jobs.size() <= 1) return jobs.empty() ? VP_OK : launch(jobs[0], stream);
+
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    Side* side = nullptr;
+    int32_t st = side_for_device(dev, &side);
+    if (st != VP_OK) return st;
+    std::stable_sort(jobs.begin(), jobs.end(), [](const Job& a, const Job& b) { return a.cost > b.cost; });
+    const int lanes = std::min<int>(static_cast<int>(jobs.size()), kSideStreams + 1);
+    std::vector<int> lane_of(jobs.size(), 0);
+    std::vector<int64_t> load(lanes, 0);
+    for (size_t k = 0; k < jobs.size(); ++k) {
+        int best = 0;
+        for (int l = 1; l < lanes; ++l)
+            if (load[l] < load[best]) best = l;
+        lane_of[k] = best;
+        load[best] += jobs[k].cost;
+    }
+    std::lock_guard<std::mutex> lk(side->mu);
+    e = hipEventRecord(side->fork, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord (fork)");
+    for (int l = 1; l < lanes; ++l) {
+        e = hipStreamWaitEvent(side->s[l - 1], side->fork, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent (fork)");
+    }
+    st = VP_OK;
+    for (size_t k = 0; k < jobs.size() && st == VP_OK; ++k)
+        st = launch(jobs[k], lane_of[k] == 0 ? stream : side->s[lane_of[k] - 1]);
+    // join even after a failed launch, so that the caller's stream still
+    // orders after whatever was enqueued
+    for (int l = 1; l < lanes; ++l) {
+        e = hipEventRecord(side->join[l - 1], side->s[l - 1]);
+        if (e == hipSuccess) e = hipStreamWaitEvent(stream, side->join[l - 1], 0);
+        if (e != hipSuccess && st == VP_OK) st = hip_fail(e, "join of a side stream");
+    }
+    return st;
 }
 
 }  // namespace
@@ -719,14 +878,11 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
     view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
     view.tables = reinterpret_cast<const int32_t*>(ws + p.off_tables);
     view.units = reinterpret_cast<const vp::StreamUnit*>(ws + p.off_units);
+    view.wgs = reinterpret_cast<const uint32_t*>(ws + p.off_wgs);
     view.n_items = n_items;
     view.n_tiles = p.prefix[n_items];
-    int err = vp::launch_generic(view, out_rows, out_dtype, norm, stream);
-    if (err != 0) return hip_fail(static_cast<hipError_t>(err), "general kernel launch");
-    for (const vp::StreamLaunch& L : p.launches) {
-        err = vp::launch_stream(view, L, out_rows, out_dtype, norm, stream);
-        if (err != 0) return hip_fail(static_cast<hipError_t>(err), "streaming kernel launch");
-    }
+    st = run_launches(p, view, out_rows, out_dtype, norm, stream);
+    if (st != VP_OK) return st;
     if (t_stop != nullptr) {
         const hipError_t e = hipEventRecord(t_stop, stream);
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");

@@ -94,7 +94,10 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
     const int64_t row_stride = int64_t(it.W) * 3;
     const int tid = threadIdx.x;
 
-    for (int dt = 0; dt < 2; ++dt) {
+    // an image, or an odd count padded with its last index: both temporal
+    // halves come from one frame, computed once and staged twice
+    const bool same = plan.indices[it.idx_off + 2 * tt] == plan.indices[it.idx_off + 2 * tt + 1];
+    for (int dt = 0; dt < (same ? 1 : 2); ++dt) {
         const int f = plan.indices[it.idx_off + 2 * tt + dt];
         const uint8_t* frame = it.frames + int64_t(f) * it.frame_bytes;
         for (int r0 = 0; r0 < kWin; r0 += it.rh) {
@@ -132,7 +135,9 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
                     const float v = fmaf(acc, norm.a[c], norm.b[c]);
                     const int il = r0 + r, jl = c0 + cc;
                     const int sub = (il >> 4) * 2 + (jl >> 4);
-                    stage[sub * kRow + ((c * 2 + dt) * kPatch + (il & 15)) * kPatch + (jl & 15)] = v;
+                    float* st = stage + sub * kRow + ((c * 2 + dt) * kPatch + (il & 15)) * kPatch + (jl & 15);
+                    st[0] = v;
+                    if (same) st[kPatch * kPatch] = v;   // the second temporal half
                 }
                 __syncthreads();
             }
@@ -195,7 +200,7 @@ __device__ __forceinline__ void wave_lds_fence() {
 template <int M, int KX, int PX, int OUT_BF16>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
     M * PX > 12 || 3 * M * PX + KX >= 52 || (OUT_BF16 == 0 && M * PX >= 12) ? 4 : 5)))
-void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out, Norm norm) {
+void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
     constexpr int kRowPx = 64 * PX;
     constexpr int V = 3 * PX;                      // values per lane per source row
@@ -204,26 +209,13 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
     extern __shared__ __align__(16) unsigned char smem[];
 
     const int lane = threadIdx.x;
-    // Workgroup -> (unit, column band).  Consecutive workgroups go to the
-    // eight XCDs in turn; while the unit count allows, the bands of one unit
-    // are given ids that fall on the same XCD, so that the source pixels two
-    // neighbouring bands share are fetched once into that XCD's L2.
-    int u, wave;
-    {
-        const int g = blockIdx.x;
-        const int full = (n_units >> 3) * 8 * n_bands;
-        if (g < full) {
-            const int r = g >> 3;
-            u = (r / n_bands) * 8 + (g & 7);
-            wave = r % n_bands;
-        } else {
-            u = (n_units & ~7) + (g - full) / n_bands;
-            wave = (g - full) % n_bands;
-        }
-        u = __builtin_amdgcn_readfirstlane(u);
-        wave = __builtin_amdgcn_readfirstlane(wave);
-    }
-    const cptr<StreamUnit> up = as_const(plan.units) + unit0 + u;
+    // Workgroup -> (unit, column band), from the host's list (which places
+    // the bands of one unit on one XCD)
+    const uint32_t wg = as_const(plan.wgs)[wg0 + static_cast<int>(blockIdx.x)];
+    if (wg == kNoWork) return;
+    const int u = static_cast<int>(wg & kWgUnitMask);
+    const int wave = static_cast<int>(wg >> kWgBandShift);
+    const cptr<StreamUnit> up = as_const(plan.units) + u;
     const int u_item = up->item, u_p = up->p, u_rows = up->rows, u_flags = up->flags;
     const cptr<DevItem> it = as_const(plan.items) + u_item;
     const int i0 = u_rows & 0xffff;
@@ -450,8 +442,8 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
         }
     };
 
-    // Source row y (its values in v) into the slots; closes an output row
-    // when y is its close row.
+    // Source row y (its values in hv) into the slots; then closes the output
+    // rows whose close row is y.
     auto process_row = [&](int y, const uint32_t (&hv)[P], cptr<float> wr) __attribute__((always_inline)) {
         float v[V];
 #pragma unroll
@@ -470,7 +462,9 @@ void stream_kernel(PlanView plan, int unit0, int n_units, int n_bands, void* out
                 acc[s][q].z = fmaf(ws, v[3 * q + 2], acc[s][q].z);
             }
         }
-        if (y == next_close) {   // wave-uniform
+        // every output row of the unit that closes on this row (several when
+        // the axis is upscaled, or at the bottom border), in order
+        while (y == next_close && base < i1) {   // wave-uniform
             const bool keep = base >= i0;
             if (keep) wave_lds_fence();
             // the closing slot goes to the wave's LDS row (kept rows only) and
@@ -533,13 +527,11 @@ template <int M, int KX, int PX>
 int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                         const Norm& norm, hipStream_t stream) {
     const int lds = stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4);
-    dim3 grid(static_cast<unsigned>(L.count) * static_cast<unsigned>(L.bands)), block(64);
+    dim3 grid(static_cast<unsigned>(L.count)), block(64);
     if (out_dtype == 1)
-        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1>), grid, block, lds, stream, plan, L.first, L.count,
-                           L.bands, out, norm);
+        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1>), grid, block, lds, stream, plan, L.first, out, norm);
     else
-        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 0>), grid, block, lds, stream, plan, L.first, L.count,
-                           L.bands, out, norm);
+        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 0>), grid, block, lds, stream, plan, L.first, out, norm);
     return static_cast<int>(hipGetLastError());
 }
 
@@ -567,8 +559,6 @@ bool stream_shape_supported(int m, int kx, int px) {
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream) {
     if (L.count <= 0) return 0;
-    if (L.bands <= 0 || int64_t(L.count) * L.bands > INT32_MAX)
-        return static_cast<int>(hipErrorInvalidConfiguration);
     if (!stream_shape_supported(L.m, L.kx, L.px) || stream_wave_bytes(L.px, L.kx, 4) > kStreamLdsBudget)
         return static_cast<int>(hipErrorInvalidConfiguration);
 #define VP_STREAM_CASE(MM, KK, PP) \

@@ -9,7 +9,9 @@
 //   int32      tile_prefix[n_items + 1]   general-kernel work of item b: [prefix[b], prefix[b+1])
 //   int32      indices[sum of padded counts]  source frame of every (frame pair, dt)
 //   int32      tables[...]                filter tables, 4-byte words
-//   StreamUnit units[...]                 streaming-kernel work units, grouped per launch
+//   StreamUnit units[...]                 streaming-kernel work units
+//   uint32     wgs[...]                   streaming-kernel workgroups, grouped per launch:
+//                                         unit index | column band << 20, or kNoWork
 //
 // Tables (word offsets into `tables`; items with the same axis share them):
 //   window table of an axis n_in -> n_out, K taps:
@@ -20,11 +22,11 @@
 //            its window to its close row; weight[s] is 2^24 times the weight
 //            of source row y in the output row that has slot s at y, or zero
 //            (the kernel reads source bytes as f16 denormals, b * 2^-24)
-//       int32 close_row[n_out + 1]   (the last entry is padding)
+//       int32 close_row[n_out + 1]   (the last entry is INT32_MAX)
 //         -- the row after which output row i is complete: the last row of its
-//            window, except that output rows whose windows all end at the bottom
-//            border close on consecutive rows n_in-1, n_in, n_in+1, ...; rows past
-//            n_in carry zero weights (one close per row)
+//            window, or the close row of output row i - 1 if that is later;
+//            never decreasing, and several output rows may close on one row
+//            (an upscaled axis, the bottom border)
 //   column table of an x axis (streaming kernel), KX taps, for output bands
 //   of `band` columns whose source pixels fit an LDS row of `row_px` pixels:
 //       int32 start[n_out]; float weight[n_out][KX]
@@ -77,9 +79,10 @@ struct DevItem {
 static_assert(sizeof(DevItem) == 104, "DevItem layout");
 
 // One streaming work unit: output rows [i0, i1) of padded frame position p
-// of an item; one single-wave workgroup per column band of the unit.  flags bit 0: the pair's two frames are the same source frame
-// (an image, or an odd count padded with its last index), so the unit
-// writes both temporal halves of the rows.
+// of an item; one single-wave workgroup per column band of the unit.
+// flags bit 0: the pair's two frames are the same source frame (an image,
+// or an odd count padded with its last index), so the unit writes both
+// temporal halves of the rows.
 struct StreamUnit {
     int32_t item;
     int32_t p;
@@ -94,6 +97,7 @@ struct PlanView {
     const int32_t* indices;
     const int32_t* tables;
     const StreamUnit* units;
+    const uint32_t* wgs;
     int32_t n_items;
     int32_t n_tiles;
 };
@@ -104,12 +108,18 @@ struct Norm {
     float z[3];   // -255 * mean_c: v = a_c * (R + z_c), the same value in pixel units
 };
 
-// One launch of the streaming kernel: units [first, first + count), all
-// with the same template shape and block size.
+// Streaming workgroup entries: unit index in the low 20 bits, column band
+// above; kNoWork marks an empty workgroup.
+constexpr uint32_t kWgUnitMask = (1u << 20) - 1;
+constexpr int kWgBandShift = 20;
+constexpr uint32_t kNoWork = 0xffffffffu;
+
+// One launch of the streaming kernel: workgroups wgs[first, first + count),
+// all with the same template shape.
 struct StreamLaunch {
     int32_t first, count;
     int32_t m, kx, px;       // accumulator slots, column taps, pixels per lane
-    int32_t bands;           // column bands per unit (workgroups per unit)
+    int64_t cost;            // host only: estimated work (source pixels read)
 };
 
 // Kernel launchers (vp_kernels.hip).  Return a hipError_t value.
