@@ -77,6 +77,7 @@ def lib() -> ctypes.CDLL:
                                              f64p, f64p, f64p]
         L.oracle_item_row.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64,
                                       f64p, f64p, i64, f64p]
+        L.oracle_patchify_item.argtypes = [u8p, i64, i64, i64, i32p, i64, f64p, f64p, f64p]
         L.oracle_layout.argtypes = [i64, i64p, i64p, i64p, i64p, i64p]
         _lib = L
     return _lib
@@ -186,6 +187,18 @@ def preprocess_item(frames: np.ndarray, indices, h: int, w: int, mean, std) -> n
                                         len(idx), h, w, _p(m, ctypes.c_double),
                                         _p(s, ctypes.c_double), _p(rows, ctypes.c_double)),
            "preprocess_item")
+    return rows
+
+
+def patchify_item(frames: np.ndarray, indices, mean, std) -> np.ndarray:
+    """Normalise + patchify only: frames uint8 [N][h][w][3], already at the
+    target size -> fp64 rows [t*(h/16)*(w/16)][1536]."""
+    f, idx, m, s = _item_args(frames, indices, mean, std)
+    n_src, h, w, _ = f.shape
+    rows = np.zeros((item_rows(len(idx), h, w), ROW), np.float64)
+    _check(lib().oracle_patchify_item(_p(f, ctypes.c_uint8), n_src, h, w, _p(idx, ctypes.c_int32),
+                                      len(idx), _p(m, ctypes.c_double), _p(s, ctypes.c_double),
+                                      _p(rows, ctypes.c_double)), "patchify_item")
     return rows
 
 

@@ -523,6 +523,45 @@ int oracle_preprocess_item(const uint8_t *frames, int64_t n_src, int64_t H, int6
 }
 
 /*
+ * Normalise and patchify only: the frames are already at the target size
+ * h x w (the cached path of Section 3.1.1, where sampling and resizing were
+ * done once offline and each RL stage still rescales, normalises and
+ * patchifies).  With the padded index list and (tt, i0, j0), (c, dt, y, x)
+ * decoded from (rho, k) as for the full path:
+ *   rows[rho][k] = normalise(frames[padded[2 tt + dt]][i0 + y][j0 + x][c]).
+ */
+int oracle_patchify_item(const uint8_t *frames, int64_t n_src, int64_t h, int64_t w,
+                         const int32_t *indices, int64_t n_idx, const double *mean,
+                         const double *std, double *rows)
+{
+    if (frames == NULL || mean == NULL || std == NULL || rows == NULL)
+        return OR_ERR_NULL;
+    int st = check_item(n_src, h, w, indices, n_idx, h, w);
+    if (st != OR_OK)
+        return st;
+    int32_t *padded = malloc(sizeof(int32_t) * (size_t)(n_idx + 1));
+    if (!padded)
+        return OR_ERR_NOMEM;
+    pad_indices(indices, n_idx, padded);
+    int64_t hg = h / OR_PATCH, wg = w / OR_PATCH;
+    int64_t frame_bytes = h * w * 3;
+    int64_t n_rows = oracle_item_rows(n_idx, h, w);
+    for (int64_t rho = 0; rho < n_rows; rho++) {
+        int64_t tt, i0, j0;
+        decode_row(rho, hg, wg, &tt, &i0, &j0);
+        for (int64_t k = 0; k < OR_ROW; k++) {
+            int64_t c, dt, y, x;
+            decode_col(k, &c, &dt, &y, &x);
+            const uint8_t *f = frames + (int64_t)padded[2 * tt + dt] * frame_bytes;
+            double r = (double)f[((i0 + y) * w + (j0 + x)) * 3 + c];
+            rows[rho * OR_ROW + k] = oracle_normalize(r, mean[c], std[c]);
+        }
+    }
+    free(padded);
+    return OR_OK;
+}
+
+/*
  * One output row rho of an item, computed element by element from the
  * direct two-dimensional sum (no separable pass, no frame buffer).  Used to
  * check sampled rows of workloads too large to recompute whole.

@@ -479,3 +479,72 @@ def test_errors_of_item_checks():
     with pytest.raises(oracle.OracleError) as e:
         oracle.preprocess_item(f, [0, 1], 32, 48, (0.5,) * 3, (0.5,) * 3)
     assert e.value.code == oracle.ERR_DIMS
+
+
+# -- normalise + patchify only (frames already at the target size) --------
+
+def test_patchify_only_inverse_by_reshape():
+    """Undoing the merge-window order of the patchify-only path with numpy
+    reshape/transpose gives the normalised, padded frames bit for bit."""
+    rng = np.random.default_rng(31)
+    n, h, w = 5, 64, 96
+    f = rng.integers(0, 256, size=(n, h, w, 3), dtype=np.uint8)
+    mean, std = (0.481, 0.458, 0.408), (0.269, 0.261, 0.276)
+    idx = [4, 0, 2]                                           # odd: padded with 2
+    rows = oracle.patchify_item(f, idx, mean, std)
+    t, hm, wm = 2, h // 32, w // 32
+    assert rows.shape == (t * hm * wm * 4, 1536)
+    v = rows.reshape(t, hm, wm, 2, 2, 3, 2, 16, 16)           # tt bh bw mh mw c dt y x
+    v = v.transpose(0, 6, 5, 1, 3, 7, 2, 4, 8).reshape(2 * t, 3, h, w)
+    ref = (f[[4, 0, 2, 2]].transpose(0, 3, 1, 2) / 255.0 - np.array(mean)[None, :, None, None]) \
+        / np.array(std)[None, :, None, None]
+    assert np.array_equal(v, ref)
+
+
+def test_patchify_only_row_and_column_order():
+    # the planted codes of the full path's order test, read back through the
+    # patchify-only path
+    H, W = 32, 96
+    vals = np.zeros((2, 3, H, W), np.int64)
+    ii, jj = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    vals[:, 0] = 10 * (ii // 16) + (jj // 16)
+    for fr in range(2):
+        vals[fr, 1] = 50 + 10 * fr
+        vals[fr, 2] = 16 * (ii % 16) + (jj % 16)
+    f = _identity_item(vals)
+    rows = oracle.patchify_item(f, [0, 1], (0.0,) * 3, (1 / 255,) * 3)
+    patch = np.rint(rows[:, :256].mean(1)).astype(int).tolist()
+    assert patch == [0, 1, 10, 11, 2, 3, 12, 13, 4, 5, 14, 15]
+    assert np.allclose(rows[:, 512:768], 50) and np.allclose(rows[:, 768:1024], 60)
+    assert np.allclose(rows[:, 1024:1280], np.arange(256)[None, :])
+
+
+def test_patchify_only_equals_full_path_at_identity_size():
+    """With the target equal to the source size the resize is the identity
+    (pinned above), so the full path and the patchify-only path agree
+    exactly, images and odd counts included."""
+    rng = np.random.default_rng(32)
+    f = rng.integers(0, 256, size=(4, 96, 64, 3), dtype=np.uint8)
+    mean, std = (0.3, 0.4, 0.5), (0.2, 0.25, 0.3)
+    for idx in ([1, 3], [2], [0, 3, 1], [3, 3, 0, 1]):
+        assert np.array_equal(oracle.patchify_item(f, idx, mean, std),
+                              oracle.preprocess_item(f, idx, 96, 64, mean, std))
+
+
+def test_patchify_only_constant_frame_closed_form():
+    f = np.full((1, 32, 64, 3), 200, np.uint8)
+    mean, std = (0.481, 0.458, 0.408), (0.269, 0.261, 0.276)
+    rows = oracle.patchify_item(f, [0], mean, std)
+    for c in range(3):
+        assert np.all(rows[:, 512 * c:512 * (c + 1)] == (200 / 255 - mean[c]) / std[c])
+
+
+def test_patchify_only_errors():
+    f = np.zeros((2, 32, 48, 3), np.uint8)               # 48 is not a multiple of 32
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.patchify_item(f, [0, 1], (0.5,) * 3, (0.5,) * 3)
+    assert e.value.code == oracle.ERR_DIMS
+    f = np.zeros((2, 32, 64, 3), np.uint8)
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.patchify_item(f, [0, 2], (0.5,) * 3, (0.5,) * 3)
+    assert e.value.code == oracle.ERR_INDEX
