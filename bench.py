@@ -60,7 +60,7 @@ def counter_traffic(workload_tag: str, sha: str):
     return d.get("hbm_bytes_per_call")
 
 
-def cpu_baseline(wl, frames_dev, planned, budget_s=12.0):
+def cpu_baseline(wl, frames_dev, planned, patch_only=False, budget_s=12.0):
     """The oracle, item by item in workload order, until `budget_s` seconds of
     oracle time have been spent (or the workload is done).  Each item's frame
     pairs are copied to the host and spread over a thread pool (ctypes
@@ -83,8 +83,11 @@ def cpu_baseline(wl, frames_dev, planned, budget_s=12.0):
                     for tt in range(len(padded) // 2)]
             del host
             t0 = time.perf_counter()
-            list(ex.map(lambda j: oracle.preprocess_item(j[0], [0, 1], j[1], j[2], wl.mean, wl.std),
-                        jobs))
+            if patch_only:
+                list(ex.map(lambda j: oracle.patchify_item(j[0], [0, 1], wl.mean, wl.std), jobs))
+            else:
+                list(ex.map(lambda j: oracle.preprocess_item(j[0], [0, 1], j[1], j[2], wl.mean,
+                                                             wl.std), jobs))
             spent += time.perf_counter() - t0
             frames_count += len(idx)
             pairs += len(jobs)
@@ -101,9 +104,12 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", type=int, default=4, choices=range(5),
                     help="workload configuration (4 = 64x256 frames 720x1280, the default)")
+    ap.add_argument("--patchify", action="store_true",
+                    help="time the normalise+patchify-only entry on the cached counterpart of "
+                         "workload 4 (64 x 256 frames already at 256x448) instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run plain 1 GiB device-to-device copies (twice) before the steps, "
@@ -129,7 +135,8 @@ def main():
     log(f"device {props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count} "
         f"mem={props.total_memory / 2**30:.0f} GiB")
 
-    wl = workloads.config(args.workload)
+    wl = workloads.patchify_config() if args.patchify else workloads.config(args.workload)
+    entry = vp.vp_patchify_batch if args.patchify else vp.vp_preprocess_batch
     log(f"workload {wl.name}")
     t0 = time.perf_counter()
     frames = [workloads.frames_torch(it, dev, chunk=32) for it in wl.items]
@@ -180,7 +187,7 @@ def main():
 
     def step():
         items, _ = plan_items()
-        vp.vp_preprocess_batch(items, wl.mean, wl.std, code, out, work, stream)
+        entry(items, wl.mean, wl.std, code, out, work, stream)
 
     for _ in range(args.warmup):
         step()
@@ -218,14 +225,14 @@ def main():
         f"({achieved / HBM_PEAK_GBPS:.1%} of 8 TB/s)")
     log("kernel ms per step: " + " ".join(f"{t:.3f}" for t in kern_ms))
 
-    tag = f"c{args.workload}"
+    tag = "p4" if args.patchify else f"c{args.workload}"
     sha = kernel_source_sha()
     traffic = counter_traffic(tag, sha)
 
     baseline = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        baseline = cpu_baseline(wl, frames, planned)
+        baseline = cpu_baseline(wl, frames, planned, patch_only=args.patchify)
         log(f"cpu baseline {baseline}")
 
     rec = {

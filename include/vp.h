@@ -186,6 +186,10 @@ int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw
  *   there on `stream` and the kernels read it.  It may be reused by the
  *   next call on the same stream.
  * stream: the HIP stream all work is enqueued on (0 = the null stream).
+ *   When a batch needs kernels of several shapes, the call runs them on up
+ *   to three more streams of the device (created once by the library, at
+ *   default priority), forked from `stream` and joined back into it with
+ *   events: to other work on `stream` the call is one ordered step.
  * out_rows is final when `stream` reaches the end of the enqueued work.
  * Errors: VP_ERR_NULL, VP_ERR_ARG (n_items < 1, bad dtype, std <= 0 or not
  * finite, misaligned pointers), VP_ERR_DIMS, VP_ERR_FRAMES, VP_ERR_INDEX,
@@ -199,8 +203,31 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
                             void* workspace, int64_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Normalise and patchify frames that are already at the target size: the
+ * cached path of Section 3.1.1, where sampling and resizing were done once
+ * offline and every RL stage still rescales, normalises and patchifies.
+ * Items as for vp_preprocess_batch, with dst_h == src_h and dst_w == src_w
+ * (multiples of 32); `indices` select and order the frames as before, odd
+ * counts padded with the last index.  The rows are those vp_preprocess_batch
+ * writes for the same items, whose resize is then the identity:
+ *   row cu[b] + ((tt*(h/32) + bh)*(w/32) + bw)*4 + mh*2 + mw,
+ *   column ((c*2 + dt)*16 + y)*16 + x  holds (F/255 - mean_c)/std_c of
+ *   F = frames[indices[2*tt + dt]][16*(2*bh + mh) + y][16*(2*bw + mw) + x][c].
+ * Arguments, ownership, asynchrony and stream as for vp_preprocess_batch;
+ * the workspace_bytes of vp_batch_layout on the same items suffice.  Each
+ * frames pointer must be 4-byte aligned.
+ * Errors: as vp_preprocess_batch, plus VP_ERR_DIMS when a target size is not
+ * its source size, VP_ERR_ARG when a frames pointer is not 4-byte aligned.
+ */
+int32_t vp_patchify_batch(const vp_item* items, int32_t n_items, const float* mean,
+                          const float* std, int32_t out_dtype, void* out_rows,
+                          int64_t out_rows_capacity, int32_t* grid_thw, int32_t* cu_seqlens,
+                          void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/*
  * Kernel timing hook (measurement only; not a step of the method).  The next
- * vp_preprocess_batch call made on this thread records `start` on its stream
+ * vp_preprocess_batch or vp_patchify_batch call made on this thread records
+ * `start` on its stream
  * immediately before its first kernel launch (after the plan upload) and
  * `stop` immediately after its last launch, then forgets both events, so
  * that hipEventElapsedTime(start, stop) is the device time of that call's

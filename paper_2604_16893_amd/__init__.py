@@ -31,7 +31,7 @@ VP_ROW = 1536
 VP_FACTOR = 32
 
 EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
-            "vp_batch_layout", "vp_preprocess_batch", "vp_status_string",
+            "vp_batch_layout", "vp_preprocess_batch", "vp_patchify_batch", "vp_status_string",
             "vp_last_error_message", "vp_set_kernel_events")
 
 
@@ -73,6 +73,7 @@ def lib() -> ctypes.CDLL:
         L.vp_batch_layout.argtypes = [itemp, i32, i32p, i32p, i64p, i64p]
         L.vp_preprocess_batch.argtypes = [itemp, i32, f32p, f32p, i32, ctypes.c_void_p, i64,
                                           i32p, i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
+        L.vp_patchify_batch.argtypes = L.vp_preprocess_batch.argtypes
         L.vp_set_kernel_events.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         L.vp_status_string.argtypes = [i32]
         L.vp_status_string.restype = ctypes.c_char_p
@@ -207,6 +208,17 @@ def vp_preprocess_batch(items: Sequence, mean, std, out_dtype: int, out_rows, wo
     current stream).  out_rows: device tensor [>= rows, 1536] of float32 or
     bfloat16 matching out_dtype; workspace: device uint8 tensor of at least
     the layout's workspace_bytes.  Returns (grid_thw, cu_seqlens)."""
+    return _run("vp_preprocess_batch", items, mean, std, out_dtype, out_rows, workspace, stream)
+
+
+def vp_patchify_batch(items: Sequence, mean, std, out_dtype: int, out_rows, workspace,
+                      stream=None):
+    """As vp_preprocess_batch, for frames already at the target size (every
+    item's dst_h, dst_w equal to its frames' H, W): normalise + patchify only."""
+    return _run("vp_patchify_batch", items, mean, std, out_dtype, out_rows, workspace, stream)
+
+
+def _run(name: str, items: Sequence, mean, std, out_dtype: int, out_rows, workspace, stream):
     import torch
     want = torch.bfloat16 if out_dtype == VP_OUT_BF16 else torch.float32
     if out_rows.dtype != want or out_rows.dim() != 2 or out_rows.shape[1] != VP_ROW \
@@ -220,12 +232,12 @@ def vp_preprocess_batch(items: Sequence, mean, std, out_dtype: int, out_rows, wo
     s = np.ascontiguousarray(np.asarray(std, np.float32).reshape(3))
     grid = np.zeros((B, 3), np.int32)
     cu = np.zeros(B + 1, np.int32)
-    _check(lib().vp_preprocess_batch(
+    _check(getattr(lib(), name)(
         b.arr, B, _ptr(m, ctypes.c_float), _ptr(s, ctypes.c_float), out_dtype,
         ctypes.c_void_p(out_rows.data_ptr()), out_rows.shape[0], _ptr(grid, ctypes.c_int32),
         _ptr(cu, ctypes.c_int32), ctypes.c_void_p(workspace.data_ptr()),
         workspace.numel() * workspace.element_size(), ctypes.c_void_p(_stream_handle(stream))),
-        "vp_preprocess_batch")
+        name)
     return grid, cu
 
 
@@ -248,6 +260,20 @@ def vp_set_kernel_events(start, stop):
     _check(lib().vp_set_kernel_events(ctypes.c_void_p(_event_handle(start)),
                                       ctypes.c_void_p(_event_handle(stop))),
            "vp_set_kernel_events")
+
+
+def patchify(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None):
+    """Allocate the outputs with torch and run vp_patchify_batch (frames
+    already at the target size).  Returns (rows, grid_thw, cu_seqlens)."""
+    import torch
+    code = VP_OUT_BF16 if out_dtype in ("bf16", VP_OUT_BF16) else VP_OUT_F32
+    grid, cu, rows, ws = vp_batch_layout(items)
+    dev = items[0].frames.device
+    out = torch.empty((rows, VP_ROW), dtype=torch.bfloat16 if code == VP_OUT_BF16 else torch.float32,
+                      device=dev)
+    work = torch.empty(ws, dtype=torch.uint8, device=dev)
+    vp_patchify_batch(items, mean, std, code, out, work, stream)
+    return out, grid, cu
 
 
 def preprocess(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None):

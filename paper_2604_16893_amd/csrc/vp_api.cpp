@@ -11,6 +11,7 @@
 #include <cstring>
 #include <algorithm>
 #include <map>
+#include <memory>
 #include <tuple>
 #include <mutex>
 #include <string>
@@ -135,7 +136,9 @@ struct Plan {
     std::vector<vp::DevItem> items;
     std::vector<int32_t> prefix;
     std::vector<int32_t> indices;
-    std::vector<int32_t> tables;
+    // the tables section: cached table words, each placed at its word offset
+    std::vector<std::pair<int32_t, std::shared_ptr<const std::vector<int32_t>>>> tables;
+    size_t table_words = 0;
     std::vector<vp::StreamUnit> units;
     std::vector<uint32_t> wgs;   // streaming workgroups: unit | band << 20, grouped per launch
     std::vector<vp::StreamLaunch> launches;
@@ -313,6 +316,55 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShap
     return best >= 0;
 }
 
+// Process-wide cache of per-axis tables.  The same axes recur from call to
+// call (an RL loop preprocesses batches of the same shapes every step), and
+// building them is most of the host's work for a batch of many shapes.
+// Entries are immutable once built and shared by pointer; a cache is
+// cleared when it reaches kTableCacheMax entries.
+struct AxisEntry {
+    AxisFilter f;
+    std::vector<int32_t> words;   // the window table: start, count, weight
+};
+struct SlotEntry {
+    int32_t m = -1;               // slots, or -1 if the axis needs too many
+    std::vector<int32_t> words;
+};
+using ColumnKey = std::tuple<int32_t, int32_t, int32_t, int32_t, int32_t>;   // n_in, n_out, kx, band, row_px
+
+constexpr size_t kTableCacheMax = 4096;
+std::mutex g_cache_mu;
+std::map<std::pair<int32_t, int32_t>, std::shared_ptr<const AxisEntry>> g_axis_cache;
+std::map<std::pair<int32_t, int32_t>, std::shared_ptr<const SlotEntry>> g_slot_cache;
+std::map<ColumnKey, std::shared_ptr<const std::vector<int32_t>>> g_column_cache;
+
+// The entry for `key`, built by `make` (outside the lock) on a miss.  If two
+// threads miss together, the first entry stored wins; both are identical.
+template <class Map, class Make>
+typename Map::mapped_type cached(Map& map, const typename Map::key_type& key, Make make) {
+    {
+        std::lock_guard<std::mutex> lk(g_cache_mu);
+        auto it = map.find(key);
+        if (it != map.end()) return it->second;
+    }
+    typename Map::mapped_type v = make();
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    if (map.size() >= kTableCacheMax) map.clear();
+    return map.emplace(key, std::move(v)).first->second;
+}
+
+std::shared_ptr<const AxisEntry> make_axis_entry(int32_t n_in, int32_t n_out) {
+    auto e = std::make_shared<AxisEntry>();
+    build_axis(n_in, n_out, axis_taps(n_in, n_out), &e->f);
+    const AxisFilter& f = e->f;
+    e->words.reserve(2 * f.start.size() + f.weight.size());
+    e->words.insert(e->words.end(), f.start.begin(), f.start.end());
+    e->words.insert(e->words.end(), f.count.begin(), f.count.end());
+    const size_t wbase = e->words.size();
+    e->words.resize(wbase + f.weight.size());
+    std::memcpy(e->words.data() + wbase, f.weight.data(), f.weight.size() * sizeof(float));
+    return e;
+}
+
 int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
@@ -323,53 +375,56 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     p->cu.assign(n + 1, 0);
     p->indices.clear();
     p->tables.clear();
-    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, AxisFilter>> axes;  // -> (word offset, filter)
+    p->table_words = 0;
+    // Tables come from the process-wide cache; each one used by the batch is
+    // copied into the plan once, and the per-call maps keep the cache
+    // entries alive while the call uses them.
+    auto append = [&](std::shared_ptr<const std::vector<int32_t>> words) -> int32_t {
+        const int32_t o = static_cast<int32_t>(p->table_words);
+        p->table_words += words->size();
+        p->tables.emplace_back(o, std::move(words));
+        return o;
+    };
+    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, std::shared_ptr<const AxisEntry>>> axes;
     auto table_for = [&](int32_t n_in, int32_t n_out, int32_t* off) -> const AxisFilter* {
-        auto key = std::make_pair(n_in, n_out);
+        const auto key = std::make_pair(n_in, n_out);
         auto found = axes.find(key);
         if (found == axes.end()) {
-            AxisFilter f;
-            build_axis(n_in, n_out, axis_taps(n_in, n_out), &f);
-            const int32_t o = static_cast<int32_t>(p->tables.size());
-            p->tables.insert(p->tables.end(), f.start.begin(), f.start.end());
-            p->tables.insert(p->tables.end(), f.count.begin(), f.count.end());
-            const size_t wbase = p->tables.size();
-            p->tables.resize(wbase + f.weight.size());
-            std::memcpy(p->tables.data() + wbase, f.weight.data(), f.weight.size() * sizeof(float));
-            found = axes.emplace(key, std::make_pair(o, std::move(f))).first;
+            auto e = cached(g_axis_cache, key, [&] { return make_axis_entry(n_in, n_out); });
+            const int32_t o = append(std::shared_ptr<const std::vector<int32_t>>(e, &e->words));
+            found = axes.emplace(key, std::make_pair(o, e)).first;
         }
         *off = found->second.first;
-        return &found->second.second;
+        return &found->second.second->f;
     };
-
-    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, int32_t>> slot_tables;  // -> (offset, m)
+    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, std::shared_ptr<const SlotEntry>>> slot_tables;
     auto slots_for = [&](const AxisFilter& f, int32_t* off, int32_t* m) -> bool {
-        auto key = std::make_pair(f.n_in, f.n_out);
+        const auto key = std::make_pair(f.n_in, f.n_out);
         auto found = slot_tables.find(key);
         if (found == slot_tables.end()) {
-            std::vector<int32_t> words;
-            const int32_t mm = build_slots(f, &words);
-            int32_t o = -1;
-            if (mm > 0) {
-                o = static_cast<int32_t>(p->tables.size());
-                p->tables.insert(p->tables.end(), words.begin(), words.end());
-            }
-            found = slot_tables.emplace(key, std::make_pair(o, mm)).first;
+            auto e = cached(g_slot_cache, key, [&] {
+                auto v = std::make_shared<SlotEntry>();
+                v->m = build_slots(f, &v->words);
+                return std::shared_ptr<const SlotEntry>(std::move(v));
+            });
+            const int32_t o = e->m > 0 ? append(std::shared_ptr<const std::vector<int32_t>>(e, &e->words)) : -1;
+            found = slot_tables.emplace(key, std::make_pair(o, e)).first;
         }
         *off = found->second.first;
-        *m = found->second.second;
+        *m = found->second.second->m;
         return found->second.first >= 0;
     };
-    std::map<std::tuple<int32_t, int32_t, int32_t, int32_t, int32_t>, int32_t> column_tables;
+    std::map<ColumnKey, int32_t> column_tables;
     auto columns_for = [&](const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px) -> int32_t {
-        auto key = std::make_tuple(f.n_in, f.n_out, kx, band, row_px);
+        const ColumnKey key = std::make_tuple(f.n_in, f.n_out, kx, band, row_px);
         auto found = column_tables.find(key);
         if (found == column_tables.end()) {
-            std::vector<int32_t> words;
-            build_columns(f, kx, band, row_px, &words);
-            const int32_t o = static_cast<int32_t>(p->tables.size());
-            p->tables.insert(p->tables.end(), words.begin(), words.end());
-            found = column_tables.emplace(key, o).first;
+            auto e = cached(g_column_cache, key, [&] {
+                auto v = std::make_shared<std::vector<int32_t>>();
+                build_columns(f, kx, band, row_px, v.get());
+                return std::shared_ptr<const std::vector<int32_t>>(std::move(v));
+            });
+            found = column_tables.emplace(key, append(e)).first;
         }
         return found->second;
     };
@@ -439,12 +494,14 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     // rows.
     constexpr int64_t kWaveSlots = 256 * 20;
     int64_t wave_rows = 0;   // source rows that all workgroups stream, whole frames
+    int64_t stream_frames = 0;
     for (int32_t b = 0; b < n; ++b) {
         const vp::DevItem& d = p->items[b];
         if (d.route != vp::kRouteStream) continue;
         for (int32_t tt = 0; tt < d.t; ++tt) {
             const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
             wave_rows += int64_t(same ? 1 : 2) * shapes[b].bands * d.H;
+            stream_frames += same ? 1 : 2;
         }
     }
     const int64_t max_src_rows = wave_rows / (kWaveSlots * 8);
@@ -455,6 +512,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         int64_t cost;
     };
     std::vector<Keyed> keyed;
+    keyed.reserve(static_cast<size_t>(stream_frames));
     for (int32_t b = 0; b < n; ++b) {
         const vp::DevItem& d = p->items[b];
         if (d.route != vp::kRouteStream) continue;
@@ -491,35 +549,48 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     // of neighbouring bands through its L2; a unit with fewer bands than the
     // others of its eight leaves empty entries.  Units are sorted by band
     // count first, which keeps those rare.
-    std::stable_sort(keyed.begin(), keyed.end(), [](const Keyed& a, const Keyed& c) {
-        return a.key != c.key ? a.key < c.key : a.bands < c.bands;
-    });
     if (keyed.size() > vp::kWgUnitMask + 1)
         return fail(VP_ERR_CAPACITY, "batch has more than 2^20 streaming work units");
+    // order: by shape, then band count, then as generated (a grouping: the
+    // units of one item are consecutive and share both)
+    std::map<std::pair<std::tuple<int32_t, int32_t, int32_t>, int32_t>, std::vector<uint32_t>> groups;
+    for (size_t k = 0; k < keyed.size();) {
+        size_t k1 = k + 1;
+        while (k1 < keyed.size() && keyed[k1].key == keyed[k].key && keyed[k1].bands == keyed[k].bands) ++k1;
+        auto& g = groups[std::make_pair(keyed[k].key, keyed[k].bands)];
+        for (; k < k1; ++k) g.push_back(static_cast<uint32_t>(k));
+    }
+    std::vector<uint32_t> order;
+    order.reserve(keyed.size());
+    for (const auto& g : groups) order.insert(order.end(), g.second.begin(), g.second.end());
     p->units.clear();
     p->wgs.clear();
     p->launches.clear();
-    for (size_t k0 = 0; k0 < keyed.size();) {
+    p->units.reserve(keyed.size());
+    p->wgs.reserve(keyed.size() * 8);
+    for (size_t k0 = 0; k0 < order.size();) {
+        const auto& key0 = keyed[order[k0]].key;
         size_t k1 = k0;
-        while (k1 < keyed.size() && keyed[k1].key == keyed[k0].key) ++k1;
+        while (k1 < order.size() && keyed[order[k1]].key == key0) ++k1;
         vp::StreamLaunch L{};
         L.first = static_cast<int32_t>(p->wgs.size());
-        L.m = std::get<0>(keyed[k0].key);
-        L.kx = std::get<1>(keyed[k0].key);
-        L.px = std::get<2>(keyed[k0].key);
+        L.m = std::get<0>(key0);
+        L.kx = std::get<1>(key0);
+        L.px = std::get<2>(key0);
         for (size_t c0 = k0; c0 < k1; c0 += 8) {
             const size_t c1 = std::min(c0 + 8, k1);
             int32_t rounds = 0;
-            for (size_t k = c0; k < c1; ++k) rounds = std::max(rounds, keyed[k].bands);
+            for (size_t k = c0; k < c1; ++k) rounds = std::max(rounds, keyed[order[k]].bands);
             const uint32_t u0 = static_cast<uint32_t>(p->units.size());
             for (size_t k = c0; k < c1; ++k) {
-                p->units.push_back(keyed[k].unit);
-                L.cost += keyed[k].cost * keyed[k].bands;
+                const Keyed& e = keyed[order[k]];
+                p->units.push_back(e.unit);
+                L.cost += e.cost * e.bands;
             }
             for (int32_t r = 0; r < rounds; ++r)
                 for (size_t x = 0; x < 8; ++x) {
                     const size_t k = c0 + x;
-                    p->wgs.push_back(k < c1 && r < keyed[k].bands
+                    p->wgs.push_back(k < c1 && r < keyed[order[k]].bands
                                          ? (u0 + static_cast<uint32_t>(x)) | (static_cast<uint32_t>(r) << vp::kWgBandShift)
                                          : vp::kNoWork);
                 }
@@ -533,9 +604,69 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
     p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
     p->off_tables = align_up(p->off_indices + sizeof(int32_t) * p->indices.size());
-    p->off_units = align_up(p->off_tables + sizeof(int32_t) * p->tables.size());
+    p->off_units = align_up(p->off_tables + sizeof(int32_t) * p->table_words);
     p->off_wgs = align_up(p->off_units + sizeof(vp::StreamUnit) * p->units.size());
     p->bytes = align_up(p->off_wgs + sizeof(uint32_t) * p->wgs.size());
+    return VP_OK;
+}
+
+// Plan of vp_patchify_batch: items whose frames are already at the target
+// size; one workgroup per merge-window row (32 pixel rows) of a frame pair.
+int32_t build_patch_plan(const vp_item* items, int32_t n, Plan* p) {
+    if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
+    if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    p->items.assign(n, vp::DevItem{});
+    p->prefix.assign(n + 1, 0);
+    p->grid.assign(size_t(n) * 3, 0);
+    p->cu.assign(n + 1, 0);
+    p->indices.clear();
+    p->tables.clear();
+    p->table_words = 0;
+    p->units.clear();
+    p->wgs.clear();
+    p->launches.clear();
+    p->generic_cost = 0;
+    int64_t rows = 0, tiles = 0;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp_item& it = items[b];
+        int32_t st = validate_item(it, b);
+        if (st != VP_OK) return st;
+        const std::string at = "item " + std::to_string(b) + ": ";
+        if (it.dst_h != it.src_h || it.dst_w != it.src_w)
+            return fail(VP_ERR_DIMS, at + "vp_patchify_batch needs frames already at the target size");
+        if (reinterpret_cast<uintptr_t>(it.frames) % 4 != 0)
+            return fail(VP_ERR_ARG, at + "frames must be 4-byte aligned");
+        vp::DevItem& d = p->items[b];
+        d.frames = it.frames;
+        d.frame_bytes = int64_t(it.src_h) * it.src_w * 3;
+        d.H = d.h = it.dst_h;
+        d.W = d.w = it.dst_w;
+        d.t = (it.n_idx + 1) / 2;
+        d.hm = it.dst_h / vp::kWin;
+        d.wm = it.dst_w / vp::kWin;
+        d.idx_off = static_cast<int32_t>(p->indices.size());
+        for (int32_t k = 0; k < 2 * d.t; ++k)
+            p->indices.push_back(it.indices[k < it.n_idx ? k : it.n_idx - 1]);
+        d.route = vp::kRoutePatch;
+        d.row_off = rows;
+        p->grid[3 * b + 0] = d.t;
+        p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
+        p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
+        rows += int64_t(d.t) * (it.dst_h / vp::kPatch) * (it.dst_w / vp::kPatch);
+        tiles += int64_t(d.t) * d.hm;
+        if (rows > INT32_MAX || tiles > INT32_MAX)
+            return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 rows");
+        p->cu[b + 1] = static_cast<int32_t>(rows);
+        p->prefix[b + 1] = static_cast<int32_t>(tiles);
+    }
+    p->total_rows = rows;
+    p->off_items = 0;
+    p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
+    p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
+    p->off_tables = align_up(p->off_indices + sizeof(int32_t) * p->indices.size());
+    p->off_units = p->off_tables;
+    p->off_wgs = p->off_tables;
+    p->bytes = p->off_tables;
     return VP_OK;
 }
 
@@ -599,15 +730,21 @@ int32_t upload_plan(const Plan& p, void* workspace, hipStream_t stream) {
         s.cap = cap;
     }
     auto* base = static_cast<uint8_t*>(s.host);
-    std::memset(base, 0, p.bytes);
-    std::memcpy(base + p.off_items, p.items.data(), sizeof(vp::DevItem) * p.items.size());
-    std::memcpy(base + p.off_prefix, p.prefix.data(), sizeof(int32_t) * p.prefix.size());
-    std::memcpy(base + p.off_indices, p.indices.data(), sizeof(int32_t) * p.indices.size());
-    std::memcpy(base + p.off_tables, p.tables.data(), sizeof(int32_t) * p.tables.size());
-    if (!p.units.empty())
-        std::memcpy(base + p.off_units, p.units.data(), sizeof(vp::StreamUnit) * p.units.size());
-    if (!p.wgs.empty())
-        std::memcpy(base + p.off_wgs, p.wgs.data(), sizeof(uint32_t) * p.wgs.size());
+    // each section, then zeros up to the next one (the gaps are never read;
+    // zeroing them keeps the blob deterministic)
+    auto put = [&](size_t off, const void* src, size_t n, size_t next) {
+        if (n != 0) std::memcpy(base + off, src, n);
+        std::memset(base + off + n, 0, next - off - n);
+    };
+    put(p.off_items, p.items.data(), sizeof(vp::DevItem) * p.items.size(), p.off_prefix);
+    put(p.off_prefix, p.prefix.data(), sizeof(int32_t) * p.prefix.size(), p.off_indices);
+    put(p.off_indices, p.indices.data(), sizeof(int32_t) * p.indices.size(), p.off_tables);
+    for (const auto& part : p.tables)
+        std::memcpy(base + p.off_tables + sizeof(int32_t) * part.first, part.second->data(),
+                    sizeof(int32_t) * part.second->size());
+    put(p.off_tables + sizeof(int32_t) * p.table_words, nullptr, 0, p.off_units);
+    put(p.off_units, p.units.data(), sizeof(vp::StreamUnit) * p.units.size(), p.off_wgs);
+    put(p.off_wgs, p.wgs.data(), sizeof(uint32_t) * p.wgs.size(), p.bytes);
     e = hipMemcpyAsync(workspace, s.host, p.bytes, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
     e = hipEventRecord(s.done, stream);
@@ -726,6 +863,72 @@ int32_t run_launches(const Plan& p, const vp::PlanView& view, void* out_rows, in
     return st;
 }
 
+// Shared body of vp_preprocess_batch (resample + normalise + patchify) and
+// vp_patchify_batch (frames already at the target size).
+int32_t run_batch(bool patch_only, const vp_item* items, int32_t n_items, const float* mean,
+                  const float* std, int32_t out_dtype, void* out_rows, int64_t out_rows_capacity,
+                  int32_t* grid_thw, int32_t* cu_seqlens, void* workspace, int64_t workspace_bytes,
+                  hipStream_t stream) {
+    if (mean == nullptr || std == nullptr || out_rows == nullptr || workspace == nullptr)
+        return fail(VP_ERR_NULL, "mean, std, out_rows and workspace must be non-NULL");
+    if (out_dtype != VP_OUT_F32 && out_dtype != VP_OUT_BF16)
+        return fail(VP_ERR_ARG, "out_dtype must be VP_OUT_F32 or VP_OUT_BF16");
+    if (reinterpret_cast<uintptr_t>(out_rows) % 16 != 0)
+        return fail(VP_ERR_ARG, "out_rows must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+        return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
+    vp::Norm norm;
+    for (int c = 0; c < 3; ++c) {
+        if (!(std[c] > 0.0f) || !std::isfinite(std[c]) || !std::isfinite(mean[c]))
+            return fail(VP_ERR_ARG, "std must be positive and finite, mean finite");
+        norm.a[c] = static_cast<float>(1.0 / (255.0 * static_cast<double>(std[c])));
+        norm.b[c] = static_cast<float>(-static_cast<double>(mean[c]) / static_cast<double>(std[c]));
+        norm.z[c] = static_cast<float>(-255.0 * static_cast<double>(mean[c]));
+    }
+    Plan p;
+    int32_t st = patch_only ? build_patch_plan(items, n_items, &p) : build_plan(items, n_items, &p);
+    if (st != VP_OK) return st;
+    if (out_rows_capacity < p.total_rows)
+        return fail(VP_ERR_CAPACITY, "out_rows holds " + std::to_string(out_rows_capacity) +
+                                         " rows, batch needs " + std::to_string(p.total_rows));
+    if (workspace_bytes < static_cast<int64_t>(p.bytes))
+        return fail(VP_ERR_CAPACITY, "workspace holds " + std::to_string(workspace_bytes) +
+                                         " bytes, plan needs " + std::to_string(p.bytes));
+    st = upload_plan(p, workspace, stream);
+    if (st != VP_OK) return st;
+    hipEvent_t t_start = g_timing_start, t_stop = g_timing_stop;
+    g_timing_start = g_timing_stop = nullptr;
+    if (t_start != nullptr) {
+        const hipError_t e = hipEventRecord(t_start, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing start)");
+    }
+    auto* ws = static_cast<uint8_t*>(workspace);
+    vp::PlanView view;
+    view.items = reinterpret_cast<const vp::DevItem*>(ws + p.off_items);
+    view.tile_prefix = reinterpret_cast<const int32_t*>(ws + p.off_prefix);
+    view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
+    view.tables = reinterpret_cast<const int32_t*>(ws + p.off_tables);
+    view.units = reinterpret_cast<const vp::StreamUnit*>(ws + p.off_units);
+    view.wgs = reinterpret_cast<const uint32_t*>(ws + p.off_wgs);
+    view.n_items = n_items;
+    view.n_tiles = p.prefix[n_items];
+    if (patch_only) {
+        const int err = vp::launch_patchify(view, out_rows, out_dtype, norm, stream);
+        if (err != 0) return hip_fail(static_cast<hipError_t>(err), "patchify kernel launch");
+    } else {
+        st = run_launches(p, view, out_rows, out_dtype, norm, stream);
+        if (st != VP_OK) return st;
+    }
+    if (t_stop != nullptr) {
+        const hipError_t e = hipEventRecord(t_stop, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");
+    }
+    if (grid_thw) std::memcpy(grid_thw, p.grid.data(), sizeof(int32_t) * p.grid.size());
+    if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
+    g_last_error.clear();
+    return VP_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -838,61 +1041,17 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
                             const float* std, int32_t out_dtype, void* out_rows,
                             int64_t out_rows_capacity, int32_t* grid_thw, int32_t* cu_seqlens,
                             void* workspace, int64_t workspace_bytes, hipStream_t stream) {
-    if (mean == nullptr || std == nullptr || out_rows == nullptr || workspace == nullptr)
-        return fail(VP_ERR_NULL, "mean, std, out_rows and workspace must be non-NULL");
-    if (out_dtype != VP_OUT_F32 && out_dtype != VP_OUT_BF16)
-        return fail(VP_ERR_ARG, "out_dtype must be VP_OUT_F32 or VP_OUT_BF16");
-    if (reinterpret_cast<uintptr_t>(out_rows) % 16 != 0)
-        return fail(VP_ERR_ARG, "out_rows must be 16-byte aligned");
-    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
-        return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
-    vp::Norm norm;
-    for (int c = 0; c < 3; ++c) {
-        if (!(std[c] > 0.0f) || !std::isfinite(std[c]) || !std::isfinite(mean[c]))
-            return fail(VP_ERR_ARG, "std must be positive and finite, mean finite");
-        norm.a[c] = static_cast<float>(1.0 / (255.0 * static_cast<double>(std[c])));
-        norm.b[c] = static_cast<float>(-static_cast<double>(mean[c]) / static_cast<double>(std[c]));
-        norm.z[c] = static_cast<float>(-255.0 * static_cast<double>(mean[c]));
-    }
-    Plan p;
-    int32_t st = build_plan(items, n_items, &p);
-    if (st != VP_OK) return st;
-    if (out_rows_capacity < p.total_rows)
-        return fail(VP_ERR_CAPACITY, "out_rows holds " + std::to_string(out_rows_capacity) +
-                                         " rows, batch needs " + std::to_string(p.total_rows));
-    if (workspace_bytes < static_cast<int64_t>(p.bytes))
-        return fail(VP_ERR_CAPACITY, "workspace holds " + std::to_string(workspace_bytes) +
-                                         " bytes, plan needs " + std::to_string(p.bytes));
-    st = upload_plan(p, workspace, stream);
-    if (st != VP_OK) return st;
-    hipEvent_t t_start = g_timing_start, t_stop = g_timing_stop;
-    g_timing_start = g_timing_stop = nullptr;
-    if (t_start != nullptr) {
-        const hipError_t e = hipEventRecord(t_start, stream);
-        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing start)");
-    }
-    auto* ws = static_cast<uint8_t*>(workspace);
-    vp::PlanView view;
-    view.items = reinterpret_cast<const vp::DevItem*>(ws + p.off_items);
-    view.tile_prefix = reinterpret_cast<const int32_t*>(ws + p.off_prefix);
-    view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
-    view.tables = reinterpret_cast<const int32_t*>(ws + p.off_tables);
-    view.units = reinterpret_cast<const vp::StreamUnit*>(ws + p.off_units);
-    view.wgs = reinterpret_cast<const uint32_t*>(ws + p.off_wgs);
-    view.n_items = n_items;
-    view.n_tiles = p.prefix[n_items];
-    st = run_launches(p, view, out_rows, out_dtype, norm, stream);
-    if (st != VP_OK) return st;
-    if (t_stop != nullptr) {
-        const hipError_t e = hipEventRecord(t_stop, stream);
-        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");
-    }
-    if (grid_thw) std::memcpy(grid_thw, p.grid.data(), sizeof(int32_t) * p.grid.size());
-    if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
-    g_last_error.clear();
-    return VP_OK;
+    return run_batch(false, items, n_items, mean, std, out_dtype, out_rows, out_rows_capacity,
+                     grid_thw, cu_seqlens, workspace, workspace_bytes, stream);
 }
 
+int32_t vp_patchify_batch(const vp_item* items, int32_t n_items, const float* mean,
+                          const float* std, int32_t out_dtype, void* out_rows,
+                          int64_t out_rows_capacity, int32_t* grid_thw, int32_t* cu_seqlens,
+                          void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+    return run_batch(true, items, n_items, mean, std, out_dtype, out_rows, out_rows_capacity,
+                     grid_thw, cu_seqlens, workspace, workspace_bytes, stream);
+}
 const char* vp_status_string(int32_t status) {
     switch (status) {
         case VP_OK: return "VP_OK";

@@ -32,6 +32,7 @@
 // splits the window into rh x cw sub-tiles.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "vp_plan.h"
@@ -160,6 +161,85 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
         float4* dst = reinterpret_cast<float4*>(static_cast<float*>(out) + row0 * kRow);
         for (int e = tid; e < kWinElems / 4; e += kGenericThreads)
             dst[e] = reinterpret_cast<const float4*>(stage)[e];
+    }
+}
+
+// ===========================================================================
+// Normalise + patchify kernel (frames already at the target size)
+// ===========================================================================
+
+// One workgroup of four waves per merge-window row (32 pixel rows) of one
+// frame pair.  Wave (dt, mh) takes pixel rows 16*mh .. 16*mh + 15 of frame
+// dt of the pair; lane (y, g) owns 8 pixels (24 bytes) of row y, at 8*g in
+// each merge window.  Window by window along the row, with the next
+// window's bytes already in flight, a lane normalises its 24 values and
+// stores three 16-byte pieces of 8 values, one per channel: for a fixed
+// channel the wave's stores fill two whole 512-byte blocks of output (one
+// per patch of its patch row), so every store is fully coalesced.
+template <int OUT_BF16>
+__global__ __launch_bounds__(256) void patchify_kernel(PlanView plan, void* out, Norm norm) {
+    using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
+    const int tile = blockIdx.x;
+    const int b = find_item(plan.tile_prefix, plan.n_items, tile);
+    const cptr<DevItem> it = as_const(plan.items) + b;
+    const int local = tile - plan.tile_prefix[b];
+    const int hm = it->hm, wm = it->wm, w = it->w;
+    const int bh = local % hm;
+    const int tt = local / hm;
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const int dt = wv >> 1, mh = wv & 1;
+    const int y = lane >> 2, g = lane & 3;
+    const int f = as_const(plan.indices)[it->idx_off + 2 * tt + dt];
+    // 4-byte aligned: the frames pointer is (checked on the host), and every
+    // offset below is a multiple of 24 bytes
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(
+        it->frames + int64_t(f) * it->frame_bytes + (int64_t(32 * bh + 16 * mh + y) * w + 8 * g) * 3);
+    const int64_t row0 = it->row_off + (int64_t(tt) * hm + bh) * wm * 4 + mh * 2 + (g >> 1);
+    elem_t* dst = static_cast<elem_t*>(out) + row0 * kRow + (dt * 16 + y) * 16 + (g & 1) * 8;
+    const float a[3] = {norm.a[0], norm.a[1], norm.a[2]};
+    const float z[3] = {norm.z[0], norm.z[1], norm.z[2]};
+
+    uint32_t cur[6], nxt[6];
+#pragma unroll
+    for (int k = 0; k < 6; ++k) cur[k] = src[k];
+    for (int bw = 0; bw < wm; ++bw) {
+        if (bw + 1 < wm) {
+#pragma unroll
+            for (int k = 0; k < 6; ++k) nxt[k] = src[24 * (bw + 1) + k];   // 96 bytes per window
+        }
+        elem_t* d = dst + int64_t(bw) * 4 * kRow;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            float v[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int byte = 3 * q + c;
+                const float x = float((cur[byte >> 2] >> (8 * (byte & 3))) & 255u);
+                v[q] = (x + z[c]) * a[c];   // (F/255 - mean)/std as a * (F - 255 mean)
+            }
+            using u4v = unsigned __attribute__((ext_vector_type(4)));
+            if constexpr (OUT_BF16 != 0) {
+                u4v pk;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    using f2 = float __attribute__((ext_vector_type(2)));
+                    using b2 = __bf16 __attribute__((ext_vector_type(2)));
+                    const f2 pair = {v[2 * e], v[2 * e + 1]};
+                    pk[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, b2));   // RNE
+                }
+                __builtin_nontemporal_store(pk, reinterpret_cast<u4v*>(d + c * 512));
+            } else {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const u4v pk = {__float_as_uint(v[4 * h]), __float_as_uint(v[4 * h + 1]),
+                                    __float_as_uint(v[4 * h + 2]), __float_as_uint(v[4 * h + 3])};
+                    __builtin_nontemporal_store(pk, reinterpret_cast<u4v*>(d + c * 512 + 4 * h));
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 6; ++k) cur[k] = nxt[k];
     }
 }
 
@@ -536,6 +616,17 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 }
 
 }  // namespace
+
+int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
+                    hipStream_t stream) {
+    if (plan.n_tiles <= 0) return 0;
+    dim3 grid(plan.n_tiles), block(256);
+    if (out_dtype == 1)
+        hipLaunchKernelGGL(patchify_kernel<1>, grid, block, 0, stream, plan, out, norm);
+    else
+        hipLaunchKernelGGL(patchify_kernel<0>, grid, block, 0, stream, plan, out, norm);
+    return static_cast<int>(hipGetLastError());
+}
 
 int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
                    hipStream_t stream) {

@@ -58,7 +58,7 @@ constexpr int stream_wave_bytes(int px, int kx, int elem_bytes) {
 }
 
 // Kernel an item is routed to.
-enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1 };
+enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1, kRoutePatch = 2 };
 
 struct DevItem {
     const uint8_t* frames;   // [n_src][H][W][3]
@@ -127,6 +127,10 @@ int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& n
                    hipStream_t stream);
 int launch_stream(const PlanView& plan, const StreamLaunch& launch, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream);
+// Normalise + patchify of frames already at the target size: one workgroup
+// per merge-window row of a frame pair (tile_prefix counts them per item).
+int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
+                    hipStream_t stream);
 // Whether a (m, kx, px) shape has a compiled streaming kernel.
 bool stream_shape_supported(int m, int kx, int px);
 

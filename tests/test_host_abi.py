@@ -194,6 +194,37 @@ def test_preprocess_errors_before_any_gpu_work():
     assert b"outside [0, 4)" in vp.lib().vp_last_error_message()
 
 
+def _raw_patchify(items, mean=(0.5, 0.5, 0.5), std=(0.5, 0.5, 0.5), dtype=vp.VP_OUT_BF16,
+                  out=0x100000, cap=1 << 30, ws=0x200000, ws_bytes=1 << 30):
+    b = vp._Batch(items)
+    m = (ctypes.c_float * 3)(*mean)
+    s = (ctypes.c_float * 3)(*std)
+    return vp.lib().vp_patchify_batch(b.arr, len(b), m, s, dtype, ctypes.c_void_p(out), cap,
+                                      None, None, ctypes.c_void_p(ws), ws_bytes, None)
+
+
+def test_patchify_errors_before_any_gpu_work():
+    """The patchify-only entry takes frames already at the target size; every
+    failure is detected on the host before anything is enqueued."""
+    ok = vp.Item((0x10000, 4, 64, 96), [0, 3], 64, 96)
+    _, _, rows, need = vp.vp_batch_layout([ok])
+    assert _raw_patchify([vp.Item((0x10000, 4, 64, 96), [0, 3], 64, 64)]) == vp.VP_ERR_DIMS
+    assert b"already at the target size" in vp.lib().vp_last_error_message()
+    assert _raw_patchify([vp.Item((0x10000, 4, 60, 96), [0, 3], 60, 96)]) == vp.VP_ERR_DIMS
+    assert _raw_patchify([vp.Item((0x10002, 4, 64, 96), [0, 3], 64, 96)]) == vp.VP_ERR_ARG
+    assert b"4-byte aligned" in vp.lib().vp_last_error_message()
+    assert _raw_patchify([vp.Item((0x10000, 4, 64, 96), [4], 64, 96)]) == vp.VP_ERR_INDEX
+    assert _raw_patchify([ok], std=(0.5, 0.0, 0.5)) == vp.VP_ERR_ARG
+    assert _raw_patchify([ok], dtype=7) == vp.VP_ERR_ARG
+    assert _raw_patchify([ok], out=0x100008) == vp.VP_ERR_ARG
+    assert _raw_patchify([ok], cap=rows - 1) == vp.VP_ERR_CAPACITY
+    assert _raw_patchify([ok], ws_bytes=0) == vp.VP_ERR_CAPACITY
+    assert _raw_patchify([ok], ws=0) == vp.VP_ERR_NULL
+    # the layout of vp_batch_layout holds for this entry too: t = ceil(n_idx / 2)
+    g, cu, rows3, _ = vp.vp_batch_layout([vp.Item((0x10000, 4, 64, 96), [0, 1, 2], 64, 96)])
+    assert g.tolist() == [[2, 4, 6]] and rows3 == 48
+
+
 def test_extreme_downscale_is_rejected_not_truncated():
     # a 40000-pixel-wide source to 32 columns: a horizontal window of ~5000
     # taps exceeds what the kernels stage; the call fails instead of clipping

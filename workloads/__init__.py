@@ -190,6 +190,17 @@ def config(k: int) -> Workload:
     raise ValueError(k)
 
 
+def patchify_config() -> Workload:
+    """The cached counterpart of configuration 4: the same 64 x 256 frames,
+    already sampled and resized to 256x448 (what an offline cache holds), to
+    be normalised and patchified only."""
+    items = [Item("video", 256, 256, 448, "gradnoise", 5000 + v, {"mode": "uniform", "n": 256},
+                  dims=(256, 448))
+             for v in range(64)]
+    return Workload("p4: 64 videos x 256 cached frames 256x448, normalise + patchify only, bf16",
+                    items, MEAN_C4, STD_C4, "bf16")
+
+
 # --------------------------------------------------------------------------
 # Frame generation
 # --------------------------------------------------------------------------
