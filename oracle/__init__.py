@@ -78,6 +78,9 @@ def lib() -> ctypes.CDLL:
         L.oracle_item_row.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64,
                                       f64p, f64p, i64, f64p]
         L.oracle_patchify_item.argtypes = [u8p, i64, i64, i64, i32p, i64, f64p, f64p, f64p]
+        L.oracle_fixed_weights.argtypes = [i64, i64, i64, i64p, i64p, i32p, i64]
+        L.oracle_resize_u8.argtypes = [u8p, i64, i64, i64, i64, u8p]
+        L.oracle_resize_u8_item.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64, u8p]
         L.oracle_layout.argtypes = [i64, i64p, i64p, i64p, i64p, i64p]
         _lib = L
     return _lib
@@ -200,6 +203,36 @@ def patchify_item(frames: np.ndarray, indices, mean, std) -> np.ndarray:
                                       len(idx), _p(m, ctypes.c_double), _p(s, ctypes.c_double),
                                       _p(rows, ctypes.c_double)), "patchify_item")
     return rows
+
+
+def fixed_weights(n_in: int, n_out: int, i: int) -> tuple[int, np.ndarray]:
+    """(window start, int32 weights in units of 2^-22) of output i."""
+    lo, n = ctypes.c_int64(), ctypes.c_int64()
+    q = np.zeros(4096, np.int32)
+    _check(lib().oracle_fixed_weights(n_in, n_out, i, ctypes.byref(lo), ctypes.byref(n),
+                                      _p(q, ctypes.c_int32), 4096), "fixed_weights")
+    return lo.value, q[:n.value].copy()
+
+
+def resize_u8(frame: np.ndarray, h: int, w: int) -> np.ndarray:
+    """Fixed-point resample of one uint8 [H][W][3] frame to uint8 [h][w][3]."""
+    f = np.ascontiguousarray(frame, dtype=np.uint8)
+    H, W, _ = f.shape
+    out = np.zeros((h, w, 3), np.uint8)
+    _check(lib().oracle_resize_u8(_p(f, ctypes.c_uint8), H, W, h, w, _p(out, ctypes.c_uint8)),
+           "resize_u8")
+    return out
+
+
+def resize_u8_item(frames: np.ndarray, indices, h: int, w: int) -> np.ndarray:
+    """The cache writer for one item: uint8 [n_idx][h][w][3]."""
+    f = np.ascontiguousarray(frames, dtype=np.uint8)
+    n_src, H, W, _ = f.shape
+    idx = np.ascontiguousarray(indices, dtype=np.int32)
+    out = np.zeros((len(idx), h, w, 3), np.uint8)
+    _check(lib().oracle_resize_u8_item(_p(f, ctypes.c_uint8), n_src, H, W, _p(idx, ctypes.c_int32),
+                                       len(idx), h, w, _p(out, ctypes.c_uint8)), "resize_u8_item")
+    return out
 
 
 def item_row(frames: np.ndarray, indices, h: int, w: int, mean, std, rho: int) -> np.ndarray:

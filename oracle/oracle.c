@@ -388,6 +388,117 @@ double oracle_resize_pixel(const uint8_t *frame, int64_t H, int64_t W, int64_t h
 }
 
 /* ------------------------------------------------------------------------ */
+/* uint8 cache writer: fixed-point resampling                               */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The cache of Section 3.1.1 stores frames that are already sampled and
+ * resized; kept as uint8 they are a quarter of the float tensors.  This
+ * variant resamples in integers so that its bytes are reproducible exactly
+ * on any machine:
+ *   q_j = w_j * 2^22 rounded half away from zero   (w_j: the weights above),
+ *   each pass:  out = clamp(floor((sum_j q_j * in_j + 2^21) / 2^22), 0, 255),
+ * i.e. a round half up of the exact fixed-point sum, then a clamp to a byte.
+ * The horizontal pass runs first, over every source row, into a uint8
+ * frame of H x w; the vertical pass reads that.  An axis whose size does
+ * not change is the identity (one weight of exactly 2^22).
+ * Reading: these are the conventions of PIL-style integer resizers for
+ * 8-bit images (22 fractional bits, horizontal pass first, a byte between
+ * the passes); the CPU tests pin the result to Pillow's bicubic resize.
+ */
+int oracle_fixed_weights(int64_t n_in, int64_t n_out, int64_t i, int64_t *lo, int64_t *count,
+                         int32_t *q, int64_t cap)
+{
+    if (q == NULL)
+        return OR_ERR_NULL;
+    double w[4096];
+    if (cap > 4096)
+        cap = 4096;
+    int st = oracle_filter(n_in, n_out, i, lo, count, w, cap);
+    if (st != OR_OK)
+        return st;
+    for (int64_t k = 0; k < *count; k++) {
+        double x = w[k] * 4194304.0;   /* 2^22 */
+        q[k] = (int32_t)(x < 0.0 ? x - 0.5 : x + 0.5);   /* truncation: half away from zero */
+    }
+    return OR_OK;
+}
+
+static int check_item(int64_t n_src, int64_t H, int64_t W, const int32_t *indices,
+                      int64_t n_idx, int64_t h, int64_t w);
+
+static uint8_t fixed_to_byte(int64_t acc)
+{
+    int64_t v = acc + 2097152;   /* + 2^21: round half up */
+    if (v < 0)
+        return 0;
+    v >>= 22;                    /* floor of a non-negative value */
+    return (uint8_t)(v > 255 ? 255 : v);
+}
+
+/* One frame F[H][W][3] -> out[h][w][3], both uint8, as defined above. */
+int oracle_resize_u8(const uint8_t *frame, int64_t H, int64_t W, int64_t h, int64_t w,
+                     uint8_t *out)
+{
+    if (frame == NULL || out == NULL)
+        return OR_ERR_NULL;
+    if (H < 1 || W < 1 || h < 1 || w < 1)
+        return OR_ERR_DIMS;
+    uint8_t *mid = malloc((size_t)(H * w * 3));
+    int32_t *q = malloc(sizeof(int32_t) * 4096);
+    if (!mid || !q) {
+        free(mid);
+        free(q);
+        return OR_ERR_NOMEM;
+    }
+    int st = OR_OK;
+    /* horizontal pass: every source row */
+    for (int64_t j = 0; j < w && st == OR_OK; j++) {
+        int64_t lo, n;
+        st = oracle_fixed_weights(W, w, j, &lo, &n, q, 4096);
+        for (int64_t y = 0; y < H && st == OR_OK; y++)
+            for (int64_t c = 0; c < 3; c++) {
+                int64_t acc = 0;
+                for (int64_t k = 0; k < n; k++)
+                    acc += (int64_t)q[k] * frame[(y * W + lo + k) * 3 + c];
+                mid[(y * w + j) * 3 + c] = fixed_to_byte(acc);
+            }
+    }
+    /* vertical pass */
+    for (int64_t i = 0; i < h && st == OR_OK; i++) {
+        int64_t lo, n;
+        st = oracle_fixed_weights(H, h, i, &lo, &n, q, 4096);
+        for (int64_t j = 0; j < w && st == OR_OK; j++)
+            for (int64_t c = 0; c < 3; c++) {
+                int64_t acc = 0;
+                for (int64_t k = 0; k < n; k++)
+                    acc += (int64_t)q[k] * mid[((lo + k) * w + j) * 3 + c];
+                out[(i * w + j) * 3 + c] = fixed_to_byte(acc);
+            }
+    }
+    free(mid);
+    free(q);
+    return st;
+}
+
+/*
+ * Whole item for the cache: frames[n_src][H][W][3] sampled at `indices` (in
+ * that order, no temporal padding) and resized to out[n_idx][h][w][3].
+ */
+int oracle_resize_u8_item(const uint8_t *frames, int64_t n_src, int64_t H, int64_t W,
+                          const int32_t *indices, int64_t n_idx, int64_t h, int64_t w,
+                          uint8_t *out)
+{
+    if (frames == NULL || out == NULL)
+        return OR_ERR_NULL;
+    int st = check_item(n_src, H, W, indices, n_idx, h, w);
+    for (int64_t k = 0; k < n_idx && st == OR_OK; k++)
+        st = oracle_resize_u8(frames + (int64_t)indices[k] * H * W * 3, H, W, h, w,
+                              out + k * h * w * 3);
+    return st;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Rescale + normalise, temporal padding, patchify                          */
 /* ------------------------------------------------------------------------ */
 

@@ -548,3 +548,80 @@ def test_patchify_only_errors():
     with pytest.raises(oracle.OracleError) as e:
         oracle.patchify_item(f, [0, 2], (0.5,) * 3, (0.5,) * 3)
     assert e.value.code == oracle.ERR_INDEX
+
+
+# -- uint8 cache writer (fixed-point resampling) ----------------------------
+
+PIL_SHAPES = [
+    (64, 96, 32, 48), (240, 320, 128, 160), (40, 50, 64, 96), (100, 60, 64, 96),
+    (96, 128, 96, 128), (1, 1, 32, 32), (300, 20, 32, 32), (77, 131, 64, 96),
+    (720, 1280, 256, 448), (480, 854, 352, 640), (723, 740, 736, 736), (333, 257, 320, 256),
+]
+
+
+@pytest.mark.parametrize("H,W,h,w", PIL_SHAPES)
+def test_resize_u8_equals_pillow_bicubic(H, W, h, w):
+    """The fixed-point cache writer reproduces Pillow's BICUBIC resize of an
+    RGB image byte for byte (an independent implementation of the same
+    conventions), on noise and on a smooth ramp with clipping overshoot."""
+    PIL = pytest.importorskip("PIL.Image")
+    rng = np.random.default_rng(H * 7919 + W)
+    noise = rng.integers(0, 256, size=(H, W, 3), dtype=np.uint8)
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    ramp = np.stack([(xx * 255 // max(W - 1, 1)), (yy * 255 // max(H - 1, 1)),
+                     ((xx + yy) % 2) * 255], axis=-1).astype(np.uint8)
+    for img in (noise, ramp):
+        ref = np.asarray(PIL.fromarray(img, "RGB").resize((w, h), PIL.BICUBIC))
+        assert np.array_equal(oracle.resize_u8(img, h, w), ref)
+
+
+def test_fixed_weights_are_rounded_float_weights():
+    # exact 2x downscale interior: the dyadic weights scale to integers
+    lo, q = oracle.fixed_weights(320, 160, 40)
+    assert lo == 77
+    assert q.tolist() == [round(v * 2 ** 22) for v in
+                          [-0.01171875, -0.03515625, 0.11328125, 0.43359375,
+                           0.43359375, 0.11328125, -0.03515625, -0.01171875]]
+    # identity: one weight of exactly 2^22
+    lo, q = oracle.fixed_weights(96, 96, 10)
+    assert q.tolist() == [0, 1 << 22, 0, 0] and lo == 9
+    # every window: within half a unit of the float weight, sums near 2^22
+    for n_in, n_out in [(720, 256), (1280, 448), (40, 64), (1080, 448)]:
+        for i in range(0, n_out, 7):
+            lo, q = oracle.fixed_weights(n_in, n_out, i)
+            lo2, wf = oracle.filter_weights(n_in, n_out, i)
+            assert lo == lo2 and len(q) == len(wf)
+            assert np.all(np.abs(q - wf * 2 ** 22) <= 0.5)
+            assert abs(int(q.sum()) - (1 << 22)) <= len(q)
+
+
+def test_resize_u8_constant_identity_and_range():
+    f = np.full((50, 70, 3), 173, np.uint8)
+    assert np.all(oracle.resize_u8(f, 32, 64) == 173)
+    rng = np.random.default_rng(9)
+    g = rng.integers(0, 256, size=(64, 96, 3), dtype=np.uint8)
+    assert np.array_equal(oracle.resize_u8(g, 64, 96), g)
+    # where nothing clips (a smooth frame inside [16, 239]) the only
+    # difference from the real-valued resize is the rounding after each pass:
+    # at most one level from the rounded real value
+    yy, xx = np.meshgrid(np.arange(64), np.arange(96), indexing="ij")
+    smooth = np.stack([16 + (xx * 223) // 95, 16 + (yy * 223) // 63,
+                       16 + ((xx + 2 * yy) * 223) // 221], axis=-1).astype(np.uint8)
+    real = oracle.resize_frame(smooth, 32, 64)                 # [3][h][w]
+    ref = np.floor(real + 0.5).transpose(1, 2, 0)
+    assert np.abs(oracle.resize_u8(smooth, 32, 64).astype(int) - ref).max() <= 1
+
+
+def test_resize_u8_item_order_and_errors():
+    rng = np.random.default_rng(10)
+    f = rng.integers(0, 256, size=(4, 40, 60, 3), dtype=np.uint8)
+    out = oracle.resize_u8_item(f, [3, 0, 3], 32, 64)
+    assert out.shape == (3, 32, 64, 3)
+    for k, src in enumerate([3, 0, 3]):
+        assert np.array_equal(out[k], oracle.resize_u8(f[src], 32, 64))
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.resize_u8_item(f, [4], 32, 64)
+    assert e.value.code == oracle.ERR_INDEX
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.resize_u8_item(f, [0], 30, 64)
+    assert e.value.code == oracle.ERR_DIMS
