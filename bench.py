@@ -60,7 +60,7 @@ def counter_traffic(workload_tag: str, sha: str):
     return d.get("hbm_bytes_per_call")
 
 
-def cpu_baseline(wl, frames_dev, planned, patch_only=False, budget_s=12.0):
+def cpu_baseline(wl, frames_dev, planned, patch_only=False, resize_only=False, budget_s=12.0):
     """The oracle, item by item in workload order, until `budget_s` seconds of
     oracle time have been spent (or the workload is done).  Each item's frame
     pairs are copied to the host and spread over a thread pool (ctypes
@@ -83,7 +83,9 @@ def cpu_baseline(wl, frames_dev, planned, patch_only=False, budget_s=12.0):
                     for tt in range(len(padded) // 2)]
             del host
             t0 = time.perf_counter()
-            if patch_only:
+            if resize_only:
+                list(ex.map(lambda j: oracle.resize_u8_item(j[0], [0, 1], j[1], j[2]), jobs))
+            elif patch_only:
                 list(ex.map(lambda j: oracle.patchify_item(j[0], [0, 1], wl.mean, wl.std), jobs))
             else:
                 list(ex.map(lambda j: oracle.preprocess_item(j[0], [0, 1], j[1], j[2], wl.mean,
@@ -110,6 +112,8 @@ def main():
     ap.add_argument("--patchify", action="store_true",
                     help="time the normalise+patchify-only entry on the cached counterpart of "
                          "workload 4 (64 x 256 frames already at 256x448) instead")
+    ap.add_argument("--resize", action="store_true",
+                    help="time the uint8 cache writer (fixed-point resize only) on the workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run plain 1 GiB device-to-device copies (twice) before the steps, "
@@ -162,15 +166,20 @@ def main():
         return vitems, planned
 
     vitems, planned = plan_items()
-    grid, cu, rows, ws_bytes = vp.vp_batch_layout(vitems)
     code = vp.VP_OUT_BF16 if wl.out_dtype == "bf16" else vp.VP_OUT_F32
-    out = torch.empty((rows, vp.VP_ROW), dtype=torch.bfloat16 if code == vp.VP_OUT_BF16
-                      else torch.float32, device=dev)
-    work = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    if args.resize:
+        frame_off, ws_bytes = vp.vp_resize_layout(vitems)
+        rows = 0
+        out = torch.empty(int(frame_off[-1]), dtype=torch.uint8, device=dev)
+    else:
+        grid, cu, rows, ws_bytes = vp.vp_batch_layout(vitems)
+        out = torch.empty((rows, vp.VP_ROW), dtype=torch.bfloat16 if code == vp.VP_OUT_BF16
+                          else torch.float32, device=dev)
+    work = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     n_frames = sum(len(p[2]) for p in planned)
     in_bytes = sum(len(p[2]) * it.frame_bytes for p, it in zip(planned, wl.items))
-    out_bytes = rows * vp.VP_ROW * out.element_size()
+    out_bytes = out.numel() * out.element_size()
     alg_bytes = in_bytes + out_bytes
     log(f"{n_frames} frames, {rows} rows, algorithmic bytes {alg_bytes / 1e9:.3f} GB "
         f"(in {in_bytes / 1e9:.3f}, out {out_bytes / 1e9:.3f})")
@@ -187,7 +196,10 @@ def main():
 
     def step():
         items, _ = plan_items()
-        entry(items, wl.mean, wl.std, code, out, work, stream)
+        if args.resize:
+            vp.vp_resize_batch(items, out, work, stream)
+        else:
+            entry(items, wl.mean, wl.std, code, out, work, stream)
 
     for _ in range(args.warmup):
         step()
@@ -225,14 +237,14 @@ def main():
         f"({achieved / HBM_PEAK_GBPS:.1%} of 8 TB/s)")
     log("kernel ms per step: " + " ".join(f"{t:.3f}" for t in kern_ms))
 
-    tag = "p4" if args.patchify else f"c{args.workload}"
+    tag = "p4" if args.patchify else (f"r{args.workload}" if args.resize else f"c{args.workload}")
     sha = kernel_source_sha()
     traffic = counter_traffic(tag, sha)
 
     baseline = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        baseline = cpu_baseline(wl, frames, planned, patch_only=args.patchify)
+        baseline = cpu_baseline(wl, frames, planned, patch_only=args.patchify, resize_only=args.resize)
         log(f"cpu baseline {baseline}")
 
     rec = {
@@ -246,14 +258,14 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "i32" if args.resize else "f32",
         "data": "synthetic (seeded SplitMix64 frames resident in HBM)",
         "config": {
-            "workload": wl.name,
+            "workload": wl.name + ("; uint8 cache writer (fixed-point resize only)" if args.resize else ""),
             "items": len(wl.items),
             "frames": n_frames,
             "rows": rows,
-            "out_dtype": wl.out_dtype,
+            "out_dtype": "u8" if args.resize else wl.out_dtype,
             "mean": list(wl.mean),
             "std": list(wl.std),
             "algorithmic_bytes": alg_bytes,

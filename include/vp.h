@@ -133,6 +133,15 @@ int32_t vp_filter_table(int32_t n_in, int32_t n_out, int32_t taps,
                         int32_t* start, int32_t* count, float* weights);
 
 /*
+ * The same filter in the fixed point of vp_resize_batch: every double
+ * weight times 2^22, rounded half away from zero, as int32 (HOST
+ * q[n_out][taps], zero beyond count[i]); start and count as above.
+ * Errors: as vp_filter_table.
+ */
+int32_t vp_filter_table_fixed(int32_t n_in, int32_t n_out, int32_t taps,
+                              int32_t* start, int32_t* count, int32_t* q);
+
+/*
  * One video or image of a batch.  A video is n_src decoded frames; an image
  * is one frame (n_src = 1, n_idx = 1) that the temporal patch of 2 turns
  * into two identical frames (Section 3.2.2: images and videos share one
@@ -225,10 +234,50 @@ int32_t vp_patchify_batch(const vp_item* items, int32_t n_items, const float* me
                           void* workspace, int64_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Layout of a vp_resize_batch call.
+ * frame_off: HOST int64[n_items + 1]: item b's resized frames start at byte
+ *   frame_off[b] of the output; frame_off[0] = 0, frame_off[b+1] =
+ *   frame_off[b] + n_idx * dst_h * dst_w * 3; frame_off[n_items] is the total.
+ * workspace_bytes: HOST, the device workspace vp_resize_batch needs.
+ * Either pointer may be NULL.  Frame pointers are not dereferenced.
+ * Errors: as vp_batch_layout, plus VP_ERR_CAPACITY when a filter window is
+ * too long for the kernel's tiles.
+ */
+int32_t vp_resize_layout(const vp_item* items, int32_t n_items, int64_t* frame_off,
+                         int64_t* workspace_bytes);
+
+/*
+ * uint8 cache writer (Section 3.1.1: the offline cache holds frames that are
+ * already sampled and resized; as uint8 they take a quarter of the float
+ * tensors' space).  For every item, every sampled frame, in index order and
+ * without temporal padding, is resampled from (src_h, src_w) to
+ * (dst_h, dst_w) in fixed point, so that the bytes are reproducible exactly:
+ *   weights q_j = the weights of vp_filter_table computed in double and
+ *   scaled by 2^22, rounded half away from zero;
+ *   a horizontal pass over every source row, then a vertical pass, each
+ *   giving clamp(floor((sum_j q_j * v_j + 2^21) / 2^22), 0, 255).
+ * These are the conventions of PIL-style integer resizers for 8-bit images.
+ * Item b's frames go to out_frames + frame_off[b] as uint8
+ * [n_idx][dst_h][dst_w][3] (see vp_resize_layout).
+ * out_frames: DEVICE, >= frame_off[n_items] bytes (out_capacity), 4-byte
+ *   aligned.
+ * frame_off: HOST output as in vp_resize_layout (may be NULL).
+ * workspace, stream, ownership and asynchrony as for vp_preprocess_batch,
+ *   with the workspace_bytes of vp_resize_layout.
+ * Errors: VP_ERR_NULL, VP_ERR_ARG (n_items < 1, misaligned pointers),
+ * VP_ERR_DIMS, VP_ERR_FRAMES, VP_ERR_INDEX, VP_ERR_CAPACITY (output or
+ * workspace too small, a filter window too long for the kernel's tiles),
+ * VP_ERR_HIP.
+ */
+int32_t vp_resize_batch(const vp_item* items, int32_t n_items, void* out_frames,
+                        int64_t out_capacity, int64_t* frame_off, void* workspace,
+                        int64_t workspace_bytes, hipStream_t stream);
+
+/*
  * Kernel timing hook (measurement only; not a step of the method).  The next
- * vp_preprocess_batch or vp_patchify_batch call made on this thread records
- * `start` on its stream
- * immediately before its first kernel launch (after the plan upload) and
+ * vp_preprocess_batch, vp_patchify_batch or vp_resize_batch call made on this
+ * thread records `start` on its stream immediately before its first kernel
+ * launch (after the plan upload) and
  * `stop` immediately after its last launch, then forgets both events, so
  * that hipEventElapsedTime(start, stop) is the device time of that call's
  * kernels alone.  A call that fails before launching records neither.

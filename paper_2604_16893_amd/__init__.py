@@ -31,8 +31,9 @@ VP_ROW = 1536
 VP_FACTOR = 32
 
 EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
-            "vp_batch_layout", "vp_preprocess_batch", "vp_patchify_batch", "vp_status_string",
-            "vp_last_error_message", "vp_set_kernel_events")
+            "vp_filter_table_fixed", "vp_batch_layout", "vp_preprocess_batch", "vp_patchify_batch",
+            "vp_resize_layout", "vp_resize_batch", "vp_status_string", "vp_last_error_message",
+            "vp_set_kernel_events")
 
 
 class VPError(RuntimeError):
@@ -74,6 +75,10 @@ def lib() -> ctypes.CDLL:
         L.vp_preprocess_batch.argtypes = [itemp, i32, f32p, f32p, i32, ctypes.c_void_p, i64,
                                           i32p, i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
         L.vp_patchify_batch.argtypes = L.vp_preprocess_batch.argtypes
+        L.vp_filter_table_fixed.argtypes = [i32, i32, i32, i32p, i32p, i32p]
+        L.vp_resize_layout.argtypes = [itemp, i32, i64p, i64p]
+        L.vp_resize_batch.argtypes = [itemp, i32, ctypes.c_void_p, i64, i64p, ctypes.c_void_p, i64,
+                                      ctypes.c_void_p]
         L.vp_set_kernel_events.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         L.vp_status_string.argtypes = [i32]
         L.vp_status_string.restype = ctypes.c_char_p
@@ -140,6 +145,20 @@ def vp_filter_table(n_in: int, n_out: int, taps: Optional[int] = None):
                                  _ptr(count, ctypes.c_int32), _ptr(w, ctypes.c_float)),
            "vp_filter_table")
     return start, count, w
+
+
+def vp_filter_table_fixed(n_in: int, n_out: int, taps: Optional[int] = None):
+    """(start int32 [n_out], count int32 [n_out], q int32 [n_out, taps]): the
+    filter's weights in units of 2^-22, as the uint8 writer uses them."""
+    if taps is None:
+        taps = vp_filter_taps(n_in, n_out)
+    start = np.zeros(n_out, np.int32)
+    count = np.zeros(n_out, np.int32)
+    q = np.zeros((n_out, taps), np.int32)
+    _check(lib().vp_filter_table_fixed(n_in, n_out, taps, _ptr(start, ctypes.c_int32),
+                                       _ptr(count, ctypes.c_int32), _ptr(q, ctypes.c_int32)),
+           "vp_filter_table_fixed")
+    return start, count, q
 
 
 # --------------------------------------------------------------------------
@@ -274,6 +293,49 @@ def patchify(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None):
     work = torch.empty(ws, dtype=torch.uint8, device=dev)
     vp_patchify_batch(items, mean, std, code, out, work, stream)
     return out, grid, cu
+
+
+def vp_resize_layout(items: Sequence):
+    """(frame_off int64 [B+1] output byte offsets, workspace_bytes) of the uint8 writer."""
+    b = _Batch(items)
+    off = np.zeros(len(b) + 1, np.int64)
+    ws = ctypes.c_int64()
+    _check(lib().vp_resize_layout(b.arr, len(b), _ptr(off, ctypes.c_int64), ctypes.byref(ws)),
+           "vp_resize_layout")
+    return off, ws.value
+
+
+def vp_resize_batch(items: Sequence, out_frames, workspace, stream=None):
+    """Enqueue the uint8 writer: out_frames is a contiguous CUDA uint8 tensor
+    of at least frame_off[-1] bytes; item b's frames [n_idx, dst_h, dst_w, 3]
+    start at byte frame_off[b].  Returns frame_off."""
+    import torch
+    if out_frames.dtype != torch.uint8 or not out_frames.is_contiguous() or not out_frames.is_cuda:
+        raise VPError(VP_ERR_ARG, "out_frames must be a contiguous CUDA uint8 tensor")
+    if not workspace.is_cuda or not workspace.is_contiguous():
+        raise VPError(VP_ERR_ARG, "workspace must be a contiguous CUDA tensor")
+    b = _Batch(items)
+    off = np.zeros(len(b) + 1, np.int64)
+    _check(lib().vp_resize_batch(b.arr, len(b), ctypes.c_void_p(out_frames.data_ptr()),
+                                 out_frames.numel(), _ptr(off, ctypes.c_int64),
+                                 ctypes.c_void_p(workspace.data_ptr()),
+                                 workspace.numel() * workspace.element_size(),
+                                 ctypes.c_void_p(_stream_handle(stream))), "vp_resize_batch")
+    return off
+
+
+def resize_u8(items: Sequence, stream=None):
+    """Allocate with torch and run the uint8 writer.  Returns a list of
+    uint8 tensors [n_idx, dst_h, dst_w, 3] (views of one buffer), final when
+    the stream is."""
+    import torch
+    off, ws = vp_resize_layout(items)
+    dev = items[0].frames.device
+    out = torch.empty(int(off[-1]), dtype=torch.uint8, device=dev)
+    work = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
+    vp_resize_batch(items, out, work, stream)
+    return [out[int(off[k]):int(off[k + 1])].view(len(it.indices), it.dst_h, it.dst_w, 3)
+            for k, it in enumerate(items)]
 
 
 def preprocess(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None):

@@ -62,14 +62,19 @@ int32_t spread_index(int64_t i, int64_t last, int64_t n) {
 struct AxisFilter {
     int32_t n_in = 0, n_out = 0, taps = 0;
     std::vector<int32_t> start, count;
-    std::vector<float> weight;  // [n_out][taps]
+    std::vector<float> weight;   // [n_out][taps]
+    std::vector<int32_t> fixed;  // [n_out][taps]: the double weights times 2^22, rounded
 };
 
-double cubic_a_half(double x) {  // Keys (1981) kernel, a = -1/2
+// Keys (1981) kernel, a = -1/2, evaluated as the polynomial is written
+// (left to right, no reassociation): the fixed-point weights of the uint8
+// writer are rounded from these doubles, so every machine must get the same
+// bits.
+double cubic_a_half(double x) {
     const double t = std::fabs(x);
-    if (t >= 2.0) return 0.0;
-    if (t >= 1.0) return ((-0.5 * t + 2.5) * t - 4.0) * t + 2.0;
-    return (1.5 * t - 2.5) * t * t + 1.0;
+    if (t < 1.0) return 1.5 * t * t * t - 2.5 * t * t + 1.0;
+    if (t < 2.0) return -0.5 * t * t * t + 2.5 * t * t - 4.0 * t + 2.0;
+    return 0.0;
 }
 
 // Window [lo, hi) of output i; the same double expressions as the documented
@@ -108,6 +113,7 @@ void build_axis(int32_t n_in, int32_t n_out, int32_t taps, AxisFilter* f) {
     f->start.assign(n_out, 0);
     f->count.assign(n_out, 0);
     f->weight.assign(static_cast<size_t>(n_out) * taps, 0.0f);
+    f->fixed.assign(static_cast<size_t>(n_out) * taps, 0);
     std::vector<double> raw(taps);
     for (int32_t i = 0; i < n_out; ++i) {
         double c, s;
@@ -120,8 +126,13 @@ void build_axis(int32_t n_in, int32_t n_out, int32_t taps, AxisFilter* f) {
         }
         f->start[i] = lo;
         f->count[i] = hi - lo;
-        for (int32_t j = lo; j < hi; ++j)
-            f->weight[static_cast<size_t>(i) * taps + (j - lo)] = static_cast<float>(raw[j - lo] / sum);
+        for (int32_t j = lo; j < hi; ++j) {
+            const double w = raw[j - lo] / sum;
+            f->weight[static_cast<size_t>(i) * taps + (j - lo)] = static_cast<float>(w);
+            const double x = w * 4194304.0;   // 2^22
+            f->fixed[static_cast<size_t>(i) * taps + (j - lo)] =
+                static_cast<int32_t>(x < 0.0 ? x - 0.5 : x + 0.5);   // half away from zero
+        }
     }
 }
 
@@ -145,6 +156,7 @@ struct Plan {
     std::vector<int32_t> grid;  // [n][3]
     std::vector<int32_t> cu;    // [n + 1]
     int64_t total_rows = 0;
+    std::vector<int64_t> byte_off;   // uint8 writer: [n + 1] output byte offsets of the items
     int64_t generic_cost = 0;   // source pixels the general kernel reads, roughly
     size_t off_items = 0, off_prefix = 0, off_indices = 0, off_tables = 0, off_units = 0, off_wgs = 0,
            bytes = 0;
@@ -323,7 +335,8 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShap
 // cleared when it reaches kTableCacheMax entries.
 struct AxisEntry {
     AxisFilter f;
-    std::vector<int32_t> words;   // the window table: start, count, weight
+    std::vector<int32_t> words;         // the window table: start, count, weight
+    std::vector<int32_t> fixed_words;   // the same with the fixed-point weights
 };
 struct SlotEntry {
     int32_t m = -1;               // slots, or -1 if the axis needs too many
@@ -362,6 +375,10 @@ std::shared_ptr<const AxisEntry> make_axis_entry(int32_t n_in, int32_t n_out) {
     const size_t wbase = e->words.size();
     e->words.resize(wbase + f.weight.size());
     std::memcpy(e->words.data() + wbase, f.weight.data(), f.weight.size() * sizeof(float));
+    e->fixed_words.reserve(e->words.size());
+    e->fixed_words.insert(e->fixed_words.end(), f.start.begin(), f.start.end());
+    e->fixed_words.insert(e->fixed_words.end(), f.count.begin(), f.count.end());
+    e->fixed_words.insert(e->fixed_words.end(), f.fixed.begin(), f.fixed.end());
     return e;
 }
 
@@ -667,6 +684,110 @@ int32_t build_patch_plan(const vp_item* items, int32_t n, Plan* p) {
     p->off_units = p->off_tables;
     p->off_wgs = p->off_tables;
     p->bytes = p->off_tables;
+    return VP_OK;
+}
+
+// Output tile of the uint8 writer for an item: the largest rows x columns
+// (rows from 32 down, then columns from 64 down) whose horizontal-pass rows,
+// staged source span and weights fit the kernel's LDS budgets.
+bool resize_tiles(const AxisFilter& fy, const AxisFilter& fx, int32_t* rb, int32_t* cb) {
+    static const int32_t kRows[] = {32, 16, 8, 4, 2, 1};
+    static const int32_t kCols[] = {64, 32, 16, 8};
+    for (int32_t r : kRows) {
+        if (int64_t(r) * fy.taps > vp::kRsQ) continue;
+        int64_t rows = 0;   // source rows the tile's horizontal pass produces
+        for (int32_t i0 = 0; i0 < fy.n_out; i0 += r) {
+            const int32_t i1 = std::min(i0 + r, fy.n_out) - 1;
+            rows = std::max<int64_t>(rows, fy.start[i1] + fy.count[i1] - fy.start[i0]);
+        }
+        for (int32_t c : kCols) {
+            if (int64_t(c) * fx.taps > vp::kRsQ) continue;
+            int64_t span = 0;   // source pixels the tile's columns read
+            for (int32_t j0 = 0; j0 < fx.n_out; j0 += c) {
+                const int32_t j1 = std::min(j0 + c, fx.n_out) - 1;
+                span = std::max<int64_t>(span, fx.start[j1] + fx.count[j1] - fx.start[j0]);
+            }
+            if (rows * c * 3 <= vp::kRsMid && span * 3 + 6 <= vp::kRsSrcRow) {
+                *rb = r;
+                *cb = c;
+                return true;
+            }
+        }
+    }
+    return false;
+}
+
+// Plan of vp_resize_batch: per item its frames in index order (no padding),
+// fixed-point tables, the output tile, and its output byte offset.
+int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
+    if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
+    if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    p->items.assign(n, vp::DevItem{});
+    p->prefix.assign(n + 1, 0);
+    p->byte_off.assign(n + 1, 0);
+    p->grid.clear();
+    p->cu.clear();
+    p->indices.clear();
+    p->tables.clear();
+    p->table_words = 0;
+    p->units.clear();
+    p->wgs.clear();
+    p->launches.clear();
+    p->generic_cost = 0;
+    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, std::shared_ptr<const AxisEntry>>> axes;
+    auto table_for = [&](int32_t n_in, int32_t n_out, int32_t* off) -> const AxisFilter* {
+        const auto key = std::make_pair(n_in, n_out);
+        auto found = axes.find(key);
+        if (found == axes.end()) {
+            auto e = cached(g_axis_cache, key, [&] { return make_axis_entry(n_in, n_out); });
+            const int32_t o = static_cast<int32_t>(p->table_words);
+            p->table_words += e->fixed_words.size();
+            p->tables.emplace_back(o, std::shared_ptr<const std::vector<int32_t>>(e, &e->fixed_words));
+            found = axes.emplace(key, std::make_pair(o, e)).first;
+        }
+        *off = found->second.first;
+        return &found->second.second->f;
+    };
+    int64_t bytes = 0, tiles = 0;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp_item& it = items[b];
+        int32_t st = validate_item(it, b);
+        if (st != VP_OK) return st;
+        vp::DevItem& d = p->items[b];
+        d.frames = it.frames;
+        d.frame_bytes = int64_t(it.src_h) * it.src_w * 3;
+        d.H = it.src_h;
+        d.W = it.src_w;
+        d.h = it.dst_h;
+        d.w = it.dst_w;
+        d.t = it.n_idx;
+        d.idx_off = static_cast<int32_t>(p->indices.size());
+        p->indices.insert(p->indices.end(), it.indices, it.indices + it.n_idx);
+        const AxisFilter* fy = table_for(it.src_h, it.dst_h, &d.ty_off);
+        const AxisFilter* fx = table_for(it.src_w, it.dst_w, &d.tx_off);
+        d.ky = fy->taps;
+        d.kx = fx->taps;
+        if (!resize_tiles(*fy, *fx, &d.rh, &d.cw))
+            return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
+                                             ": filter window too long for the uint8 writer's tiles");
+        d.hm = (it.dst_h + d.rh - 1) / d.rh;
+        d.wm = (it.dst_w + d.cw - 1) / d.cw;
+        d.route = vp::kRouteResize;
+        d.row_off = bytes;   // output byte offset of the item
+        bytes += int64_t(it.n_idx) * it.dst_h * it.dst_w * 3;
+        tiles += int64_t(it.n_idx) * d.hm * d.wm;
+        if (tiles > INT32_MAX) return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 tiles");
+        p->byte_off[b + 1] = bytes;
+        p->prefix[b + 1] = static_cast<int32_t>(tiles);
+    }
+    p->total_rows = 0;
+    p->off_items = 0;
+    p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
+    p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
+    p->off_tables = align_up(p->off_indices + sizeof(int32_t) * p->indices.size());
+    p->off_units = align_up(p->off_tables + sizeof(int32_t) * p->table_words);
+    p->off_wgs = p->off_units;
+    p->bytes = p->off_units;
     return VP_OK;
 }
 
@@ -1025,6 +1146,21 @@ int32_t vp_filter_table(int32_t n_in, int32_t n_out, int32_t taps, int32_t* star
     return VP_OK;
 }
 
+int32_t vp_filter_table_fixed(int32_t n_in, int32_t n_out, int32_t taps, int32_t* start,
+                              int32_t* count, int32_t* q) {
+    if (start == nullptr || count == nullptr || q == nullptr)
+        return fail(VP_ERR_NULL, "output pointer is NULL");
+    if (n_in < 1 || n_out < 1) return fail(VP_ERR_ARG, "n_in and n_out must be >= 1");
+    const int32_t need = axis_taps(n_in, n_out);
+    if (taps < need) return fail(VP_ERR_CAPACITY, "taps below the longest window");
+    AxisFilter f;
+    build_axis(n_in, n_out, taps, &f);
+    std::memcpy(start, f.start.data(), sizeof(int32_t) * n_out);
+    std::memcpy(count, f.count.data(), sizeof(int32_t) * n_out);
+    std::memcpy(q, f.fixed.data(), sizeof(int32_t) * f.fixed.size());
+    return VP_OK;
+}
+
 int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw,
                         int32_t* cu_seqlens, int64_t* total_rows, int64_t* workspace_bytes) {
     Plan p;
@@ -1052,6 +1188,64 @@ int32_t vp_patchify_batch(const vp_item* items, int32_t n_items, const float* me
     return run_batch(true, items, n_items, mean, std, out_dtype, out_rows, out_rows_capacity,
                      grid_thw, cu_seqlens, workspace, workspace_bytes, stream);
 }
+int32_t vp_resize_layout(const vp_item* items, int32_t n_items, int64_t* frame_off,
+                         int64_t* workspace_bytes) {
+    Plan p;
+    const int32_t st = build_resize_plan(items, n_items, &p);
+    if (st != VP_OK) return st;
+    if (frame_off) std::memcpy(frame_off, p.byte_off.data(), sizeof(int64_t) * p.byte_off.size());
+    if (workspace_bytes) *workspace_bytes = static_cast<int64_t>(p.bytes);
+    g_last_error.clear();
+    return VP_OK;
+}
+
+int32_t vp_resize_batch(const vp_item* items, int32_t n_items, void* out_frames,
+                        int64_t out_capacity, int64_t* frame_off, void* workspace,
+                        int64_t workspace_bytes, hipStream_t stream) {
+    if (out_frames == nullptr || workspace == nullptr)
+        return fail(VP_ERR_NULL, "out_frames and workspace must be non-NULL");
+    if (reinterpret_cast<uintptr_t>(out_frames) % 4 != 0)
+        return fail(VP_ERR_ARG, "out_frames must be 4-byte aligned");
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+        return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
+    Plan p;
+    int32_t st = build_resize_plan(items, n_items, &p);
+    if (st != VP_OK) return st;
+    if (out_capacity < p.byte_off[n_items])
+        return fail(VP_ERR_CAPACITY, "out_frames holds " + std::to_string(out_capacity) +
+                                         " bytes, batch needs " + std::to_string(p.byte_off[n_items]));
+    if (workspace_bytes < static_cast<int64_t>(p.bytes))
+        return fail(VP_ERR_CAPACITY, "workspace holds " + std::to_string(workspace_bytes) +
+                                         " bytes, plan needs " + std::to_string(p.bytes));
+    st = upload_plan(p, workspace, stream);
+    if (st != VP_OK) return st;
+    hipEvent_t t_start = g_timing_start, t_stop = g_timing_stop;
+    g_timing_start = g_timing_stop = nullptr;
+    if (t_start != nullptr) {
+        const hipError_t e = hipEventRecord(t_start, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing start)");
+    }
+    auto* ws = static_cast<uint8_t*>(workspace);
+    vp::PlanView view{};
+    view.items = reinterpret_cast<const vp::DevItem*>(ws + p.off_items);
+    view.tile_prefix = reinterpret_cast<const int32_t*>(ws + p.off_prefix);
+    view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
+    view.tables = reinterpret_cast<const int32_t*>(ws + p.off_tables);
+    view.units = nullptr;
+    view.wgs = nullptr;
+    view.n_items = n_items;
+    view.n_tiles = p.prefix[n_items];
+    const int err = vp::launch_resize(view, out_frames, stream);
+    if (err != 0) return hip_fail(static_cast<hipError_t>(err), "uint8 writer launch");
+    if (t_stop != nullptr) {
+        const hipError_t e = hipEventRecord(t_stop, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");
+    }
+    if (frame_off) std::memcpy(frame_off, p.byte_off.data(), sizeof(int64_t) * p.byte_off.size());
+    g_last_error.clear();
+    return VP_OK;
+}
+
 const char* vp_status_string(int32_t status) {
     switch (status) {
         case VP_OK: return "VP_OK";

@@ -165,6 +165,131 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
 }
 
 // ===========================================================================
+// uint8 cache writer (fixed-point resampling)
+// ===========================================================================
+
+// round half up of a sum in units of 2^-22, clamped to a byte
+__device__ __forceinline__ uint32_t fixed_to_byte(int32_t acc) {
+    const int32_t v = acc + (1 << 21);
+    return v < 0 ? 0u : min(static_cast<uint32_t>(v) >> 22, 255u);
+}
+
+// One workgroup per tile of up to 32 output rows x 64 output columns of one
+// sampled frame.  The horizontal pass runs first (the fixed-point
+// convention): the source rows the tile's vertical windows need are staged
+// four at a time in LDS as bytes, and each thread (row, column) forms the
+// three channels of one horizontally resampled pixel, rounded and clamped to
+// a byte, into the tile's LDS rows.  The vertical pass then forms each output
+// byte from those and stores them four at a time.  Sums are exact in int32:
+// |q| < 2^23, bytes < 2^8, and the weights of a window sum to about 2^22.
+__global__ __launch_bounds__(kRsThreads) void resize_u8_kernel(PlanView plan, uint8_t* out) {
+    __shared__ __align__(16) uint32_t src32[kRsChunk][kRsSrcRow / 4];
+    __shared__ __align__(16) uint8_t mid[kRsMid];
+    __shared__ int32_t qx[kRsQ], qy[kRsQ];
+    __shared__ int32_t col_off[kRsColsMax], col_n[kRsColsMax], row_off[kRsRowsMax], row_n[kRsRowsMax];
+
+    const int tile = blockIdx.x;
+    const int b = find_item(plan.tile_prefix, plan.n_items, tile);
+    const DevItem it = plan.items[b];
+    const int local = tile - plan.tile_prefix[b];
+    const int tx = local % it.wm;
+    const int q2 = local / it.wm;
+    const int ty = q2 % it.hm;
+    const int k = q2 / it.hm;
+    const int RB = it.rh, CB = it.cw;
+    const int i0 = ty * RB, j0 = tx * CB;
+    const int nr = min(RB, it.h - i0), nc = min(CB, it.w - j0);
+    const int32_t* ys = plan.tables + it.ty_off;
+    const int32_t* yn = ys + it.h;
+    const int32_t* yq = yn + it.h;
+    const int32_t* xs = plan.tables + it.tx_off;
+    const int32_t* xn = xs + it.w;
+    const int32_t* xq = xn + it.w;
+    // window ends never decrease, so the tile reads [ylo, yhi) x [xlo, xhi)
+    const int ylo = ys[i0], yhi = ys[i0 + nr - 1] + yn[i0 + nr - 1];
+    const int xlo = xs[j0], xhi = xs[j0 + nc - 1] + xn[j0 + nc - 1];
+    const int tid = threadIdx.x;
+    for (int e = tid; e < nc * it.kx; e += kRsThreads)
+        qx[e] = xq[int64_t(j0 + e / it.kx) * it.kx + e % it.kx];
+    for (int e = tid; e < nr * it.ky; e += kRsThreads)
+        qy[e] = yq[int64_t(i0 + e / it.ky) * it.ky + e % it.ky];
+    if (tid < nc) {
+        col_off[tid] = 3 * (xs[j0 + tid] - xlo);
+        col_n[tid] = xn[j0 + tid];
+    }
+    if (tid < nr) {
+        row_off[tid] = ys[i0 + tid] - ylo;
+        row_n[tid] = yn[i0 + tid];
+    }
+
+    // the frame through a buffer resource (range: the frame in whole dwords,
+    // so a dword that runs past its end reads zeros)
+    const int f = plan.indices[it.idx_off + k];
+    const uintptr_t fa = reinterpret_cast<uintptr_t>(it.frames + int64_t(f) * it.frame_bytes);
+    const uint32_t lead = static_cast<uint32_t>(fa & 3u);
+    const uint32_t range = static_cast<uint32_t>((it.frame_bytes + lead + 3) & ~int64_t(3));
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(fa - lead), (short)0, static_cast<int>(range), 0x00020000);
+    const uint32_t row_bytes = static_cast<uint32_t>(it.W) * 3u;
+    const int span = (xhi - xlo) * 3;
+    __syncthreads();
+
+    const int r = tid >> 6, jj = tid & 63;
+    for (int y0 = ylo; y0 < yhi; y0 += kRsChunk) {
+        for (int e = tid; e < kRsChunk * (kRsSrcRow / 4); e += kRsThreads) {
+            const int rr = e / (kRsSrcRow / 4), d = e % (kRsSrcRow / 4);
+            const int y = y0 + rr;
+            const uint32_t o = lead + static_cast<uint32_t>(y) * row_bytes + 3u * static_cast<uint32_t>(xlo);
+            const int ndw = (span + static_cast<int>(o & 3u) + 3) >> 2;
+            if (y < yhi && d < ndw)
+                src32[rr][d] = static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (o & ~3u) + 4u * d, 0, 0));
+        }
+        __syncthreads();
+        const int y = y0 + r;
+        if (y < yhi && jj < nc) {
+            const uint32_t o = lead + static_cast<uint32_t>(y) * row_bytes + 3u * static_cast<uint32_t>(xlo);
+            const uint8_t* px = reinterpret_cast<const uint8_t*>(src32[r]) + (o & 3u) + col_off[jj];
+            const int32_t* q = qx + jj * it.kx;
+            const int n = col_n[jj];
+            int32_t a0 = 0, a1 = 0, a2 = 0;
+            for (int t = 0; t < n; ++t) {
+                const int32_t w = q[t];
+                a0 += __mul24(w, static_cast<int32_t>(px[3 * t]));
+                a1 += __mul24(w, static_cast<int32_t>(px[3 * t + 1]));
+                a2 += __mul24(w, static_cast<int32_t>(px[3 * t + 2]));
+            }
+            uint8_t* m = mid + ((y - ylo) * CB + jj) * 3;
+            m[0] = static_cast<uint8_t>(fixed_to_byte(a0));
+            m[1] = static_cast<uint8_t>(fixed_to_byte(a1));
+            m[2] = static_cast<uint8_t>(fixed_to_byte(a2));
+        }
+        __syncthreads();
+    }
+
+    // vertical pass: four output bytes per step (the tile's row segments are
+    // nc * 3 bytes, a multiple of 24, and start on 4-byte boundaries)
+    const int words = nc * 3 / 4;
+    uint8_t* ob = out + it.row_off + (int64_t(k) * it.h + i0) * it.w * 3 + int64_t(j0) * 3;
+    for (int e = tid; e < nr * words; e += kRsThreads) {
+        const int ii = e / words, d = e % words;
+        const int32_t* q = qy + ii * it.ky;
+        const int n = row_n[ii];
+        const uint8_t* m0 = mid + row_off[ii] * CB * 3;
+        uint32_t word = 0;
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb) {
+            const int byte = 4 * d + bb;   // pixel byte / 3, channel byte % 3
+            const int col = byte / 3, c = byte - 3 * col;
+            const uint8_t* m = m0 + col * 3 + c;
+            int32_t acc = 0;
+            for (int t = 0; t < n; ++t) acc += __mul24(q[t], static_cast<int32_t>(m[t * CB * 3]));
+            word |= fixed_to_byte(acc) << (8 * bb);
+        }
+        *reinterpret_cast<uint32_t*>(ob + int64_t(ii) * it.w * 3 + 4 * d) = word;
+    }
+}
+
+// ===========================================================================
 // Normalise + patchify kernel (frames already at the target size)
 // ===========================================================================
 
@@ -616,6 +741,13 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 }
 
 }  // namespace
+
+int launch_resize(const PlanView& plan, void* out, hipStream_t stream) {
+    if (plan.n_tiles <= 0) return 0;
+    hipLaunchKernelGGL(resize_u8_kernel, dim3(plan.n_tiles), dim3(kRsThreads), 0, stream, plan,
+                       static_cast<uint8_t*>(out));
+    return static_cast<int>(hipGetLastError());
+}
 
 int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
                     hipStream_t stream) {

@@ -27,6 +27,8 @@
 //            window, or the close row of output row i - 1 if that is later;
 //            never decreasing, and several output rows may close on one row
 //            (an upscaled axis, the bottom border)
+//   fixed-point window table (uint8 writer): as the window table, with int32
+//       weights in units of 2^-22
 //   column table of an x axis (streaming kernel), KX taps, for output bands
 //   of `band` columns whose source pixels fit an LDS row of `row_px` pixels:
 //       int32 start[n_out]; float weight[n_out][KX]
@@ -58,7 +60,18 @@ constexpr int stream_wave_bytes(int px, int kx, int elem_bytes) {
 }
 
 // Kernel an item is routed to.
-enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1, kRoutePatch = 2 };
+enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1, kRoutePatch = 2, kRouteResize = 3 };
+
+// uint8 cache writer (resize_u8_kernel): one workgroup of kRsThreads per tile
+// of up to 32 output rows x 64 output columns of one frame; the host picks
+// smaller tiles where these LDS budgets require it.
+constexpr int kRsThreads = 256;
+constexpr int kRsChunk = 4;          // source rows staged per horizontal step (kRsThreads / 64)
+constexpr int kRsSrcRow = 2048;      // LDS bytes per staged source row
+constexpr int kRsMid = 32768;        // LDS bytes of the horizontal pass's uint8 rows
+constexpr int kRsQ = 2048;           // int32 weights of one axis per tile
+constexpr int kRsRowsMax = 32;
+constexpr int kRsColsMax = 64;
 
 struct DevItem {
     const uint8_t* frames;   // [n_src][H][W][3]
@@ -131,6 +144,9 @@ int launch_stream(const PlanView& plan, const StreamLaunch& launch, void* out, i
 // per merge-window row of a frame pair (tile_prefix counts them per item).
 int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
                     hipStream_t stream);
+// uint8 cache writer over tile_prefix (items with route kRouteResize: rh x cw
+// output tiles, tables holding fixed-point weights); out is the byte buffer.
+int launch_resize(const PlanView& plan, void* out, hipStream_t stream);
 // Whether a (m, kx, px) shape has a compiled streaming kernel.
 bool stream_shape_supported(int m, int kx, int px);
 

@@ -232,3 +232,39 @@ def test_extreme_downscale_is_rejected_not_truncated():
     with pytest.raises(vp.VPError) as e:
         vp.vp_batch_layout([it])
     assert e.value.status == vp.VP_ERR_CAPACITY
+
+
+@pytest.mark.parametrize("n_in,n_out", [(720, 256), (1280, 448), (1080, 448), (1920, 800),
+                                         (480, 352), (854, 640), (40, 64), (96, 96),
+                                         (3000, 96), (1, 32), (723, 736), (257, 256)])
+def test_fixed_filter_table_bit_exact_vs_oracle(n_in, n_out):
+    """The uint8 writer's 22-bit weights are rounded from the same doubles on
+    both sides, so they agree bit for bit."""
+    start, count, q = vp.vp_filter_table_fixed(n_in, n_out)
+    for i in range(n_out):
+        lo, ref = oracle.fixed_weights(n_in, n_out, i)
+        assert start[i] == lo and count[i] == len(ref)
+        assert np.array_equal(q[i, :count[i]], ref) and not q[i, count[i]:].any()
+
+
+def test_resize_layout_offsets_and_errors():
+    items = [vp.Item((0x10000, 5, 100, 70), [4, 0, 2], 64, 32),
+             vp.Item((0x20000, 1, 40, 50), [0], 64, 96)]
+    off, ws = vp.vp_resize_layout(items)
+    assert off.tolist() == [0, 3 * 64 * 32 * 3, 3 * 64 * 32 * 3 + 64 * 96 * 3] and ws > 0
+    L = vp.lib()
+    b = vp._Batch(items)
+    def raw(out=0x100000, cap=1 << 30, ws_ptr=0x200000, ws_bytes=1 << 30, its=b):
+        return L.vp_resize_batch(its.arr, len(its), ctypes.c_void_p(out), cap, None,
+                                 ctypes.c_void_p(ws_ptr), ws_bytes, None)
+    assert raw(out=0x100002) == vp.VP_ERR_ARG          # output not 4-byte aligned
+    assert raw(ws_ptr=0x200040) == vp.VP_ERR_ARG       # workspace not 256-byte aligned
+    assert raw(out=0) == vp.VP_ERR_NULL
+    assert raw(cap=int(off[-1]) - 1) == vp.VP_ERR_CAPACITY
+    assert raw(ws_bytes=ws - 1) == vp.VP_ERR_CAPACITY
+    assert raw(its=vp._Batch([vp.Item((0x10000, 5, 100, 70), [5], 64, 32)])) == vp.VP_ERR_INDEX
+    assert raw(its=vp._Batch([vp.Item((0x10000, 5, 100, 70), [1], 60, 32)])) == vp.VP_ERR_DIMS
+    # a window too long for any tile is rejected, not clipped
+    with pytest.raises(vp.VPError) as e:
+        vp.vp_resize_layout([vp.Item((0x10000, 1, 100, 40000), [0], 32, 32)])
+    assert e.value.status == vp.VP_ERR_CAPACITY
