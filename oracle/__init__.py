@@ -82,6 +82,7 @@ def lib() -> ctypes.CDLL:
         L.oracle_resize_u8.argtypes = [u8p, i64, i64, i64, i64, u8p]
         L.oracle_resize_u8_item.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64, u8p]
         L.oracle_layout.argtypes = [i64, i64p, i64p, i64p, i64p, i64p]
+        L.oracle_position_ids.argtypes = [i64, i64p, i64p, i64p, i64p, i64p, i64p, i64p]
         _lib = L
     return _lib
 
@@ -258,3 +259,22 @@ def layout(n_idx, h, w) -> tuple[np.ndarray, np.ndarray]:
                                _p(ww, ctypes.c_int64), _p(g, ctypes.c_int64),
                                _p(cu, ctypes.c_int64)), "layout")
     return g, cu
+
+
+def position_ids(n_idx, h, w):
+    """(vit_pos int64 [rows][3], llm_pos int64 [rows/4][3], vit_cu int64 [S+1])."""
+    n = np.ascontiguousarray(n_idx, dtype=np.int64)
+    hh = np.ascontiguousarray(h, dtype=np.int64)
+    ww = np.ascontiguousarray(w, dtype=np.int64)
+    rows = int(sum(item_rows(int(a), int(b), int(c)) for a, b, c in zip(n, hh, ww)))
+    slices = int(sum((int(a) + 1) // 2 for a in n))
+    vit = np.zeros((rows, 3), np.int64)
+    llm = np.zeros((rows // 4, 3), np.int64)
+    cu = np.zeros(slices + 1, np.int64)
+    ns = ctypes.c_int64()
+    _check(lib().oracle_position_ids(len(n), _p(n, ctypes.c_int64), _p(hh, ctypes.c_int64),
+                                     _p(ww, ctypes.c_int64), _p(vit, ctypes.c_int64),
+                                     _p(llm, ctypes.c_int64), _p(cu, ctypes.c_int64),
+                                     ctypes.byref(ns)), "position_ids")
+    assert ns.value == slices
+    return vit, llm, cu

@@ -708,6 +708,64 @@ int oracle_item_row(const uint8_t *frames, int64_t n_src, int64_t H, int64_t W,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Position tables (Section 1: metadata-consistent spatial-temporal         */
+/* positional encoding; Section 3.1.1: the same video_grid_thw everywhere)  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For every output row rho of the batch (item b owns rows [cu[b], cu[b+1])
+ * in merge-window order, decoded as in the patchify step):
+ *   vit_pos[rho] = (tt, 2*bh + mh, 2*bw + mw)   frame pair, patch row, patch column
+ * and for every merge window g = rho / 4 (one token after the 2x2 merge):
+ *   llm_pos[g] = (tt, bh, bw).
+ * The ViT attends within one frame pair of one item at a time:
+ *   vit_cu[0] = 0, vit_cu[s+1] = vit_cu[s] + (h/16)*(w/16) for every frame
+ *   pair s of every item in order; returns the number of pairs in *n_slices.
+ * Reading: these are the grid coordinates a 2D RoPE (ViT) and a 3-axis
+ * M-RoPE (LLM) take; the model's own temporal scaling and text offset are
+ * applied by the model, not here.
+ */
+int oracle_position_ids(int64_t n_items, const int64_t *n_idx, const int64_t *h, const int64_t *w,
+                        int64_t *vit_pos, int64_t *llm_pos, int64_t *vit_cu, int64_t *n_slices)
+{
+    if (n_idx == NULL || h == NULL || w == NULL || vit_pos == NULL || llm_pos == NULL ||
+        vit_cu == NULL || n_slices == NULL)
+        return OR_ERR_NULL;
+    int64_t row = 0, slice = 0;
+    vit_cu[0] = 0;
+    for (int64_t b = 0; b < n_items; b++) {
+        if (n_idx[b] < 1)
+            return OR_ERR_FRAMES;
+        if (h[b] < 32 || w[b] < 32 || h[b] % 32 != 0 || w[b] % 32 != 0)
+            return OR_ERR_DIMS;
+        int64_t hg = h[b] / OR_PATCH, wg = w[b] / OR_PATCH;
+        int64_t n_rows = oracle_item_rows(n_idx[b], h[b], w[b]);
+        for (int64_t r = 0; r < n_rows; r++) {
+            int64_t tt, i0, j0;
+            decode_row(r, hg, wg, &tt, &i0, &j0);
+            int64_t *v = vit_pos + 3 * (row + r);
+            v[0] = tt;
+            v[1] = i0 / OR_PATCH;
+            v[2] = j0 / OR_PATCH;
+            if (r % 4 == 0) {
+                int64_t *l = llm_pos + 3 * ((row + r) / 4);
+                l[0] = tt;
+                l[1] = i0 / (OR_PATCH * OR_MERGE);
+                l[2] = j0 / (OR_PATCH * OR_MERGE);
+            }
+        }
+        int64_t t = (n_idx[b] + 1) / 2;
+        for (int64_t k = 0; k < t; k++) {
+            vit_cu[slice + 1] = vit_cu[slice] + hg * wg;
+            slice++;
+        }
+        row += n_rows;
+    }
+    *n_slices = slice;
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* grid_thw and cu_seqlens (Section 3.1.1: every stage must produce the     */
 /* same video_grid_thw)                                                     */
 /* ------------------------------------------------------------------------ */

@@ -625,3 +625,42 @@ def test_resize_u8_item_order_and_errors():
     with pytest.raises(oracle.OracleError) as e:
         oracle.resize_u8_item(f, [0], 30, 64)
     assert e.value.code == oracle.ERR_DIMS
+
+
+# -- position tables ---------------------------------------------------------
+
+def test_position_ids_read_back_from_patchified_coordinates():
+    """Patchify frames whose pixels hold their own patch coordinates: each
+    row's content then names its patch, which must be the row's ViT position
+    (and its window's LLM position)."""
+    H, W = 64, 96
+    ii, jj = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    vals = np.zeros((4, 3, H, W), np.int64)
+    for fr in range(4):
+        vals[fr, 0] = ii // 16
+        vals[fr, 1] = jj // 16
+        vals[fr, 2] = 10 * (fr // 2)                     # frame pair
+    f = _identity_item(vals)
+    rows = oracle.patchify_item(f, [0, 1, 2, 3], (0.0,) * 3, (1 / 255,) * 3)
+    vit, llm, cu = oracle.position_ids([4], [H], [W])
+    got = np.stack([np.rint(rows[:, 1024]) // 10, np.rint(rows[:, 0]), np.rint(rows[:, 512])], 1)
+    assert np.array_equal(vit, got.astype(np.int64))
+    assert np.array_equal(llm, np.stack([vit[::4, 0], vit[::4, 1] // 2, vit[::4, 2] // 2], 1))
+    assert cu.tolist() == [0, 24, 48]
+
+
+def test_position_ids_by_reshape_and_ragged_segments():
+    n_idx, hs, ws = [3, 1, 4], [64, 96, 32], [32, 64, 160]
+    vit, llm, cu = oracle.position_ids(n_idx, hs, ws)
+    parts = []
+    for n, h, w in zip(n_idx, hs, ws):
+        t, hm, wm = (n + 1) // 2, h // 32, w // 32
+        tt, bh, bw, mh, mw = np.meshgrid(np.arange(t), np.arange(hm), np.arange(wm),
+                                         np.arange(2), np.arange(2), indexing="ij")
+        parts.append(np.stack([tt, 2 * bh + mh, 2 * bw + mw], -1).reshape(-1, 3))
+    assert np.array_equal(vit, np.concatenate(parts))
+    assert np.array_equal(llm[:, 1:], vit[::4, 1:] // 2) and np.array_equal(llm[:, 0], vit[::4, 0])
+    # one segment per frame pair: 2 + 1 + 2 pairs
+    assert cu.tolist() == [0, 8, 16, 40, 60, 80]
+    _, ocu = oracle.layout(n_idx, hs, ws)
+    assert cu[-1] == ocu[-1] == len(vit)
