@@ -114,6 +114,8 @@ def main():
                          "workload 4 (64 x 256 frames already at 256x448) instead")
     ap.add_argument("--resize", action="store_true",
                     help="time the uint8 cache writer (fixed-point resize only) on the workload")
+    ap.add_argument("--positions", action="store_true",
+                    help="time the position tables (ViT rows, LLM windows) of the workload's rows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run plain 1 GiB device-to-device copies (twice) before the steps, "
@@ -171,6 +173,10 @@ def main():
         frame_off, ws_bytes = vp.vp_resize_layout(vitems)
         rows = 0
         out = torch.empty(int(frame_off[-1]), dtype=torch.uint8, device=dev)
+    elif args.positions:
+        grid, cu, rows, ws_bytes = vp.vp_batch_layout(vitems)
+        out = torch.empty((rows, 3), dtype=torch.int32, device=dev)
+        out_llm = torch.empty((rows // 4, 3), dtype=torch.int32, device=dev)
     else:
         grid, cu, rows, ws_bytes = vp.vp_batch_layout(vitems)
         out = torch.empty((rows, vp.VP_ROW), dtype=torch.bfloat16 if code == vp.VP_OUT_BF16
@@ -180,6 +186,9 @@ def main():
     n_frames = sum(len(p[2]) for p in planned)
     in_bytes = sum(len(p[2]) * it.frame_bytes for p, it in zip(planned, wl.items))
     out_bytes = out.numel() * out.element_size()
+    if args.positions:   # no frame is read; both tables are written
+        in_bytes = 0
+        out_bytes += out_llm.numel() * out_llm.element_size()
     alg_bytes = in_bytes + out_bytes
     log(f"{n_frames} frames, {rows} rows, algorithmic bytes {alg_bytes / 1e9:.3f} GB "
         f"(in {in_bytes / 1e9:.3f}, out {out_bytes / 1e9:.3f})")
@@ -198,6 +207,8 @@ def main():
         items, _ = plan_items()
         if args.resize:
             vp.vp_resize_batch(items, out, work, stream)
+        elif args.positions:
+            vp.vp_position_ids(items, out, out_llm, work, stream)
         else:
             entry(items, wl.mean, wl.std, code, out, work, stream)
 
@@ -237,12 +248,13 @@ def main():
         f"({achieved / HBM_PEAK_GBPS:.1%} of 8 TB/s)")
     log("kernel ms per step: " + " ".join(f"{t:.3f}" for t in kern_ms))
 
-    tag = "p4" if args.patchify else (f"r{args.workload}" if args.resize else f"c{args.workload}")
+    tag = "p4" if args.patchify else (f"r{args.workload}" if args.resize else
+                                      (f"i{args.workload}" if args.positions else f"c{args.workload}"))
     sha = kernel_source_sha()
     traffic = counter_traffic(tag, sha)
 
     baseline = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.positions:
         log("timing the CPU oracle on a bounded sample")
         baseline = cpu_baseline(wl, frames, planned, patch_only=args.patchify, resize_only=args.resize)
         log(f"cpu baseline {baseline}")
@@ -258,14 +270,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "i32" if args.resize else "f32",
+        "dtype": "i32" if (args.resize or args.positions) else "f32",
         "data": "synthetic (seeded SplitMix64 frames resident in HBM)",
         "config": {
-            "workload": wl.name + ("; uint8 cache writer (fixed-point resize only)" if args.resize else ""),
+            "workload": wl.name + ("; uint8 cache writer (fixed-point resize only)" if args.resize else
+                                   "; position tables only" if args.positions else ""),
             "items": len(wl.items),
             "frames": n_frames,
             "rows": rows,
-            "out_dtype": "u8" if args.resize else wl.out_dtype,
+            "out_dtype": "u8" if args.resize else ("i32" if args.positions else wl.out_dtype),
             "mean": list(wl.mean),
             "std": list(wl.std),
             "algorithmic_bytes": alg_bytes,

@@ -274,9 +274,40 @@ int32_t vp_resize_batch(const vp_item* items, int32_t n_items, void* out_frames,
                         int64_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Position tables of a batch (Section 1: metadata-consistent
+ * spatial-temporal positional encoding; Section 3.1.1: the same
+ * video_grid_thw in every stage).  Items and their rows as in
+ * vp_batch_layout / vp_preprocess_batch (item b owns rows [cu[b], cu[b+1]),
+ * row cu[b] + ((tt*(h/32) + bh)*(w/32) + bw)*4 + mh*2 + mw):
+ *   vit_pos[row] = (tt, 2*bh + mh, 2*bw + mw)  frame pair, patch row, patch column
+ *     -- the coordinates of the ViT's 2D rotary embedding;
+ *   llm_pos[row/4] = (tt, bh, bw)  one per merge window, the token it becomes
+ *     after the 2x2 merge -- the grid coordinates of the LLM's 3-axis M-RoPE
+ *     (the model adds its own temporal scaling and text offset);
+ *   vit_cu: the ViT's attention segments, one per frame pair of each item:
+ *     vit_cu[0] = 0, vit_cu[s+1] = vit_cu[s] + (h/16)*(w/16).
+ * vit_pos: DEVICE int32 [rows][3], llm_pos: DEVICE int32 [rows/4][3]; either
+ *   may be NULL; rows_capacity = rows the caller's vit_pos holds (llm_pos
+ *   holds rows_capacity/4); 4-byte aligned.
+ * vit_cu: HOST int32 [vit_cu_capacity] (may be NULL); *n_slices (HOST, may
+ *   be NULL) = S, the number of segments.
+ * workspace, stream, ownership and asynchrony as for vp_preprocess_batch,
+ *   with the workspace_bytes of vp_batch_layout.  The frames pointers are
+ *   not dereferenced.
+ * Errors: VP_ERR_NULL, VP_ERR_ARG, VP_ERR_DIMS, VP_ERR_FRAMES, VP_ERR_INDEX,
+ * VP_ERR_CAPACITY (rows_capacity < rows, vit_cu_capacity < S + 1,
+ * workspace too small), VP_ERR_HIP.
+ */
+int32_t vp_position_ids(const vp_item* items, int32_t n_items, int32_t* vit_pos,
+                        int32_t* llm_pos, int64_t rows_capacity, int32_t* vit_cu,
+                        int32_t vit_cu_capacity, int32_t* n_slices, void* workspace,
+                        int64_t workspace_bytes, hipStream_t stream);
+
+/*
  * Kernel timing hook (measurement only; not a step of the method).  The next
- * vp_preprocess_batch, vp_patchify_batch or vp_resize_batch call made on this
- * thread records `start` on its stream immediately before its first kernel
+ * vp_preprocess_batch, vp_patchify_batch, vp_resize_batch or vp_position_ids
+ * call made on this thread (one that launches kernels) records `start` on
+ * its stream immediately before its first kernel
  * launch (after the plan upload) and
  * `stop` immediately after its last launch, then forgets both events, so
  * that hipEventElapsedTime(start, stop) is the device time of that call's

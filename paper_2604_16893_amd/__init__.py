@@ -32,8 +32,8 @@ VP_FACTOR = 32
 
 EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
             "vp_filter_table_fixed", "vp_batch_layout", "vp_preprocess_batch", "vp_patchify_batch",
-            "vp_resize_layout", "vp_resize_batch", "vp_status_string", "vp_last_error_message",
-            "vp_set_kernel_events")
+            "vp_resize_layout", "vp_resize_batch", "vp_position_ids", "vp_status_string",
+            "vp_last_error_message", "vp_set_kernel_events")
 
 
 class VPError(RuntimeError):
@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
                                           i32p, i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
         L.vp_patchify_batch.argtypes = L.vp_preprocess_batch.argtypes
         L.vp_filter_table_fixed.argtypes = [i32, i32, i32, i32p, i32p, i32p]
+        L.vp_position_ids.argtypes = [itemp, i32, ctypes.c_void_p, ctypes.c_void_p, i64, i32p, i32,
+                                      i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
         L.vp_resize_layout.argtypes = [itemp, i32, i64p, i64p]
         L.vp_resize_batch.argtypes = [itemp, i32, ctypes.c_void_p, i64, i64p, ctypes.c_void_p, i64,
                                       ctypes.c_void_p]
@@ -322,6 +324,33 @@ def vp_resize_batch(items: Sequence, out_frames, workspace, stream=None):
                                  workspace.numel() * workspace.element_size(),
                                  ctypes.c_void_p(_stream_handle(stream))), "vp_resize_batch")
     return off
+
+
+def vp_position_ids(items: Sequence, vit_pos, llm_pos, workspace, stream=None):
+    """Enqueue the position tables: vit_pos int32 CUDA tensor [>= rows, 3] and
+    llm_pos int32 CUDA tensor [>= rows/4, 3] (either may be None); workspace
+    as for vp_preprocess_batch.  Returns the ViT segments vit_cu (int32
+    numpy [S+1]), final on return."""
+    import torch
+    for name, t in (("vit_pos", vit_pos), ("llm_pos", llm_pos)):
+        if t is not None and (t.dtype != torch.int32 or t.dim() != 2 or t.shape[1] != 3
+                              or not t.is_contiguous() or not t.is_cuda):
+            raise VPError(VP_ERR_ARG, f"{name} must be a contiguous CUDA int32 [n, 3] tensor")
+    b = _Batch(items)
+    B = len(b)
+    cap = sum((len(np.asarray(it.indices).reshape(-1)) + 1) // 2 for it in items) + 1
+    cu = np.zeros(cap, np.int32)
+    ns = ctypes.c_int32()
+    rows_cap = vit_pos.shape[0] if vit_pos is not None else (llm_pos.shape[0] * 4 if llm_pos is not None else 0)
+    if vit_pos is not None and llm_pos is not None:
+        rows_cap = min(vit_pos.shape[0], llm_pos.shape[0] * 4)
+    _check(lib().vp_position_ids(
+        b.arr, B, ctypes.c_void_p(vit_pos.data_ptr() if vit_pos is not None else 0),
+        ctypes.c_void_p(llm_pos.data_ptr() if llm_pos is not None else 0), rows_cap,
+        _ptr(cu, ctypes.c_int32), cap, ctypes.byref(ns), ctypes.c_void_p(workspace.data_ptr()),
+        workspace.numel() * workspace.element_size(), ctypes.c_void_p(_stream_handle(stream))),
+        "vp_position_ids")
+    return cu[:ns.value + 1]
 
 
 def resize_u8(items: Sequence, stream=None):

@@ -687,6 +687,52 @@ int32_t build_patch_plan(const vp_item* items, int32_t n, Plan* p) {
     return VP_OK;
 }
 
+// Plan of the row tables (vp_position_ids): per item its grid, with the
+// items' row offsets (cu) as the prefix the kernel searches.
+int32_t build_rows_plan(const vp_item* items, int32_t n, Plan* p) {
+    if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
+    if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    p->items.assign(n, vp::DevItem{});
+    p->grid.assign(size_t(n) * 3, 0);
+    p->cu.assign(n + 1, 0);
+    p->indices.clear();
+    p->tables.clear();
+    p->table_words = 0;
+    p->units.clear();
+    p->wgs.clear();
+    p->launches.clear();
+    p->generic_cost = 0;
+    int64_t rows = 0;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp_item& it = items[b];
+        const int32_t st = validate_item(it, b);
+        if (st != VP_OK) return st;
+        vp::DevItem& d = p->items[b];
+        d.h = it.dst_h;
+        d.w = it.dst_w;
+        d.t = (it.n_idx + 1) / 2;
+        d.hm = it.dst_h / vp::kWin;
+        d.wm = it.dst_w / vp::kWin;
+        d.row_off = rows;
+        p->grid[3 * b + 0] = d.t;
+        p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
+        p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
+        rows += int64_t(d.t) * (it.dst_h / vp::kPatch) * (it.dst_w / vp::kPatch);
+        if (rows > INT32_MAX) return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 rows");
+        p->cu[b + 1] = static_cast<int32_t>(rows);
+    }
+    p->prefix = p->cu;
+    p->total_rows = rows;
+    p->off_items = 0;
+    p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
+    p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
+    p->off_tables = p->off_indices;
+    p->off_units = p->off_indices;
+    p->off_wgs = p->off_indices;
+    p->bytes = p->off_indices;
+    return VP_OK;
+}
+
 // Output tile of the uint8 writer for an item: the largest rows x columns
 // (rows from 32 down, then columns from 64 down) whose horizontal-pass rows,
 // staged source span and weights fit the kernel's LDS budgets.
@@ -1242,6 +1288,64 @@ int32_t vp_resize_batch(const vp_item* items, int32_t n_items, void* out_frames,
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");
     }
     if (frame_off) std::memcpy(frame_off, p.byte_off.data(), sizeof(int64_t) * p.byte_off.size());
+    g_last_error.clear();
+    return VP_OK;
+}
+
+int32_t vp_position_ids(const vp_item* items, int32_t n_items, int32_t* vit_pos,
+                        int32_t* llm_pos, int64_t rows_capacity, int32_t* vit_cu,
+                        int32_t vit_cu_capacity, int32_t* n_slices, void* workspace,
+                        int64_t workspace_bytes, hipStream_t stream) {
+    if (workspace == nullptr) return fail(VP_ERR_NULL, "workspace must be non-NULL");
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+        return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
+    if (reinterpret_cast<uintptr_t>(vit_pos) % 4 != 0 || reinterpret_cast<uintptr_t>(llm_pos) % 4 != 0)
+        return fail(VP_ERR_ARG, "vit_pos and llm_pos must be 4-byte aligned");
+    Plan p;
+    int32_t st = build_rows_plan(items, n_items, &p);
+    if (st != VP_OK) return st;
+    if ((vit_pos != nullptr || llm_pos != nullptr) && rows_capacity < p.total_rows)
+        return fail(VP_ERR_CAPACITY, "position tables hold " + std::to_string(rows_capacity) +
+                                         " rows, batch needs " + std::to_string(p.total_rows));
+    int64_t slices = 0;
+    for (int32_t b = 0; b < n_items; ++b) slices += p.items[b].t;
+    if (vit_cu != nullptr && vit_cu_capacity < slices + 1)
+        return fail(VP_ERR_CAPACITY, "vit_cu holds " + std::to_string(vit_cu_capacity) +
+                                         " entries, batch needs " + std::to_string(slices + 1));
+    if (workspace_bytes < static_cast<int64_t>(p.bytes))
+        return fail(VP_ERR_CAPACITY, "workspace holds " + std::to_string(workspace_bytes) +
+                                         " bytes, plan needs " + std::to_string(p.bytes));
+    hipEvent_t t_start = g_timing_start, t_stop = g_timing_stop;
+    g_timing_start = g_timing_stop = nullptr;
+    if (vit_pos != nullptr || llm_pos != nullptr) {
+        st = upload_plan(p, workspace, stream);
+        if (st != VP_OK) return st;
+        if (t_start != nullptr) {
+            const hipError_t e = hipEventRecord(t_start, stream);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing start)");
+        }
+        auto* ws = static_cast<uint8_t*>(workspace);
+        vp::PlanView view{};
+        view.items = reinterpret_cast<const vp::DevItem*>(ws + p.off_items);
+        view.tile_prefix = reinterpret_cast<const int32_t*>(ws + p.off_prefix);
+        view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
+        view.n_items = n_items;
+        view.n_tiles = 0;
+        const int err = vp::launch_positions(view, vit_pos, llm_pos, p.total_rows, stream);
+        if (err != 0) return hip_fail(static_cast<hipError_t>(err), "position kernel launch");
+        if (t_stop != nullptr) {
+            const hipError_t e = hipEventRecord(t_stop, stream);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");
+        }
+    }
+    if (vit_cu != nullptr) {
+        int64_t s = 0;
+        vit_cu[0] = 0;
+        for (int32_t b = 0; b < n_items; ++b)
+            for (int32_t k = 0; k < p.items[b].t; ++k, ++s)
+                vit_cu[s + 1] = vit_cu[s] + p.grid[3 * b + 1] * p.grid[3 * b + 2];
+    }
+    if (n_slices) *n_slices = static_cast<int32_t>(slices);
     g_last_error.clear();
     return VP_OK;
 }

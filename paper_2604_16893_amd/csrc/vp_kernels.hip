@@ -165,6 +165,41 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
 }
 
 // ===========================================================================
+// Position tables
+// ===========================================================================
+
+// One thread per output row: the row's item (binary search over the row
+// offsets), then its frame pair, patch row and patch column from the
+// merge-window order; the first row of each window also writes the window's
+// token coordinates.
+__global__ __launch_bounds__(256) void positions_kernel(PlanView plan, int32_t* vit, int32_t* llm,
+                                                         int64_t rows) {
+    for (int64_t row = int64_t(blockIdx.x) * 256 + threadIdx.x; row < rows;
+         row += int64_t(gridDim.x) * 256) {
+        const int b = find_item(plan.tile_prefix, plan.n_items, static_cast<int>(row));
+        const cptr<DevItem> it = as_const(plan.items) + b;
+        const int local = static_cast<int>(row) - plan.tile_prefix[b];
+        const int sub = local & 3, win = local >> 2;
+        const int wm = it->wm, hm = it->hm;
+        const int bw = win % wm;
+        const int bh = (win / wm) % hm;
+        const int tt = win / (wm * hm);
+        if (vit != nullptr) {
+            int32_t* v = vit + row * 3;
+            v[0] = tt;
+            v[1] = 2 * bh + (sub >> 1);
+            v[2] = 2 * bw + (sub & 1);
+        }
+        if (llm != nullptr && sub == 0) {
+            int32_t* l = llm + (row >> 2) * 3;
+            l[0] = tt;
+            l[1] = bh;
+            l[2] = bw;
+        }
+    }
+}
+
+// ===========================================================================
 // uint8 cache writer (fixed-point resampling)
 // ===========================================================================
 
@@ -741,6 +776,15 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 }
 
 }  // namespace
+
+int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t rows,
+                     hipStream_t stream) {
+    if (rows <= 0 || (vit == nullptr && llm == nullptr)) return 0;
+    const int64_t blocks = std::min<int64_t>((rows + 255) / 256, 65536);
+    hipLaunchKernelGGL(positions_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, plan,
+                       vit, llm, rows);
+    return static_cast<int>(hipGetLastError());
+}
 
 int launch_resize(const PlanView& plan, void* out, hipStream_t stream) {
     if (plan.n_tiles <= 0) return 0;

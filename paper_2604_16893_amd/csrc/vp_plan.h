@@ -147,6 +147,10 @@ int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& 
 // uint8 cache writer over tile_prefix (items with route kRouteResize: rh x cw
 // output tiles, tables holding fixed-point weights); out is the byte buffer.
 int launch_resize(const PlanView& plan, void* out, hipStream_t stream);
+// Position tables: one thread per output row; tile_prefix holds the items'
+// row offsets (cu).  vit / llm may be null.
+int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t rows,
+                     hipStream_t stream);
 // Whether a (m, kx, px) shape has a compiled streaming kernel.
 bool stream_shape_supported(int m, int kx, int px);
 

@@ -268,3 +268,31 @@ def test_resize_layout_offsets_and_errors():
     with pytest.raises(vp.VPError) as e:
         vp.vp_resize_layout([vp.Item((0x10000, 1, 100, 40000), [0], 32, 32)])
     assert e.value.status == vp.VP_ERR_CAPACITY
+
+
+def test_position_ids_segments_and_errors_on_host():
+    """The ViT segments come back on the host; the device tables need a GPU
+    (their errors are all found before anything is enqueued)."""
+    items = [vp.Item((0x10000, 5, 100, 70), [4, 0, 2], 64, 32),
+             vp.Item((0x20000, 1, 40, 50), [0], 96, 64)]
+    L = vp.lib()
+    b = vp._Batch(items)
+    cu = np.zeros(4, np.int32)
+    ns = ctypes.c_int32()
+    ws = ctypes.c_void_p(0x200000)
+    # no device table: only the segments, and nothing is enqueued
+    assert L.vp_position_ids(b.arr, 2, None, None, 0, cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                             4, ctypes.byref(ns), ws, 1 << 20, None) == vp.VP_OK
+    _, _, ocu = oracle.position_ids([3, 1], [64, 96], [32, 64])
+    assert ns.value == 3 and cu.tolist() == ocu.tolist()
+    cu_p = cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    assert L.vp_position_ids(b.arr, 2, None, None, 0, cu_p, 3, None, ws, 1 << 20, None) == vp.VP_ERR_CAPACITY
+    dev = ctypes.c_void_p(0x300000)
+    assert L.vp_position_ids(b.arr, 2, dev, None, 39, None, 0, None, ws, 1 << 20, None) == vp.VP_ERR_CAPACITY   # 40 rows
+    assert L.vp_position_ids(b.arr, 2, ctypes.c_void_p(0x300002), None, 1 << 20, None, 0, None, ws,
+                             1 << 20, None) == vp.VP_ERR_ARG
+    assert L.vp_position_ids(b.arr, 2, dev, None, 1 << 20, None, 0, None, ctypes.c_void_p(0x200010),
+                             1 << 20, None) == vp.VP_ERR_ARG
+    assert L.vp_position_ids(b.arr, 2, dev, None, 1 << 20, None, 0, None, None, 1 << 20, None) == vp.VP_ERR_NULL
+    bad = vp._Batch([vp.Item((0x10000, 5, 100, 70), [4, 0, 2], 64, 48)])
+    assert L.vp_position_ids(bad.arr, 1, dev, None, 1 << 20, None, 0, None, ws, 1 << 20, None) == vp.VP_ERR_DIMS
