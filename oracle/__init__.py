@@ -71,18 +71,18 @@ def lib() -> ctypes.CDLL:
         L.oracle_resize_pixel.restype = ctypes.c_double
         L.oracle_normalize.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double]
         L.oracle_normalize.restype = ctypes.c_double
-        L.oracle_item_rows.argtypes = [i64, i64, i64]
+        L.oracle_item_rows.argtypes = [i64, i64, i64, i64]
         L.oracle_item_rows.restype = i64
-        L.oracle_preprocess_item.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64,
+        L.oracle_preprocess_item.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64, i64,
                                              f64p, f64p, f64p]
-        L.oracle_item_row.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64,
+        L.oracle_item_row.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64, i64,
                                       f64p, f64p, i64, f64p]
-        L.oracle_patchify_item.argtypes = [u8p, i64, i64, i64, i32p, i64, f64p, f64p, f64p]
+        L.oracle_patchify_item.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, f64p, f64p, f64p]
         L.oracle_fixed_weights.argtypes = [i64, i64, i64, i64p, i64p, i32p, i64]
         L.oracle_resize_u8.argtypes = [u8p, i64, i64, i64, i64, u8p]
-        L.oracle_resize_u8_item.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64, u8p]
-        L.oracle_layout.argtypes = [i64, i64p, i64p, i64p, i64p, i64p]
-        L.oracle_position_ids.argtypes = [i64, i64p, i64p, i64p, i64p, i64p, i64p, i64p]
+        L.oracle_resize_u8_item.argtypes = [u8p, i64, i64, i64, i32p, i64, i64, i64, i64, u8p]
+        L.oracle_layout.argtypes = [i64, i64p, i64p, i64p, i64, i64p, i64p]
+        L.oracle_position_ids.argtypes = [i64, i64p, i64p, i64p, i64, i64p, i64p, i64p, i64p]
         _lib = L
     return _lib
 
@@ -169,8 +169,13 @@ def normalize(r: float, mean: float, std: float) -> float:
     return lib().oracle_normalize(r, mean, std)
 
 
-def item_rows(n_idx: int, h: int, w: int) -> int:
-    return lib().oracle_item_rows(n_idx, h, w)
+def item_rows(n_idx: int, h: int, w: int, patch: int = 16) -> int:
+    return lib().oracle_item_rows(n_idx, h, w, patch)
+
+
+def row_width(patch: int = 16) -> int:
+    """Values per merge-window row: 3 channels x 2 frames x patch x patch."""
+    return 6 * patch * patch
 
 
 def _item_args(frames, indices, mean, std):
@@ -182,26 +187,27 @@ def _item_args(frames, indices, mean, std):
     return f, idx, m, s
 
 
-def preprocess_item(frames: np.ndarray, indices, h: int, w: int, mean, std) -> np.ndarray:
-    """frames uint8 [N][H][W][3] -> fp64 rows [t*(h/16)*(w/16)][1536]."""
+def preprocess_item(frames: np.ndarray, indices, h: int, w: int, mean, std,
+                    patch: int = 16) -> np.ndarray:
+    """frames uint8 [N][H][W][3] -> fp64 rows [t*(h/P)*(w/P)][6*P*P]."""
     f, idx, m, s = _item_args(frames, indices, mean, std)
     n_src, H, W, _ = f.shape
-    rows = np.zeros((item_rows(len(idx), h, w), ROW), np.float64)
+    rows = np.zeros((item_rows(len(idx), h, w, patch), row_width(patch)), np.float64)
     _check(lib().oracle_preprocess_item(_p(f, ctypes.c_uint8), n_src, H, W, _p(idx, ctypes.c_int32),
-                                        len(idx), h, w, _p(m, ctypes.c_double),
+                                        len(idx), h, w, patch, _p(m, ctypes.c_double),
                                         _p(s, ctypes.c_double), _p(rows, ctypes.c_double)),
            "preprocess_item")
     return rows
 
 
-def patchify_item(frames: np.ndarray, indices, mean, std) -> np.ndarray:
+def patchify_item(frames: np.ndarray, indices, mean, std, patch: int = 16) -> np.ndarray:
     """Normalise + patchify only: frames uint8 [N][h][w][3], already at the
-    target size -> fp64 rows [t*(h/16)*(w/16)][1536]."""
+    target size -> fp64 rows [t*(h/P)*(w/P)][6*P*P]."""
     f, idx, m, s = _item_args(frames, indices, mean, std)
     n_src, h, w, _ = f.shape
-    rows = np.zeros((item_rows(len(idx), h, w), ROW), np.float64)
+    rows = np.zeros((item_rows(len(idx), h, w, patch), row_width(patch)), np.float64)
     _check(lib().oracle_patchify_item(_p(f, ctypes.c_uint8), n_src, h, w, _p(idx, ctypes.c_int32),
-                                      len(idx), _p(m, ctypes.c_double), _p(s, ctypes.c_double),
+                                      len(idx), patch, _p(m, ctypes.c_double), _p(s, ctypes.c_double),
                                       _p(rows, ctypes.c_double)), "patchify_item")
     return rows
 
@@ -225,29 +231,30 @@ def resize_u8(frame: np.ndarray, h: int, w: int) -> np.ndarray:
     return out
 
 
-def resize_u8_item(frames: np.ndarray, indices, h: int, w: int) -> np.ndarray:
+def resize_u8_item(frames: np.ndarray, indices, h: int, w: int, patch: int = 16) -> np.ndarray:
     """The cache writer for one item: uint8 [n_idx][h][w][3]."""
     f = np.ascontiguousarray(frames, dtype=np.uint8)
     n_src, H, W, _ = f.shape
     idx = np.ascontiguousarray(indices, dtype=np.int32)
     out = np.zeros((len(idx), h, w, 3), np.uint8)
     _check(lib().oracle_resize_u8_item(_p(f, ctypes.c_uint8), n_src, H, W, _p(idx, ctypes.c_int32),
-                                       len(idx), h, w, _p(out, ctypes.c_uint8)), "resize_u8_item")
+                                       len(idx), h, w, patch, _p(out, ctypes.c_uint8)), "resize_u8_item")
     return out
 
 
-def item_row(frames: np.ndarray, indices, h: int, w: int, mean, std, rho: int) -> np.ndarray:
-    """One output row by the direct 2D sum (fp64 [1536])."""
+def item_row(frames: np.ndarray, indices, h: int, w: int, mean, std, rho: int,
+             patch: int = 16) -> np.ndarray:
+    """One output row by the direct 2D sum (fp64 [6*P*P])."""
     f, idx, m, s = _item_args(frames, indices, mean, std)
     n_src, H, W, _ = f.shape
-    row = np.zeros(ROW, np.float64)
+    row = np.zeros(row_width(patch), np.float64)
     _check(lib().oracle_item_row(_p(f, ctypes.c_uint8), n_src, H, W, _p(idx, ctypes.c_int32),
-                                 len(idx), h, w, _p(m, ctypes.c_double), _p(s, ctypes.c_double),
+                                 len(idx), h, w, patch, _p(m, ctypes.c_double), _p(s, ctypes.c_double),
                                  rho, _p(row, ctypes.c_double)), "item_row")
     return row
 
 
-def layout(n_idx, h, w) -> tuple[np.ndarray, np.ndarray]:
+def layout(n_idx, h, w, patch: int = 16) -> tuple[np.ndarray, np.ndarray]:
     """(grid_thw [B][3], cu_seqlens [B+1]) as int64."""
     n = np.ascontiguousarray(n_idx, dtype=np.int64)
     hh = np.ascontiguousarray(h, dtype=np.int64)
@@ -256,24 +263,24 @@ def layout(n_idx, h, w) -> tuple[np.ndarray, np.ndarray]:
     g = np.zeros((B, 3), np.int64)
     cu = np.zeros(B + 1, np.int64)
     _check(lib().oracle_layout(B, _p(n, ctypes.c_int64), _p(hh, ctypes.c_int64),
-                               _p(ww, ctypes.c_int64), _p(g, ctypes.c_int64),
+                               _p(ww, ctypes.c_int64), patch, _p(g, ctypes.c_int64),
                                _p(cu, ctypes.c_int64)), "layout")
     return g, cu
 
 
-def position_ids(n_idx, h, w):
+def position_ids(n_idx, h, w, patch: int = 16):
     """(vit_pos int64 [rows][3], llm_pos int64 [rows/4][3], vit_cu int64 [S+1])."""
     n = np.ascontiguousarray(n_idx, dtype=np.int64)
     hh = np.ascontiguousarray(h, dtype=np.int64)
     ww = np.ascontiguousarray(w, dtype=np.int64)
-    rows = int(sum(item_rows(int(a), int(b), int(c)) for a, b, c in zip(n, hh, ww)))
+    rows = int(sum(item_rows(int(a), int(b), int(c), patch) for a, b, c in zip(n, hh, ww)))
     slices = int(sum((int(a) + 1) // 2 for a in n))
     vit = np.zeros((rows, 3), np.int64)
     llm = np.zeros((rows // 4, 3), np.int64)
     cu = np.zeros(slices + 1, np.int64)
     ns = ctypes.c_int64()
     _check(lib().oracle_position_ids(len(n), _p(n, ctypes.c_int64), _p(hh, ctypes.c_int64),
-                                     _p(ww, ctypes.c_int64), _p(vit, ctypes.c_int64),
+                                     _p(ww, ctypes.c_int64), patch, _p(vit, ctypes.c_int64),
                                      _p(llm, ctypes.c_int64), _p(cu, ctypes.c_int64),
                                      ctypes.byref(ns)), "position_ids")
     assert ns.value == slices

@@ -8,10 +8,11 @@
  * Section 4.1, "Training Configuration"):
  *
  *   temporal frame-index sampling -> smart_resize of (H, W) to multiples of
- *   32 under a pixel budget -> antialiased bicubic resampling of uint8 RGB
+ *   2P under a pixel budget -> antialiased bicubic resampling of uint8 RGB
  *   frames -> rescale by 1/255 and per-channel mean/std normalisation ->
- *   patchification into merge-window rows of 3*2*16*16 = 1536 values, with
- *   the per-item grid (t, h/16, w/16) and the row-offset table.
+ *   patchification into merge-window rows of 3*2*P*P values (P = 16: 1536;
+ *   P = 14: 1176), with the per-item grid (t, h/P, w/P) and the row-offset
+ *   table.
  *
  * The paper names these stages and their parameters (fps, max_frames,
  * max_pixels, separate image/video budgets, identical video_grid_thw in every
@@ -49,12 +50,13 @@
 #define OR_ERR_CAPACITY 7
 #define OR_ERR_NOMEM 9
 
-/* Geometry of a Qwen-VL-style vision input: patch 16, spatial merge 2,
- * temporal patch 2, so a merge-window row holds 3 * 2 * 16 * 16 values. */
-#define OR_PATCH 16
+/* Geometry of a Qwen-VL-style vision input: a patch of P x P pixels
+ * (P = 16 for Qwen3-VL, 14 for Qwen2-VL and Qwen2.5-VL), spatial merge 2,
+ * temporal patch 2, so a merge-window row holds 3 * 2 * P * P values
+ * (1536 or 1176).  P is an argument of every function that needs it. */
 #define OR_MERGE 2
 #define OR_TPATCH 2
-#define OR_ROW (3 * OR_TPATCH * OR_PATCH * OR_PATCH)
+#define OR_ROW(P) (3 * OR_TPATCH * (P) * (P))
 
 /* ------------------------------------------------------------------------ */
 /* Rounding helpers                                                         */
@@ -425,7 +427,7 @@ int oracle_fixed_weights(int64_t n_in, int64_t n_out, int64_t i, int64_t *lo, in
 }
 
 static int check_item(int64_t n_src, int64_t H, int64_t W, const int32_t *indices,
-                      int64_t n_idx, int64_t h, int64_t w);
+                      int64_t n_idx, int64_t h, int64_t w, int64_t patch);
 
 static uint8_t fixed_to_byte(int64_t acc)
 {
@@ -487,11 +489,11 @@ int oracle_resize_u8(const uint8_t *frame, int64_t H, int64_t W, int64_t h, int6
  */
 int oracle_resize_u8_item(const uint8_t *frames, int64_t n_src, int64_t H, int64_t W,
                           const int32_t *indices, int64_t n_idx, int64_t h, int64_t w,
-                          uint8_t *out)
+                          int64_t patch, uint8_t *out)
 {
     if (frames == NULL || out == NULL)
         return OR_ERR_NULL;
-    int st = check_item(n_src, H, W, indices, n_idx, h, w);
+    int st = check_item(n_src, H, W, indices, n_idx, h, w, patch);
     for (int64_t k = 0; k < n_idx && st == OR_OK; k++)
         st = oracle_resize_u8(frames + (int64_t)indices[k] * H * W * 3, H, W, h, w,
                               out + k * h * w * 3);
@@ -534,8 +536,8 @@ static int64_t pad_indices(const int32_t *indices, int64_t n_idx, int32_t *padde
  * then temporal, then a 16x16 raster.  These two functions map a (rho, k)
  * pair back to (frame-in-pair, channel, pixel row, pixel column).
  */
-static void decode_row(int64_t rho, int64_t hg, int64_t wg, int64_t *tt, int64_t *i0,
-                       int64_t *j0)
+static void decode_row(int64_t rho, int64_t hg, int64_t wg, int64_t patch, int64_t *tt,
+                       int64_t *i0, int64_t *j0)
 {
     int64_t hm = hg / OR_MERGE, wm = wg / OR_MERGE;
     int64_t win = rho / 4, sub = rho % 4;
@@ -543,26 +545,28 @@ static void decode_row(int64_t rho, int64_t hg, int64_t wg, int64_t *tt, int64_t
     int64_t bw = win % wm;
     int64_t bh = (win / wm) % hm;
     *tt = win / (wm * hm);
-    *i0 = OR_PATCH * (2 * bh + mh);
-    *j0 = OR_PATCH * (2 * bw + mw);
+    *i0 = patch * (2 * bh + mh);
+    *j0 = patch * (2 * bw + mw);
 }
 
-static void decode_col(int64_t k, int64_t *c, int64_t *dt, int64_t *y, int64_t *x)
+static void decode_col(int64_t k, int64_t patch, int64_t *c, int64_t *dt, int64_t *y, int64_t *x)
 {
-    *x = k % OR_PATCH;
-    *y = (k / OR_PATCH) % OR_PATCH;
-    *dt = (k / (OR_PATCH * OR_PATCH)) % OR_TPATCH;
-    *c = k / (OR_PATCH * OR_PATCH * OR_TPATCH);
+    *x = k % patch;
+    *y = (k / patch) % patch;
+    *dt = (k / (patch * patch)) % OR_TPATCH;
+    *c = k / (patch * patch * OR_TPATCH);
 }
 
 static int check_item(int64_t n_src, int64_t H, int64_t W, const int32_t *indices,
-                      int64_t n_idx, int64_t h, int64_t w)
+                      int64_t n_idx, int64_t h, int64_t w, int64_t patch)
 {
+    if (patch < 1)
+        return OR_ERR_ARG;
     if (indices == NULL)
         return OR_ERR_NULL;
     if (n_src < 1 || H < 1 || W < 1 || h < 1 || w < 1)
         return OR_ERR_DIMS;
-    if (h % (OR_PATCH * OR_MERGE) != 0 || w % (OR_PATCH * OR_MERGE) != 0)
+    if (h % (patch * OR_MERGE) != 0 || w % (patch * OR_MERGE) != 0)
         return OR_ERR_DIMS;
     if (n_idx < 1)
         return OR_ERR_FRAMES;
@@ -572,26 +576,26 @@ static int check_item(int64_t n_src, int64_t H, int64_t W, const int32_t *indice
     return OR_OK;
 }
 
-/* Number of output rows of one item: t * (h/16) * (w/16), t = ceil(n_idx/2). */
-int64_t oracle_item_rows(int64_t n_idx, int64_t h, int64_t w)
+/* Number of output rows of one item: t * (h/P) * (w/P), t = ceil(n_idx/2). */
+int64_t oracle_item_rows(int64_t n_idx, int64_t h, int64_t w, int64_t patch)
 {
     int64_t t = (n_idx + 1) / 2;
-    return t * (h / OR_PATCH) * (w / OR_PATCH);
+    return t * (h / patch) * (w / patch);
 }
 
 /*
  * Whole item: frames[n_src][H][W][3] (uint8), sampled at `indices`, resized
  * to h x w, normalised, padded to an even frame count and patchified into
- * rows[oracle_item_rows][1536] (double).  Frame pairs are processed one at a
+ * rows[oracle_item_rows][6*P*P] (double).  Frame pairs are processed one at a
  * time; the result does not depend on that order.
  */
 int oracle_preprocess_item(const uint8_t *frames, int64_t n_src, int64_t H, int64_t W,
                            const int32_t *indices, int64_t n_idx, int64_t h, int64_t w,
-                           const double *mean, const double *std, double *rows)
+                           int64_t patch, const double *mean, const double *std, double *rows)
 {
     if (frames == NULL || mean == NULL || std == NULL || rows == NULL)
         return OR_ERR_NULL;
-    int st = check_item(n_src, H, W, indices, n_idx, h, w);
+    int st = check_item(n_src, H, W, indices, n_idx, h, w, patch);
     if (st != OR_OK)
         return st;
     int32_t *padded = malloc(sizeof(int32_t) * (size_t)(n_idx + 1));
@@ -604,7 +608,7 @@ int oracle_preprocess_item(const uint8_t *frames, int64_t n_src, int64_t H, int6
         return OR_ERR_NOMEM;
     }
     int64_t n_pad = pad_indices(indices, n_idx, padded);
-    int64_t t = n_pad / OR_TPATCH, hg = h / OR_PATCH, wg = w / OR_PATCH;
+    int64_t t = n_pad / OR_TPATCH, hg = h / patch, wg = w / patch;
     int64_t rows_per_t = hg * wg;
     int64_t frame_bytes = H * W * 3;
     for (int64_t tt = 0; tt < t && st == OR_OK; tt++) {
@@ -619,11 +623,11 @@ int oracle_preprocess_item(const uint8_t *frames, int64_t n_src, int64_t H, int6
         for (int64_t r = 0; r < rows_per_t && st == OR_OK; r++) {
             int64_t rho = tt * rows_per_t + r;
             int64_t t_chk, i0, j0;
-            decode_row(rho, hg, wg, &t_chk, &i0, &j0);
-            for (int64_t k = 0; k < OR_ROW; k++) {
+            decode_row(rho, hg, wg, patch, &t_chk, &i0, &j0);
+            for (int64_t k = 0; k < OR_ROW(patch); k++) {
                 int64_t c, dt, y, x;
-                decode_col(k, &c, &dt, &y, &x);
-                rows[rho * OR_ROW + k] = v[dt][(c * h + (i0 + y)) * w + (j0 + x)];
+                decode_col(k, patch, &c, &dt, &y, &x);
+                rows[rho * OR_ROW(patch) + k] = v[dt][(c * h + (i0 + y)) * w + (j0 + x)];
             }
         }
     }
@@ -642,30 +646,30 @@ int oracle_preprocess_item(const uint8_t *frames, int64_t n_src, int64_t H, int6
  *   rows[rho][k] = normalise(frames[padded[2 tt + dt]][i0 + y][j0 + x][c]).
  */
 int oracle_patchify_item(const uint8_t *frames, int64_t n_src, int64_t h, int64_t w,
-                         const int32_t *indices, int64_t n_idx, const double *mean,
+                         const int32_t *indices, int64_t n_idx, int64_t patch, const double *mean,
                          const double *std, double *rows)
 {
     if (frames == NULL || mean == NULL || std == NULL || rows == NULL)
         return OR_ERR_NULL;
-    int st = check_item(n_src, h, w, indices, n_idx, h, w);
+    int st = check_item(n_src, h, w, indices, n_idx, h, w, patch);
     if (st != OR_OK)
         return st;
     int32_t *padded = malloc(sizeof(int32_t) * (size_t)(n_idx + 1));
     if (!padded)
         return OR_ERR_NOMEM;
     pad_indices(indices, n_idx, padded);
-    int64_t hg = h / OR_PATCH, wg = w / OR_PATCH;
+    int64_t hg = h / patch, wg = w / patch;
     int64_t frame_bytes = h * w * 3;
-    int64_t n_rows = oracle_item_rows(n_idx, h, w);
+    int64_t n_rows = oracle_item_rows(n_idx, h, w, patch);
     for (int64_t rho = 0; rho < n_rows; rho++) {
         int64_t tt, i0, j0;
-        decode_row(rho, hg, wg, &tt, &i0, &j0);
-        for (int64_t k = 0; k < OR_ROW; k++) {
+        decode_row(rho, hg, wg, patch, &tt, &i0, &j0);
+        for (int64_t k = 0; k < OR_ROW(patch); k++) {
             int64_t c, dt, y, x;
-            decode_col(k, &c, &dt, &y, &x);
+            decode_col(k, patch, &c, &dt, &y, &x);
             const uint8_t *f = frames + (int64_t)padded[2 * tt + dt] * frame_bytes;
             double r = (double)f[((i0 + y) * w + (j0 + x)) * 3 + c];
-            rows[rho * OR_ROW + k] = oracle_normalize(r, mean[c], std[c]);
+            rows[rho * OR_ROW(patch) + k] = oracle_normalize(r, mean[c], std[c]);
         }
     }
     free(padded);
@@ -678,27 +682,27 @@ int oracle_patchify_item(const uint8_t *frames, int64_t n_src, int64_t h, int64_
  * check sampled rows of workloads too large to recompute whole.
  */
 int oracle_item_row(const uint8_t *frames, int64_t n_src, int64_t H, int64_t W,
-                    const int32_t *indices, int64_t n_idx, int64_t h, int64_t w,
+                    const int32_t *indices, int64_t n_idx, int64_t h, int64_t w, int64_t patch,
                     const double *mean, const double *std, int64_t rho, double *row)
 {
     if (frames == NULL || mean == NULL || std == NULL || row == NULL)
         return OR_ERR_NULL;
-    int st = check_item(n_src, H, W, indices, n_idx, h, w);
+    int st = check_item(n_src, H, W, indices, n_idx, h, w, patch);
     if (st != OR_OK)
         return st;
-    if (rho < 0 || rho >= oracle_item_rows(n_idx, h, w))
+    if (rho < 0 || rho >= oracle_item_rows(n_idx, h, w, patch))
         return OR_ERR_ARG;
     int32_t *padded = malloc(sizeof(int32_t) * (size_t)(n_idx + 1));
     if (!padded)
         return OR_ERR_NOMEM;
     pad_indices(indices, n_idx, padded);
-    int64_t hg = h / OR_PATCH, wg = w / OR_PATCH;
+    int64_t hg = h / patch, wg = w / patch;
     int64_t tt, i0, j0;
-    decode_row(rho, hg, wg, &tt, &i0, &j0);
+    decode_row(rho, hg, wg, patch, &tt, &i0, &j0);
     int64_t frame_bytes = H * W * 3;
-    for (int64_t k = 0; k < OR_ROW; k++) {
+    for (int64_t k = 0; k < OR_ROW(patch); k++) {
         int64_t c, dt, y, x;
-        decode_col(k, &c, &dt, &y, &x);
+        decode_col(k, patch, &c, &dt, &y, &x);
         const uint8_t *f = frames + (int64_t)padded[2 * tt + dt] * frame_bytes;
         double r = oracle_resize_pixel(f, H, W, h, w, i0 + y, j0 + x, c);
         row[k] = oracle_normalize(r, mean[c], std[c]);
@@ -719,39 +723,42 @@ int oracle_item_row(const uint8_t *frames, int64_t n_src, int64_t H, int64_t W,
  * and for every merge window g = rho / 4 (one token after the 2x2 merge):
  *   llm_pos[g] = (tt, bh, bw).
  * The ViT attends within one frame pair of one item at a time:
- *   vit_cu[0] = 0, vit_cu[s+1] = vit_cu[s] + (h/16)*(w/16) for every frame
+ *   vit_cu[0] = 0, vit_cu[s+1] = vit_cu[s] + (h/P)*(w/P) for every frame
  *   pair s of every item in order; returns the number of pairs in *n_slices.
  * Reading: these are the grid coordinates a 2D RoPE (ViT) and a 3-axis
  * M-RoPE (LLM) take; the model's own temporal scaling and text offset are
  * applied by the model, not here.
  */
 int oracle_position_ids(int64_t n_items, const int64_t *n_idx, const int64_t *h, const int64_t *w,
-                        int64_t *vit_pos, int64_t *llm_pos, int64_t *vit_cu, int64_t *n_slices)
+                        int64_t patch, int64_t *vit_pos, int64_t *llm_pos, int64_t *vit_cu,
+                        int64_t *n_slices)
 {
     if (n_idx == NULL || h == NULL || w == NULL || vit_pos == NULL || llm_pos == NULL ||
         vit_cu == NULL || n_slices == NULL)
         return OR_ERR_NULL;
+    if (patch < 1)
+        return OR_ERR_ARG;
     int64_t row = 0, slice = 0;
     vit_cu[0] = 0;
     for (int64_t b = 0; b < n_items; b++) {
         if (n_idx[b] < 1)
             return OR_ERR_FRAMES;
-        if (h[b] < 32 || w[b] < 32 || h[b] % 32 != 0 || w[b] % 32 != 0)
+        if (h[b] < 2 * patch || w[b] < 2 * patch || h[b] % (2 * patch) != 0 || w[b] % (2 * patch) != 0)
             return OR_ERR_DIMS;
-        int64_t hg = h[b] / OR_PATCH, wg = w[b] / OR_PATCH;
-        int64_t n_rows = oracle_item_rows(n_idx[b], h[b], w[b]);
+        int64_t hg = h[b] / patch, wg = w[b] / patch;
+        int64_t n_rows = oracle_item_rows(n_idx[b], h[b], w[b], patch);
         for (int64_t r = 0; r < n_rows; r++) {
             int64_t tt, i0, j0;
-            decode_row(r, hg, wg, &tt, &i0, &j0);
+            decode_row(r, hg, wg, patch, &tt, &i0, &j0);
             int64_t *v = vit_pos + 3 * (row + r);
             v[0] = tt;
-            v[1] = i0 / OR_PATCH;
-            v[2] = j0 / OR_PATCH;
+            v[1] = i0 / patch;
+            v[2] = j0 / patch;
             if (r % 4 == 0) {
                 int64_t *l = llm_pos + 3 * ((row + r) / 4);
                 l[0] = tt;
-                l[1] = i0 / (OR_PATCH * OR_MERGE);
-                l[2] = j0 / (OR_PATCH * OR_MERGE);
+                l[1] = i0 / (patch * OR_MERGE);
+                l[2] = j0 / (patch * OR_MERGE);
             }
         }
         int64_t t = (n_idx[b] + 1) / 2;
@@ -771,25 +778,27 @@ int oracle_position_ids(int64_t n_items, const int64_t *n_idx, const int64_t *h,
 /* ------------------------------------------------------------------------ */
 
 /*
- * grid_thw[b] = (t, h/16, w/16) with t = ceil(n_idx / 2);
- * cu[0] = 0, cu[b+1] = cu[b] + t * (h/16) * (w/16).
+ * grid_thw[b] = (t, h/P, w/P) with t = ceil(n_idx / 2);
+ * cu[0] = 0, cu[b+1] = cu[b] + t * (h/P) * (w/P).
  */
 int oracle_layout(int64_t n_items, const int64_t *n_idx, const int64_t *h, const int64_t *w,
-                  int64_t *grid_thw, int64_t *cu)
+                  int64_t patch, int64_t *grid_thw, int64_t *cu)
 {
     if (n_idx == NULL || h == NULL || w == NULL || grid_thw == NULL || cu == NULL)
         return OR_ERR_NULL;
+    if (patch < 1)
+        return OR_ERR_ARG;
     cu[0] = 0;
     for (int64_t b = 0; b < n_items; b++) {
         if (n_idx[b] < 1)
             return OR_ERR_FRAMES;
-        if (h[b] < 1 || w[b] < 1 || h[b] % 32 != 0 || w[b] % 32 != 0)
+        if (h[b] < 1 || w[b] < 1 || h[b] % (2 * patch) != 0 || w[b] % (2 * patch) != 0)
             return OR_ERR_DIMS;
         int64_t t = (n_idx[b] + 1) / 2;
         grid_thw[3 * b + 0] = t;
-        grid_thw[3 * b + 1] = h[b] / OR_PATCH;
-        grid_thw[3 * b + 2] = w[b] / OR_PATCH;
-        cu[b + 1] = cu[b] + t * (h[b] / OR_PATCH) * (w[b] / OR_PATCH);
+        grid_thw[3 * b + 1] = h[b] / patch;
+        grid_thw[3 * b + 2] = w[b] / patch;
+        cu[b + 1] = cu[b] + t * (h[b] / patch) * (w[b] / patch);
     }
     return OR_OK;
 }

@@ -664,3 +664,65 @@ def test_position_ids_by_reshape_and_ragged_segments():
     assert cu.tolist() == [0, 8, 16, 40, 60, 80]
     _, ocu = oracle.layout(n_idx, hs, ws)
     assert cu[-1] == ocu[-1] == len(vit)
+
+
+# -- Qwen2/2.5-VL geometry: patch 14, merge windows of 28, rows of 1176 -----
+
+def test_smart_resize_factor_28_worked_values():
+    # 720x1280 under 262,144 px: beta = sqrt(921600/262144) = 1.875,
+    # floor(720/1.875/28) = 13, floor(1280/1.875/28) = 24
+    assert oracle.smart_resize(720, 1280, 28, 0, 262144) == (364, 672)
+    # 480x854 under 230,400 px: rhe(854/28 = 30.5) = 30 first, then the
+    # budget branch: floor(12.85) = 12, floor(22.87) = 22
+    assert oracle.smart_resize(480, 854, 28, 0, 230400) == (336, 616)
+    assert oracle.smart_resize(1024, 1024, 28, 0, 1003520) == (980, 980)
+    h, w = oracle.smart_resize(333, 257, 28, 65536, 1003520)
+    assert h % 28 == 0 and w % 28 == 0
+
+
+def test_patch14_inverse_by_reshape_full_and_patchify_paths():
+    rng = np.random.default_rng(61)
+    n, H, W = 3, 56, 84
+    f = rng.integers(0, 256, size=(n, H, W, 3), dtype=np.uint8)
+    mean, std = (0.48, 0.46, 0.41), (0.27, 0.26, 0.28)
+    idx = [2, 0, 1]                                           # padded with 1
+    ref = (f[[2, 0, 1, 1]].transpose(0, 3, 1, 2) / 255.0 - np.array(mean)[None, :, None, None]) \
+        / np.array(std)[None, :, None, None]
+    for rows in (oracle.patchify_item(f, idx, mean, std, patch=14),
+                 oracle.preprocess_item(f, idx, H, W, mean, std, patch=14)):
+        t, hm, wm = 2, H // 28, W // 28
+        assert rows.shape == (t * hm * wm * 4, 1176)
+        v = rows.reshape(t, hm, wm, 2, 2, 3, 2, 14, 14).transpose(0, 6, 5, 1, 3, 7, 2, 4, 8)
+        np.testing.assert_allclose(v.reshape(2 * t, 3, H, W), ref, rtol=0, atol=1e-12)
+
+
+def test_patch14_row_and_column_order():
+    H, W = 28, 84
+    vals = np.zeros((2, 3, H, W), np.int64)
+    ii, jj = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    vals[:, 0] = 10 * (ii // 14) + (jj // 14)
+    for fr in range(2):
+        vals[fr, 1] = 50 + 10 * fr
+        vals[fr, 2] = 14 * (ii % 14) + (jj % 14)
+    f = _identity_item(vals)
+    rows = oracle.patchify_item(f, [0, 1], (0.0,) * 3, (1 / 255,) * 3, patch=14)
+    assert rows.shape == (12, 1176)
+    assert np.rint(rows[:, :196].mean(1)).astype(int).tolist() == [0, 1, 10, 11, 2, 3, 12, 13, 4, 5, 14, 15]
+    assert np.allclose(rows[:, 392:588], 50) and np.allclose(rows[:, 588:784], 60)
+    assert np.allclose(rows[:, 784:980], np.arange(196)[None, :])
+
+
+def test_patch14_layout_and_positions():
+    g, cu = oracle.layout([8, 1], [364, 980], [672, 980], patch=14)
+    assert g.tolist() == [[4, 26, 48], [1, 70, 70]]
+    assert cu.tolist() == [0, 4 * 26 * 48, 4 * 26 * 48 + 4900]
+    assert oracle.item_rows(256, 252, 448, 14) == 128 * 18 * 32
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.layout([2], [64], [64], patch=14)              # not a multiple of 28
+    assert e.value.code == oracle.ERR_DIMS
+    vit, llm, vcu = oracle.position_ids([3], [56], [84], patch=14)
+    t, hm, wm = 2, 2, 3
+    tt, bh, bw, mh, mw = np.meshgrid(np.arange(t), np.arange(hm), np.arange(wm), np.arange(2),
+                                     np.arange(2), indexing="ij")
+    assert np.array_equal(vit, np.stack([tt, 2 * bh + mh, 2 * bw + mw], -1).reshape(-1, 3))
+    assert vcu.tolist() == [0, 24, 48]
