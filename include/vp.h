@@ -5,13 +5,15 @@
  * Qwen-VL-style vision input that EasyVideoR1 (arXiv 2604.16893) caches
  * offline so that it leaves the RL loop (Section 3.1.1, "Efficient RL with
  * Video Caching"): temporal frame-index sampling, smart_resize to multiples
- * of 32 under a per-modality pixel budget (Section 3.1.2, "Independent
+ * of 2P under a per-modality pixel budget (Section 3.1.2, "Independent
  * Resolution Budgets"; Section 4.1, "Training Configuration"), separable
  * antialiased bicubic resampling of decoded uint8 RGB frames, rescale by
  * 1/255 and per-channel mean/std normalisation (Section 1 names sampling,
  * resizing and normalisation as the costly steps), and patchification into
- * merge-window rows of 3 * 2 * 16 * 16 = 1536 values with the per-item grid
- * (t, h/16, w/16) -- the video_grid_thw that every stage must reproduce
+ * merge-window rows of 3 * 2 * P * P values -- P = 16 for Qwen3-VL (1536
+ * values), P = 14 for Qwen2-VL and Qwen2.5-VL (1176), the families the
+ * paper supports (Section 4.1) -- with the per-item grid (t, h/P, w/P) --
+ * the video_grid_thw that every stage must reproduce
  * identically (Section 3.1.1) -- and a row-offset table for ragged mixed
  * image/video batches (Section 3.2.2, "Joint Image-Video Training").
  *
@@ -47,18 +49,20 @@ extern "C" {
 #define VP_ERR_NULL 1       /* a required pointer is NULL                         */
 #define VP_ERR_ARG 2        /* an argument is out of its documented range         */
 #define VP_ERR_ASPECT 3     /* smart_resize: longer/shorter side ratio above 200  */
-#define VP_ERR_DIMS 4       /* a size is non-positive or not a multiple of 32     */
+#define VP_ERR_DIMS 4       /* a size is non-positive or not a multiple of 2P     */
 #define VP_ERR_INDEX 5      /* a frame index lies outside [0, n_src)              */
 #define VP_ERR_FRAMES 6     /* a frame count is impossible (n < 1, n > N, ...)    */
 #define VP_ERR_CAPACITY 7   /* an output or workspace buffer is too small         */
 #define VP_ERR_HIP 8        /* a HIP runtime call failed (detail in the message)  */
 
-/* Geometry: patch 16, spatial merge 2, temporal patch 2. */
+/* Geometry: patch P = 16 by default (vp_item.patch selects 14), spatial
+ * merge 2, temporal patch 2. */
 #define VP_PATCH 16
+#define VP_PATCH_QWEN2 14
 #define VP_MERGE 2
 #define VP_TEMPORAL_PATCH 2
-#define VP_FACTOR 32        /* VP_PATCH * VP_MERGE */
-#define VP_ROW 1536         /* 3 * VP_TEMPORAL_PATCH * VP_PATCH * VP_PATCH */
+#define VP_FACTOR 32        /* VP_PATCH * VP_MERGE (28 for patch 14) */
+#define VP_ROW 1536         /* 3 * VP_TEMPORAL_PATCH * VP_PATCH * VP_PATCH (1176 for patch 14) */
 
 /* Frame-index sampling modes. */
 #define VP_SAMPLE_UNIFORM 0
@@ -72,9 +76,9 @@ extern "C" {
  * smart_resize (Section 3.1.1: resize under max_pixels; Section 3.1.2:
  * separate image / video budgets; Section 4.1: a per-frame budget).
  *
- * Target size (out_h, out_w), both positive multiples of `factor` (32 for
- * this geometry), for a height x width source under the per-frame budget
- * [min_pixels, max_pixels]:
+ * Target size (out_h, out_w), both positive multiples of `factor` (2P: 32
+ * for patch 16, 28 for patch 14), for a height x width source under the
+ * per-frame budget [min_pixels, max_pixels]:
  *   h = max(F, rhe(H/F)*F), w = max(F, rhe(W/F)*F)   (rhe: round half to even);
  *   if h*w > max_pixels: beta = sqrt(H*W/max_pixels),
  *       h = max(F, floor(H/beta/F)*F), w = max(F, floor(W/beta/F)*F);
@@ -154,14 +158,20 @@ typedef struct vp_item {
     int32_t n_src;           /* decoded frames available, >= 1                          */
     int32_t src_h, src_w;    /* source size, >= 1                                       */
     int32_t n_idx;           /* sampled frames, >= 1                                    */
-    int32_t dst_h, dst_w;    /* target size, positive multiples of 32
-                                (for instance from vp_smart_resize_dims)            */
+    int32_t dst_h, dst_w;    /* target size, positive multiples of 2 * patch
+                                (for instance from vp_smart_resize_dims with
+                                factor 2 * patch)                                  */
+    int32_t patch;           /* patch edge P in pixels: 16 (Qwen3-VL; 0 also means
+                                16) or 14 (Qwen2-VL, Qwen2.5-VL).  All items of
+                                one call share it; rows hold 3 * 2 * P * P values
+                                (1536 or 1176)                                     */
 } vp_item;
 
 /*
  * Batch layout (Section 3.1.1: identical video_grid_thw in every stage).
- * grid_thw: HOST int32[n_items][3] = (t, dst_h/16, dst_w/16), t = ceil(n_idx/2).
- * cu_seqlens: HOST int32[n_items + 1], cu[0] = 0, cu[b+1] = cu[b] + t*(h/16)*(w/16);
+ * With P the items' patch size:
+ * grid_thw: HOST int32[n_items][3] = (t, dst_h/P, dst_w/P), t = ceil(n_idx/2).
+ * cu_seqlens: HOST int32[n_items + 1], cu[0] = 0, cu[b+1] = cu[b] + t*(h/P)*(w/P);
  *   item b owns output rows [cu[b], cu[b+1]).
  * total_rows: HOST, = cu[n_items].
  * workspace_bytes: HOST, the device workspace vp_preprocess_batch needs.
@@ -179,14 +189,14 @@ int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw
  * resampled from (src_h, src_w) to (dst_h, dst_w) with the filter of
  * vp_filter_table along x then y (no clamping, no rounding in between),
  * normalised as v = (R/255 - mean_c)/std_c, padded to an even frame count,
- * and written as merge-window rows:
- *   row cu[b] + ((tt*(h/32) + bh)*(w/32) + bw)*4 + mh*2 + mw,
- *   column ((c*2 + dt)*16 + y)*16 + x  holds
- *   v[frame 2*tt + dt][c][16*(2*bh + mh) + y][16*(2*bw + mw) + x].
+ * and written as merge-window rows of 6*P*P values (P the patch size):
+ *   row cu[b] + ((tt*(h/2P) + bh)*(w/2P) + bw)*4 + mh*2 + mw,
+ *   column ((c*2 + dt)*P + y)*P + x  holds
+ *   v[frame 2*tt + dt][c][P*(2*bh + mh) + y][P*(2*bw + mw) + x].
  *
  * mean, std: HOST float[3] (std > 0, finite).
  * out_dtype: VP_OUT_F32 or VP_OUT_BF16 (round to nearest even).
- * out_rows: DEVICE [out_rows_capacity][1536] of out_dtype, row-major,
+ * out_rows: DEVICE [out_rows_capacity][6*P*P] of out_dtype, row-major,
  *   16-byte aligned.
  * grid_thw, cu_seqlens: HOST outputs as in vp_batch_layout (may be NULL);
  *   final when the call returns.
@@ -201,7 +211,8 @@ int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw
  *   events: to other work on `stream` the call is one ordered step.
  * out_rows is final when `stream` reaches the end of the enqueued work.
  * Errors: VP_ERR_NULL, VP_ERR_ARG (n_items < 1, bad dtype, std <= 0 or not
- * finite, misaligned pointers), VP_ERR_DIMS, VP_ERR_FRAMES, VP_ERR_INDEX,
+ * finite, misaligned pointers, a patch size other than 14 or 16, items with
+ * different patch sizes), VP_ERR_DIMS, VP_ERR_FRAMES, VP_ERR_INDEX,
  * VP_ERR_CAPACITY (out_rows_capacity < total rows, workspace too small, a
  * frame of 4 GiB or more, a filter window too long for the kernels),
  * VP_ERR_HIP.
@@ -216,12 +227,12 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
  * cached path of Section 3.1.1, where sampling and resizing were done once
  * offline and every RL stage still rescales, normalises and patchifies.
  * Items as for vp_preprocess_batch, with dst_h == src_h and dst_w == src_w
- * (multiples of 32); `indices` select and order the frames as before, odd
+ * (multiples of 2P); `indices` select and order the frames as before, odd
  * counts padded with the last index.  The rows are those vp_preprocess_batch
  * writes for the same items, whose resize is then the identity:
- *   row cu[b] + ((tt*(h/32) + bh)*(w/32) + bw)*4 + mh*2 + mw,
- *   column ((c*2 + dt)*16 + y)*16 + x  holds (F/255 - mean_c)/std_c of
- *   F = frames[indices[2*tt + dt]][16*(2*bh + mh) + y][16*(2*bw + mw) + x][c].
+ *   row cu[b] + ((tt*(h/2P) + bh)*(w/2P) + bw)*4 + mh*2 + mw,
+ *   column ((c*2 + dt)*P + y)*P + x  holds (F/255 - mean_c)/std_c of
+ *   F = frames[indices[2*tt + dt]][P*(2*bh + mh) + y][P*(2*bw + mw) + x][c].
  * Arguments, ownership, asynchrony and stream as for vp_preprocess_batch;
  * the workspace_bytes of vp_batch_layout on the same items suffice.  Each
  * frames pointer must be 4-byte aligned.
@@ -278,14 +289,14 @@ int32_t vp_resize_batch(const vp_item* items, int32_t n_items, void* out_frames,
  * spatial-temporal positional encoding; Section 3.1.1: the same
  * video_grid_thw in every stage).  Items and their rows as in
  * vp_batch_layout / vp_preprocess_batch (item b owns rows [cu[b], cu[b+1]),
- * row cu[b] + ((tt*(h/32) + bh)*(w/32) + bw)*4 + mh*2 + mw):
+ * row cu[b] + ((tt*(h/2P) + bh)*(w/2P) + bw)*4 + mh*2 + mw):
  *   vit_pos[row] = (tt, 2*bh + mh, 2*bw + mw)  frame pair, patch row, patch column
  *     -- the coordinates of the ViT's 2D rotary embedding;
  *   llm_pos[row/4] = (tt, bh, bw)  one per merge window, the token it becomes
  *     after the 2x2 merge -- the grid coordinates of the LLM's 3-axis M-RoPE
  *     (the model adds its own temporal scaling and text offset);
  *   vit_cu: the ViT's attention segments, one per frame pair of each item:
- *     vit_cu[0] = 0, vit_cu[s+1] = vit_cu[s] + (h/16)*(w/16).
+ *     vit_cu[0] = 0, vit_cu[s+1] = vit_cu[s] + (h/P)*(w/P).
  * vit_pos: DEVICE int32 [rows][3], llm_pos: DEVICE int32 [rows/4][3]; either
  *   may be NULL; rows_capacity = rows the caller's vit_pos holds (llm_pos
  *   holds rows_capacity/4); 4-byte aligned.

@@ -28,6 +28,13 @@ VP_OK, VP_ERR_NULL, VP_ERR_ARG, VP_ERR_ASPECT, VP_ERR_DIMS, VP_ERR_INDEX, VP_ERR
 VP_SAMPLE_UNIFORM, VP_SAMPLE_FPS = 0, 1
 VP_OUT_F32, VP_OUT_BF16 = 0, 1
 VP_ROW = 1536
+VP_PATCH = 16
+
+
+def row_width(patch: int = VP_PATCH) -> int:
+    """Values per merge-window row: 3 channels x 2 frames x patch x patch
+    (1536 for patch 16, 1176 for patch 14)."""
+    return 6 * patch * patch
 VP_FACTOR = 32
 
 EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
@@ -50,7 +57,8 @@ class vp_item(ctypes.Structure):
                 ("src_w", ctypes.c_int32),
                 ("n_idx", ctypes.c_int32),
                 ("dst_h", ctypes.c_int32),
-                ("dst_w", ctypes.c_int32)]
+                ("dst_w", ctypes.c_int32),
+                ("patch", ctypes.c_int32)]
 
 
 _lib = None
@@ -170,11 +178,13 @@ def vp_filter_table_fixed(n_in: int, n_out: int, taps: Optional[int] = None):
 @dataclasses.dataclass
 class Item:
     """One video or image: device frames [n_src, H, W, 3] uint8, sampled
-    indices, and the target size (multiples of 32)."""
+    indices, the target size (multiples of 2 * patch) and the patch size
+    (16, or 14 for the Qwen2/2.5-VL geometry; one per call)."""
     frames: object
     indices: Sequence[int]
     dst_h: int
     dst_w: int
+    patch: int = VP_PATCH
 
 
 class _Batch:
@@ -196,7 +206,7 @@ class _Batch:
             idx = np.ascontiguousarray(np.asarray(it.indices, dtype=np.int32).reshape(-1))
             self.idx.append(idx)
             self.arr[k] = vp_item(ptr, _ptr(idx, ctypes.c_int32), n_src, H, W, len(idx),
-                                  it.dst_h, it.dst_w)
+                                  it.dst_h, it.dst_w, getattr(it, "patch", VP_PATCH))
 
     def __len__(self):
         return len(self.arr)
@@ -242,9 +252,10 @@ def vp_patchify_batch(items: Sequence, mean, std, out_dtype: int, out_rows, work
 def _run(name: str, items: Sequence, mean, std, out_dtype: int, out_rows, workspace, stream):
     import torch
     want = torch.bfloat16 if out_dtype == VP_OUT_BF16 else torch.float32
-    if out_rows.dtype != want or out_rows.dim() != 2 or out_rows.shape[1] != VP_ROW \
+    width = row_width(getattr(items[0], "patch", VP_PATCH)) if len(items) else VP_ROW
+    if out_rows.dtype != want or out_rows.dim() != 2 or out_rows.shape[1] != width \
             or not out_rows.is_contiguous() or not out_rows.is_cuda:
-        raise VPError(VP_ERR_ARG, f"out_rows must be a contiguous CUDA [rows, {VP_ROW}] {want} tensor")
+        raise VPError(VP_ERR_ARG, f"out_rows must be a contiguous CUDA [rows, {width}] {want} tensor")
     if not workspace.is_cuda or not workspace.is_contiguous():
         raise VPError(VP_ERR_ARG, "workspace must be a contiguous CUDA tensor")
     b = _Batch(items)
@@ -290,7 +301,8 @@ def patchify(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None):
     code = VP_OUT_BF16 if out_dtype in ("bf16", VP_OUT_BF16) else VP_OUT_F32
     grid, cu, rows, ws = vp_batch_layout(items)
     dev = items[0].frames.device
-    out = torch.empty((rows, VP_ROW), dtype=torch.bfloat16 if code == VP_OUT_BF16 else torch.float32,
+    out = torch.empty((rows, row_width(getattr(items[0], "patch", VP_PATCH))),
+                      dtype=torch.bfloat16 if code == VP_OUT_BF16 else torch.float32,
                       device=dev)
     work = torch.empty(ws, dtype=torch.uint8, device=dev)
     vp_patchify_batch(items, mean, std, code, out, work, stream)
@@ -376,7 +388,8 @@ def preprocess(items: Sequence, mean, std, out_dtype: str = "bf16", stream=None)
     code = VP_OUT_BF16 if out_dtype in ("bf16", VP_OUT_BF16) else VP_OUT_F32
     grid, cu, rows, ws = vp_batch_layout(items)
     dev = items[0].frames.device
-    out = torch.empty((rows, VP_ROW), dtype=torch.bfloat16 if code == VP_OUT_BF16 else torch.float32,
+    out = torch.empty((rows, row_width(getattr(items[0], "patch", VP_PATCH))),
+                      dtype=torch.bfloat16 if code == VP_OUT_BF16 else torch.float32,
                       device=dev)
     work = torch.empty(ws, dtype=torch.uint8, device=dev)
     vp_preprocess_batch(items, mean, std, code, out, work, stream)

@@ -162,6 +162,21 @@ struct Plan {
            bytes = 0;
 };
 
+int32_t item_patch(const vp_item& it) { return it.patch == 0 ? vp::kPatch : it.patch; }
+
+// Every item of one call must share one patch size (the rows of one output
+// buffer have one width).
+int32_t batch_patch(const vp_item* items, int32_t n, int32_t* patch) {
+    *patch = vp::kPatch;
+    if (items == nullptr || n < 1) return VP_OK;   // reported by the caller's own checks
+    *patch = item_patch(items[0]);
+    for (int32_t b = 1; b < n; ++b)
+        if (item_patch(items[b]) != *patch)
+            return fail(VP_ERR_ARG, "items of one call must share one patch size (item " +
+                                        std::to_string(b) + ")");
+    return VP_OK;
+}
+
 int32_t validate_item(const vp_item& it, int32_t b) {
     const std::string at = "item " + std::to_string(b) + ": ";
     if (it.frames == nullptr) return fail(VP_ERR_NULL, at + "frames is NULL");
@@ -169,8 +184,11 @@ int32_t validate_item(const vp_item& it, int32_t b) {
     if (it.n_src < 1) return fail(VP_ERR_FRAMES, at + "n_src < 1");
     if (it.src_h < 1 || it.src_w < 1) return fail(VP_ERR_DIMS, at + "source size < 1");
     if (it.n_idx < 1) return fail(VP_ERR_FRAMES, at + "n_idx < 1");
-    if (it.dst_h < vp::kWin || it.dst_w < vp::kWin || it.dst_h % vp::kWin || it.dst_w % vp::kWin)
-        return fail(VP_ERR_DIMS, at + "target size not a positive multiple of 32");
+    if (it.patch != 0 && it.patch != 14 && it.patch != 16)
+        return fail(VP_ERR_ARG, at + "patch must be 14 or 16 (0 for 16)");
+    const int32_t win = 2 * item_patch(it);
+    if (it.dst_h < win || it.dst_w < win || it.dst_h % win || it.dst_w % win)
+        return fail(VP_ERR_DIMS, at + "target size not a positive multiple of " + std::to_string(win));
     for (int32_t k = 0; k < it.n_idx; ++k)
         if (it.indices[k] < 0 || it.indices[k] >= it.n_src)
             return fail(VP_ERR_INDEX, at + "index " + std::to_string(it.indices[k]) +
@@ -182,9 +200,12 @@ int32_t validate_item(const vp_item& it, int32_t b) {
 
 // Largest generic sub-tile (rh x cw output pixels) whose y-resampled column
 // tile fits the kernel's LDS buffer for every merge window of the item.
-bool generic_subtile(const AxisFilter& fx, int32_t* rh, int32_t* cw) {
-    for (int32_t r = 32; r >= 1; r /= 2) {
-        for (int32_t c = 32; c >= 1; c /= 2) {
+bool generic_subtile(const AxisFilter& fx, int32_t win, int32_t* rh, int32_t* cw) {
+    std::vector<int32_t> sizes;   // the divisors of the window edge, largest first
+    for (int32_t d = win; d >= 1; --d)
+        if (win % d == 0) sizes.push_back(d);
+    for (int32_t r : sizes) {
+        for (int32_t c : sizes) {
             int32_t worst = 0;
             for (int32_t j0 = 0; j0 < fx.n_out; j0 += c) {
                 const int32_t span = fx.start[j0 + c - 1] + fx.count[j0 + c - 1] - fx.start[j0];
@@ -385,6 +406,8 @@ std::shared_ptr<const AxisEntry> make_axis_entry(int32_t n_in, int32_t n_out) {
 int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    int32_t P = vp::kPatch;
+    if (const int32_t st = batch_patch(items, n, &P); st != VP_OK) return st;
     p->items.assign(n, vp::DevItem{});
     p->generic_cost = 0;
     p->prefix.assign(n + 1, 0);
@@ -460,8 +483,9 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         d.h = it.dst_h;
         d.w = it.dst_w;
         d.t = (it.n_idx + 1) / 2;
-        d.hm = it.dst_h / vp::kWin;
-        d.wm = it.dst_w / vp::kWin;
+        d.patch = P;
+        d.hm = it.dst_h / (2 * P);
+        d.wm = it.dst_w / (2 * P);
         d.idx_off = static_cast<int32_t>(p->indices.size());
         for (int32_t k = 0; k < 2 * d.t; ++k)
             p->indices.push_back(it.indices[k < it.n_idx ? k : it.n_idx - 1]);
@@ -472,21 +496,21 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         d.route = vp::kRouteGeneric;
         int32_t m = 0;
         StreamShape sh;
-        if (slots_for(*fy, &d.sy_off, &m) && stream_shape(it, *fx, m, &sh)) {
+        if (P == vp::kPatch && slots_for(*fy, &d.sy_off, &m) && stream_shape(it, *fx, m, &sh)) {
             d.route = vp::kRouteStream;
             d.band = sh.band;
             d.row_px = 64 * sh.px;
             d.sx_off = columns_for(*fx, sh.kx, sh.band, d.row_px);
             shapes[b] = sh;
-        } else if (!generic_subtile(*fx, &d.rh, &d.cw)) {
+        } else if (!generic_subtile(*fx, 2 * P, &d.rh, &d.cw)) {
             return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
                                              ": horizontal filter window too long (downscale too large)");
         }
         d.row_off = rows;
-        const int64_t item_rows = int64_t(d.t) * (it.dst_h / vp::kPatch) * (it.dst_w / vp::kPatch);
+        const int64_t item_rows = int64_t(d.t) * (it.dst_h / P) * (it.dst_w / P);
         p->grid[3 * b + 0] = d.t;
-        p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
-        p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
+        p->grid[3 * b + 1] = it.dst_h / P;
+        p->grid[3 * b + 2] = it.dst_w / P;
         rows += item_rows;
         if (d.route == vp::kRouteGeneric) {
             tiles += int64_t(d.t) * d.hm * d.wm;
@@ -632,6 +656,8 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
 int32_t build_patch_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    int32_t P = vp::kPatch;
+    if (const int32_t st = batch_patch(items, n, &P); st != VP_OK) return st;
     p->items.assign(n, vp::DevItem{});
     p->prefix.assign(n + 1, 0);
     p->grid.assign(size_t(n) * 3, 0);
@@ -659,17 +685,18 @@ int32_t build_patch_plan(const vp_item* items, int32_t n, Plan* p) {
         d.H = d.h = it.dst_h;
         d.W = d.w = it.dst_w;
         d.t = (it.n_idx + 1) / 2;
-        d.hm = it.dst_h / vp::kWin;
-        d.wm = it.dst_w / vp::kWin;
+        d.patch = P;
+        d.hm = it.dst_h / (2 * P);
+        d.wm = it.dst_w / (2 * P);
         d.idx_off = static_cast<int32_t>(p->indices.size());
         for (int32_t k = 0; k < 2 * d.t; ++k)
             p->indices.push_back(it.indices[k < it.n_idx ? k : it.n_idx - 1]);
         d.route = vp::kRoutePatch;
         d.row_off = rows;
         p->grid[3 * b + 0] = d.t;
-        p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
-        p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
-        rows += int64_t(d.t) * (it.dst_h / vp::kPatch) * (it.dst_w / vp::kPatch);
+        p->grid[3 * b + 1] = it.dst_h / P;
+        p->grid[3 * b + 2] = it.dst_w / P;
+        rows += int64_t(d.t) * (it.dst_h / P) * (it.dst_w / P);
         tiles += int64_t(d.t) * d.hm;
         if (rows > INT32_MAX || tiles > INT32_MAX)
             return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 rows");
@@ -692,6 +719,8 @@ int32_t build_patch_plan(const vp_item* items, int32_t n, Plan* p) {
 int32_t build_rows_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    int32_t P = vp::kPatch;
+    if (const int32_t st = batch_patch(items, n, &P); st != VP_OK) return st;
     p->items.assign(n, vp::DevItem{});
     p->grid.assign(size_t(n) * 3, 0);
     p->cu.assign(n + 1, 0);
@@ -711,13 +740,14 @@ int32_t build_rows_plan(const vp_item* items, int32_t n, Plan* p) {
         d.h = it.dst_h;
         d.w = it.dst_w;
         d.t = (it.n_idx + 1) / 2;
-        d.hm = it.dst_h / vp::kWin;
-        d.wm = it.dst_w / vp::kWin;
+        d.patch = P;
+        d.hm = it.dst_h / (2 * P);
+        d.wm = it.dst_w / (2 * P);
         d.row_off = rows;
         p->grid[3 * b + 0] = d.t;
-        p->grid[3 * b + 1] = it.dst_h / vp::kPatch;
-        p->grid[3 * b + 2] = it.dst_w / vp::kPatch;
-        rows += int64_t(d.t) * (it.dst_h / vp::kPatch) * (it.dst_w / vp::kPatch);
+        p->grid[3 * b + 1] = it.dst_h / P;
+        p->grid[3 * b + 2] = it.dst_w / P;
+        rows += int64_t(d.t) * (it.dst_h / P) * (it.dst_w / P);
         if (rows > INT32_MAX) return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 rows");
         p->cu[b + 1] = static_cast<int32_t>(rows);
     }
@@ -768,6 +798,8 @@ bool resize_tiles(const AxisFilter& fy, const AxisFilter& fx, int32_t* rb, int32
 int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
+    int32_t P = vp::kPatch;
+    if (const int32_t st = batch_patch(items, n, &P); st != VP_OK) return st;
     p->items.assign(n, vp::DevItem{});
     p->prefix.assign(n + 1, 0);
     p->byte_off.assign(n + 1, 0);
@@ -819,6 +851,7 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         d.hm = (it.dst_h + d.rh - 1) / d.rh;
         d.wm = (it.dst_w + d.cw - 1) / d.cw;
         d.route = vp::kRouteResize;
+        d.patch = P;
         d.row_off = bytes;   // output byte offset of the item
         bytes += int64_t(it.n_idx) * it.dst_h * it.dst_w * 3;
         tiles += int64_t(it.n_idx) * d.hm * d.wm;
@@ -1080,7 +1113,7 @@ int32_t run_batch(bool patch_only, const vp_item* items, int32_t n_items, const 
     view.n_items = n_items;
     view.n_tiles = p.prefix[n_items];
     if (patch_only) {
-        const int err = vp::launch_patchify(view, out_rows, out_dtype, norm, stream);
+        const int err = vp::launch_patchify(view, out_rows, out_dtype, norm, p.items[0].patch, stream);
         if (err != 0) return hip_fail(static_cast<hipError_t>(err), "patchify kernel launch");
     } else {
         st = run_launches(p, view, out_rows, out_dtype, norm, stream);

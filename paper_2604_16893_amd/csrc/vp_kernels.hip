@@ -75,7 +75,7 @@ template <int OUT_BF16>
 __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView plan, void* out,
                                                                        Norm norm) {
     __shared__ float tcol[kGenericTCap];   // y-resampled columns of one sub-tile, [r][x][c]
-    __shared__ float stage[kWinElems];     // the unit's four output rows, output order
+    __shared__ float stage[kWinElems];     // the unit's four output rows, output order (P <= 16)
 
     const int tile = blockIdx.x;
     const int b = find_item(plan.tile_prefix, plan.n_items, tile);
@@ -94,6 +94,7 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
     const float* wx = reinterpret_cast<const float*>(xn + it.w);
     const int64_t row_stride = int64_t(it.W) * 3;
     const int tid = threadIdx.x;
+    const int P = it.patch, win = 2 * it.patch, row_len = 6 * it.patch * it.patch;
 
     // an image, or an odd count padded with its last index: both temporal
     // halves come from one frame, computed once and staged twice
@@ -101,10 +102,10 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
     for (int dt = 0; dt < (same ? 1 : 2); ++dt) {
         const int f = plan.indices[it.idx_off + 2 * tt + dt];
         const uint8_t* frame = it.frames + int64_t(f) * it.frame_bytes;
-        for (int r0 = 0; r0 < kWin; r0 += it.rh) {
-            for (int c0 = 0; c0 < kWin; c0 += it.cw) {
-                const int i0 = kWin * bh + r0;
-                const int j0 = kWin * bw + c0;
+        for (int r0 = 0; r0 < win; r0 += it.rh) {
+            for (int c0 = 0; c0 < win; c0 += it.cw) {
+                const int i0 = win * bh + r0;
+                const int j0 = win * bw + c0;
                 const int x0 = xs[j0];
                 const int xw = xs[j0 + it.cw - 1] + xn[j0 + it.cw - 1] - x0;
                 const int span = xw * 3;
@@ -133,12 +134,15 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
                     const float* src = tcol + r * span + (xs[j] - x0) * 3 + c;
                     float acc = 0.f;
                     for (int k = 0; k < n; ++k) acc = fmaf(wr[k], src[3 * k], acc);
-                    const float v = fmaf(acc, norm.a[c], norm.b[c]);
+                    // the normalisation every kernel uses, a_c * (R + z_c): at
+                    // identity size R is the pixel itself and the paths agree
+                    // bit for bit
+                    const float v = (acc + norm.z[c]) * norm.a[c];
                     const int il = r0 + r, jl = c0 + cc;
-                    const int sub = (il >> 4) * 2 + (jl >> 4);
-                    float* st = stage + sub * kRow + ((c * 2 + dt) * kPatch + (il & 15)) * kPatch + (jl & 15);
+                    const int sub = (il / P) * 2 + (jl / P);
+                    float* st = stage + sub * row_len + ((c * 2 + dt) * P + il % P) * P + jl % P;
                     st[0] = v;
-                    if (same) st[kPatch * kPatch] = v;   // the second temporal half
+                    if (same) st[P * P] = v;   // the second temporal half
                 }
                 __syncthreads();
             }
@@ -146,9 +150,12 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
     }
 
     const int64_t row0 = it.row_off + ((int64_t(tt) * it.hm + bh) * it.wm + bw) * 4;
+    // the four rows are contiguous: 4 * 6 P^2 values, a multiple of 8, and
+    // they start on a 16-byte boundary (6 P^2 * 2 bytes is one for P = 14, 16)
+    const int win_elems = 4 * row_len;
     if (OUT_BF16) {
-        uint4* dst = reinterpret_cast<uint4*>(static_cast<uint16_t*>(out) + row0 * kRow);
-        for (int e = tid; e < kWinElems / 8; e += kGenericThreads) {
+        uint4* dst = reinterpret_cast<uint4*>(static_cast<uint16_t*>(out) + row0 * row_len);
+        for (int e = tid; e < win_elems / 8; e += kGenericThreads) {
             const float* s = stage + e * 8;
             uint4 v;
             v.x = bf16_rne(s[0]) | (bf16_rne(s[1]) << 16);
@@ -158,8 +165,8 @@ __global__ __launch_bounds__(kGenericThreads) void generic_tile_kernel(PlanView 
             dst[e] = v;
         }
     } else {
-        float4* dst = reinterpret_cast<float4*>(static_cast<float*>(out) + row0 * kRow);
-        for (int e = tid; e < kWinElems / 4; e += kGenericThreads)
+        float4* dst = reinterpret_cast<float4*>(static_cast<float*>(out) + row0 * row_len);
+        for (int e = tid; e < win_elems / 4; e += kGenericThreads)
             dst[e] = reinterpret_cast<const float4*>(stage)[e];
     }
 }
@@ -400,6 +407,79 @@ __global__ __launch_bounds__(256) void patchify_kernel(PlanView plan, void* out,
         }
 #pragma unroll
         for (int k = 0; k < 6; ++k) cur[k] = nxt[k];
+    }
+}
+
+// The same for patches of 14 (Qwen2/2.5-VL geometry: windows of 28, rows of
+// 1176).  Wave (dt, mh) as above; lane l < 56 owns one patch row, P = 14
+// pixels (42 bytes): row y = l % 14 of patch mw = (l / 14) & 1 in window
+// bw = 2 * step + (l / 28).  A patch row can start off a dword boundary, so
+// the lane loads the 12 dwords that cover it from any offset (42 bytes plus
+// up to 3) through a buffer resource (range-checked at the frame's end) and
+// aligns them with v_alignbyte.  Per channel its 14 values are one contiguous run of
+// the output row (4-byte aligned for bf16, 8-byte for float32).
+template <int OUT_BF16>
+__global__ __launch_bounds__(256) void patchify14_kernel(PlanView plan, void* out, Norm norm) {
+    using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
+    constexpr int P = 14;
+    constexpr int kRowLen = 6 * P * P;   // 1176
+    const int tile = blockIdx.x;
+    const int b = find_item(plan.tile_prefix, plan.n_items, tile);
+    const cptr<DevItem> it = as_const(plan.items) + b;
+    const int local = tile - plan.tile_prefix[b];
+    const int hm = it->hm, wm = it->wm, w = it->w;
+    const int bh = local % hm;
+    const int tt = local / hm;
+    const int wv = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const int dt = wv >> 1, mh = wv & 1;
+    if (lane >= 4 * P) return;   // no barrier follows
+    const int y = lane % P, mw = (lane / P) & 1, par = lane / (2 * P);
+    const int f = as_const(plan.indices)[it->idx_off + 2 * tt + dt];
+    const uintptr_t fa = reinterpret_cast<uintptr_t>(it->frames + int64_t(f) * it->frame_bytes);
+    const uint32_t lead = static_cast<uint32_t>(fa & 3u);
+    const uint32_t range = static_cast<uint32_t>((it->frame_bytes + lead + 3) & ~int64_t(3));
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(fa - lead), (short)0, static_cast<int>(range), 0x00020000);
+    const uint32_t row_byte0 = lead + static_cast<uint32_t>((2 * P * bh + P * mh + y) * w) * 3u;
+    const float a[3] = {norm.a[0], norm.a[1], norm.a[2]};
+    const float z[3] = {norm.z[0], norm.z[1], norm.z[2]};
+    const int64_t row_base = it->row_off + (int64_t(tt) * hm + bh) * wm * 4 + mh * 2 + mw;
+
+    for (int bw = par; bw < wm; bw += 2) {
+        const uint32_t o = row_byte0 + static_cast<uint32_t>(2 * P * bw + P * mw) * 3u;
+        const uint32_t sh = o & 3u;
+        uint32_t d[12];
+#pragma unroll
+        for (int k = 0; k < 12; ++k)
+            d[k] = static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (o & ~3u) + 4u * k, 0, 0));
+        uint32_t bytes[11];   // the patch row's 42 bytes from byte 0
+#pragma unroll
+        for (int k = 0; k < 11; ++k) bytes[k] = __builtin_amdgcn_alignbyte(d[k + 1], d[k], sh);
+        elem_t* dst = static_cast<elem_t*>(out) + (row_base + int64_t(bw) * 4) * kRowLen + (dt * P + y) * P;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            float v[P];
+#pragma unroll
+            for (int q = 0; q < P; ++q) {
+                const int byte = 3 * q + c;
+                v[q] = (float((bytes[byte >> 2] >> (8 * (byte & 3))) & 255u) + z[c]) * a[c];
+            }
+            elem_t* dc = dst + c * 2 * P * P;
+            if constexpr (OUT_BF16 != 0) {
+                using f2 = float __attribute__((ext_vector_type(2)));
+                using b2 = __bf16 __attribute__((ext_vector_type(2)));
+#pragma unroll
+                for (int e = 0; e < P / 2; ++e) {
+                    const f2 pr = {v[2 * e], v[2 * e + 1]};
+                    reinterpret_cast<uint32_t*>(dc)[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pr, b2));
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < P / 2; ++e)
+                    reinterpret_cast<float2*>(dc)[e] = make_float2(v[2 * e], v[2 * e + 1]);
+            }
+        }
     }
 }
 
@@ -793,14 +873,20 @@ int launch_resize(const PlanView& plan, void* out, hipStream_t stream) {
     return static_cast<int>(hipGetLastError());
 }
 
-int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
+int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm, int patch,
                     hipStream_t stream) {
     if (plan.n_tiles <= 0) return 0;
     dim3 grid(plan.n_tiles), block(256);
-    if (out_dtype == 1)
+    if (patch == 14) {
+        if (out_dtype == 1)
+            hipLaunchKernelGGL(patchify14_kernel<1>, grid, block, 0, stream, plan, out, norm);
+        else
+            hipLaunchKernelGGL(patchify14_kernel<0>, grid, block, 0, stream, plan, out, norm);
+    } else if (out_dtype == 1) {
         hipLaunchKernelGGL(patchify_kernel<1>, grid, block, 0, stream, plan, out, norm);
-    else
+    } else {
         hipLaunchKernelGGL(patchify_kernel<0>, grid, block, 0, stream, plan, out, norm);
+    }
     return static_cast<int>(hipGetLastError());
 }
 

@@ -87,7 +87,7 @@ struct DevItem {
     int32_t band;            // streaming kernel: output columns per wave (16, 32, 48 or 64)
     int32_t sy_off, sx_off;  // streaming kernel: slot and column tables
     int32_t row_px;          // streaming kernel: source pixels per wave row (64 * px)
-    int32_t pad0;
+    int32_t patch;           // patch edge P (16 or 14): rows of 6 P^2 values, windows of 2P
 };
 static_assert(sizeof(DevItem) == 104, "DevItem layout");
 
@@ -142,7 +142,7 @@ int launch_stream(const PlanView& plan, const StreamLaunch& launch, void* out, i
                   const Norm& norm, hipStream_t stream);
 // Normalise + patchify of frames already at the target size: one workgroup
 // per merge-window row of a frame pair (tile_prefix counts them per item).
-int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
+int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& norm, int patch,
                     hipStream_t stream);
 // uint8 cache writer over tile_prefix (items with route kRouteResize: rh x cw
 // output tiles, tables holding fixed-point weights); out is the byte buffer.

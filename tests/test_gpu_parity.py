@@ -60,13 +60,13 @@ def plan_item(it: workloads.Item):
     return h, w, idx
 
 
-def run_gpu(items, mean, std, dtype, extra_rows=8, stream=None):
+def run_gpu(items, mean, std, dtype, extra_rows=8, stream=None, patch=16):
     """items: list of (device frames, indices, h, w).  Output is prefilled
     with NaN and has `extra_rows` spare rows that must stay NaN."""
-    vitems = [vp.Item(f, idx, h, w) for f, idx, h, w in items]
+    vitems = [vp.Item(f, idx, h, w, patch) for f, idx, h, w in items]
     grid, cu, rows, ws = vp.vp_batch_layout(vitems)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    out = torch.full((rows + extra_rows, vp.VP_ROW), float("nan"), dtype=tdt, device=DEV)
+    out = torch.full((rows + extra_rows, vp.row_width(patch)), float("nan"), dtype=tdt, device=DEV)
     work = torch.empty(ws, dtype=torch.uint8, device=DEV)
     g2, cu2 = vp.vp_preprocess_batch(vitems, mean, std,
                                      vp.VP_OUT_BF16 if dtype == "bf16" else vp.VP_OUT_F32,
@@ -74,7 +74,7 @@ def run_gpu(items, mean, std, dtype, extra_rows=8, stream=None):
     assert g2.tolist() == grid.tolist() and cu2.tolist() == cu.tolist()
     torch.cuda.synchronize()
     og, ocu = oracle.layout([len(i[1]) for i in items], [i[2] for i in items],
-                            [i[3] for i in items])
+                            [i[3] for i in items], patch=patch)
     assert grid.tolist() == og.tolist() and cu.tolist() == ocu.tolist()
     if extra_rows:
         assert torch.isnan(out[rows:].float()).all(), "rows beyond the batch were written"
@@ -312,3 +312,33 @@ def test_workload_c4_full_size():
     for b in rng.choice(64, 16, replace=False).tolist():
         f, idx, h, w = items[b]
         _check_sampled_rows(out, cu, b, f, idx, h, w, rng.integers(0, 57344, 40).tolist(), wl, "bf16")
+
+
+# --------------------------------------------------------------------------
+# Qwen2/2.5-VL geometry: patch 14 (windows of 28, rows of 1176)
+# --------------------------------------------------------------------------
+
+PATCH14 = [
+    ("p14_downscale_f32", [(3, 150, 260, [2, 0], 84, 140)], "f32"),
+    ("p14_upscale_bf16", [(2, 40, 50, [1, 0, 1], 56, 84)], "bf16"),
+    ("p14_identity_f32", [(2, 56, 84, [1, 0], 56, 84)], "f32"),
+    ("p14_ragged_bf16", [(5, 70, 90, [4, 1, 3], 56, 112), (1, 333, 257, [0], 308, 252),
+                         (3, 480, 854, [0, 1, 2], 112, 196)], "bf16"),
+]
+
+
+@pytest.mark.parametrize("name,specs,dtype", PATCH14, ids=[c[0] for c in PATCH14])
+def test_patch14_small_cases_full(name, specs, dtype):
+    mean, std = (0.48145466, 0.4578275, 0.40821073), (0.26862954, 0.26130258, 0.27577711)
+    items, host = [], []
+    for k, (n_src, H, W, idx, h, w) in enumerate(specs):
+        it = _rand_video(600 + k, n_src, H, W)
+        items.append((workloads.frames_torch(it, DEV), np.asarray(idx, np.int32), h, w))
+        host.append(workloads.frames_np(it))
+    log(f"case {name}: {[(s[0], s[1], s[2], s[4], s[5]) for s in specs]} {dtype}")
+    out, grid, cu = run_gpu(items, mean, std, dtype, patch=14)
+    assert all_written(out)
+    for k, (f, idx, h, w) in enumerate(items):
+        ref = oracle.preprocess_item(host[k], idx, h, w, mean, std, patch=14)
+        assert_close(host_rows(out, cu[k], cu[k + 1], dtype), ref, dtype, f"{name} item {k}")
+

@@ -35,19 +35,19 @@ def _free_memory():
     torch.cuda.empty_cache()
 
 
-def run(entry, items, mean, std, dtype, extra_rows=8):
+def run(entry, items, mean, std, dtype, extra_rows=8, patch=16):
     """items: list of (device frames, indices); every target is its frames' size."""
-    vitems = [vp.Item(f, idx, f.shape[1], f.shape[2]) for f, idx in items]
+    vitems = [vp.Item(f, idx, f.shape[1], f.shape[2], patch) for f, idx in items]
     grid, cu, rows, ws = vp.vp_batch_layout(vitems)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    out = torch.full((rows + extra_rows, vp.VP_ROW), float("nan"), dtype=tdt, device=DEV)
+    out = torch.full((rows + extra_rows, vp.row_width(patch)), float("nan"), dtype=tdt, device=DEV)
     work = torch.empty(ws, dtype=torch.uint8, device=DEV)
     g2, cu2 = entry(vitems, mean, std, vp.VP_OUT_BF16 if dtype == "bf16" else vp.VP_OUT_F32,
                     out, work)
     torch.cuda.synchronize()
     assert g2.tolist() == grid.tolist() and cu2.tolist() == cu.tolist()
     og, ocu = oracle.layout([len(i[1]) for i in items], [i[0].shape[1] for i in items],
-                            [i[0].shape[2] for i in items])
+                            [i[0].shape[2] for i in items], patch=patch)
     assert grid.tolist() == og.tolist() and cu.tolist() == ocu.tolist()
     if extra_rows:
         assert torch.isnan(out[rows:].float()).all(), "rows beyond the batch were written"
@@ -138,3 +138,38 @@ def test_patchify_cached_workload_full_size():
         lo = int(cu[k]) + tt * per_pair
         assert_close(host_rows(out, lo, lo + per_pair, wl.out_dtype), ref, wl.out_dtype,
                      f"cached workload item {int(k)} pair {tt}")
+
+
+CASES14 = [
+    ("p14_one_window", [(2, 28, 28, [0, 1])], "f32"),
+    ("p14_video", [(5, 56, 84, [4, 0, 2, 1])], "bf16"),
+    ("p14_odd_and_image", [(3, 84, 56, [2, 0, 1]), (1, 252, 448, [0])], "bf16"),
+    ("p14_wide_rows", [(2, 28, 1008, [1, 0])], "f32"),
+]
+
+
+@pytest.mark.parametrize("name,specs,dtype", CASES14, ids=[c[0] for c in CASES14])
+def test_patchify_patch14_vs_oracle(name, specs, dtype):
+    items, host = [], []
+    for k, (n, h, w, idx) in enumerate(specs):
+        fd, fh = _frames(700 + k, n, h, w)
+        items.append((fd, np.asarray(idx, np.int32)))
+        host.append(fh)
+    log(f"case {name}: {[(s[0], s[1], s[2]) for s in specs]} {dtype}")
+    out, cu = run(vp.vp_patchify_batch, items, MEAN, STD, dtype, patch=14)
+    for k, (fd, idx) in enumerate(items):
+        ref = oracle.patchify_item(host[k], idx, MEAN, STD, patch=14)
+        assert_close(host_rows(out, cu[k], cu[k + 1], dtype), ref, dtype, f"{name} item {k}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_patch14_patchify_equals_preprocess_at_identity_size(dtype):
+    items = []
+    for k, (n, h, w, idx) in enumerate([(4, 56, 84, [3, 0, 1]), (1, 112, 56, [0])]):
+        fd, _ = _frames(800 + k, n, h, w)
+        items.append((fd, np.asarray(idx, np.int32)))
+    a, _ = run(vp.vp_patchify_batch, items, MEAN, STD, dtype, patch=14)
+    b, _ = run(vp.vp_preprocess_batch, items, MEAN, STD, dtype, patch=14)
+    assert torch.equal(a.view(torch.int16) if dtype == "bf16" else a.view(torch.int32),
+                       b.view(torch.int16) if dtype == "bf16" else b.view(torch.int32))
+

@@ -22,10 +22,11 @@ def log(msg):
     sys.stdout.flush()
 
 
-def _check(items_spec):
+def _check(items_spec, patch=16):
     # frames are never read: any valid device pointer will do
     dummy = torch.zeros((1, 32, 32, 3), dtype=torch.uint8, device=DEV)
-    items = [vp.Item((dummy.data_ptr(), n_src, 32, 32), idx, h, w) for n_src, idx, h, w in items_spec]
+    items = [vp.Item((dummy.data_ptr(), n_src, 32, 32), idx, h, w, patch)
+             for n_src, idx, h, w in items_spec]
     _, _, rows, ws = vp.vp_batch_layout(items)
     vit = torch.full((rows + 4, 3), -7, dtype=torch.int32, device=DEV)
     llm = torch.full((rows // 4 + 2, 3), -7, dtype=torch.int32, device=DEV)
@@ -33,7 +34,7 @@ def _check(items_spec):
     cu = vp.vp_position_ids(items, vit, llm, work)
     torch.cuda.synchronize()
     ov, ol, ocu = oracle.position_ids([len(s[1]) for s in items_spec], [s[2] for s in items_spec],
-                                      [s[3] for s in items_spec])
+                                      [s[3] for s in items_spec], patch=patch)
     v = vit.cpu().numpy()
     l = llm.cpu().numpy()
     assert np.array_equal(v[:rows], ov) and (v[rows:] == -7).all()
@@ -50,3 +51,9 @@ def test_positions_ragged_batch():
 def test_positions_rollout_workload_full_size():
     wl = workloads.config(4)
     _check([(it.n_src, list(range(256)), 256, 448) for it in wl.items])
+
+
+def test_positions_patch14_ragged_batch():
+    _check([(5, [4, 0, 2], 56, 28), (1, [0], 84, 56), (3, [1, 2, 0, 1, 2], 252, 448),
+            (1, [0], 980, 980)], patch=14)
+

@@ -296,3 +296,25 @@ def test_position_ids_segments_and_errors_on_host():
     assert L.vp_position_ids(b.arr, 2, dev, None, 1 << 20, None, 0, None, None, 1 << 20, None) == vp.VP_ERR_NULL
     bad = vp._Batch([vp.Item((0x10000, 5, 100, 70), [4, 0, 2], 64, 48)])
     assert L.vp_position_ids(bad.arr, 1, dev, None, 1 << 20, None, 0, None, ws, 1 << 20, None) == vp.VP_ERR_DIMS
+
+
+def test_patch14_layout_and_checks():
+    """Qwen2/2.5-VL geometry: patch 14, windows of 28, rows of 1176."""
+    for H, W, maxp in [(720, 1280, 262144), (480, 854, 230400), (1024, 1024, 1003520), (720, 1280, 122880)]:
+        assert vp.vp_smart_resize_dims(H, W, 28, 0, maxp) == oracle.smart_resize(H, W, 28, 0, maxp)
+    items = [vp.Item((0x10000, 9, 100, 70), [4, 0, 2, 8, 1], 252, 448, patch=14),
+             vp.Item((0x20000, 1, 40, 50), [0], 980, 980, patch=14)]
+    grid, cu, rows, _ = vp.vp_batch_layout(items)
+    og, ocu = oracle.layout([5, 1], [252, 980], [448, 980], patch=14)
+    assert grid.tolist() == og.tolist() == [[3, 18, 32], [1, 70, 70]]
+    assert cu.tolist() == ocu.tolist() and rows == cu[-1]
+    assert vp.row_width(14) == 1176
+    def status(its):
+        with pytest.raises(vp.VPError) as e:
+            vp.vp_batch_layout(its)
+        return e.value.status
+    assert status([vp.Item((0x10000, 2, 64, 64), [0], 64, 64, patch=14)]) == vp.VP_ERR_DIMS
+    assert status([vp.Item((0x10000, 2, 64, 64), [0], 64, 64, patch=12)]) == vp.VP_ERR_ARG
+    assert status([vp.Item((0x10000, 2, 64, 64), [0], 64, 64),
+                   vp.Item((0x10000, 2, 64, 64), [0], 56, 56, patch=14)]) == vp.VP_ERR_ARG
+    assert b"share one patch size" in vp.lib().vp_last_error_message()
