@@ -89,7 +89,7 @@ def cpu_baseline(wl, frames_dev, planned, patch_only=False, resize_only=False, b
                 list(ex.map(lambda j: oracle.patchify_item(j[0], [0, 1], wl.mean, wl.std), jobs))
             else:
                 list(ex.map(lambda j: oracle.preprocess_item(j[0], [0, 1], j[1], j[2], wl.mean,
-                                                             wl.std), jobs))
+                                                             wl.std, patch=wl.items[0].patch), jobs))
             spent += time.perf_counter() - t0
             frames_count += len(idx)
             pairs += len(jobs)
@@ -116,6 +116,8 @@ def main():
                     help="time the uint8 cache writer (fixed-point resize only) on the workload")
     ap.add_argument("--positions", action="store_true",
                     help="time the position tables (ViT rows, LLM windows) of the workload's rows")
+    ap.add_argument("--patch", type=int, default=16, choices=(14, 16),
+                    help="14: the Qwen2/2.5-VL geometry on workload 4's frames (252x448, rows of 1176)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run plain 1 GiB device-to-device copies (twice) before the steps, "
@@ -141,7 +143,10 @@ def main():
     log(f"device {props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count} "
         f"mem={props.total_memory / 2**30:.0f} GiB")
 
-    wl = workloads.patchify_config() if args.patchify else workloads.config(args.workload)
+    if args.patch == 14:
+        wl = workloads.patch14_config()
+    else:
+        wl = workloads.patchify_config() if args.patchify else workloads.config(args.workload)
     entry = vp.vp_patchify_batch if args.patchify else vp.vp_preprocess_batch
     log(f"workload {wl.name}")
     t0 = time.perf_counter()
@@ -156,14 +161,14 @@ def main():
             if it.dims is not None:
                 h, w = it.dims
             else:
-                h, w = vp.vp_smart_resize_dims(it.H, it.W, 32, it.min_pixels, it.max_pixels)
+                h, w = vp.vp_smart_resize_dims(it.H, it.W, 2 * it.patch, it.min_pixels, it.max_pixels)
             s = it.sample
             if s["mode"] == "uniform":
                 idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_UNIFORM, s["n"])
             else:
                 idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_FPS, 0, s["video_fps"], s["fps"],
                                            s["min_frames"], s["max_frames"])
-            vitems.append(vp.Item(fr, idx, h, w))
+            vitems.append(vp.Item(fr, idx, h, w, it.patch))
             planned.append((h, w, idx))
         return vitems, planned
 
@@ -179,8 +184,8 @@ def main():
         out_llm = torch.empty((rows // 4, 3), dtype=torch.int32, device=dev)
     else:
         grid, cu, rows, ws_bytes = vp.vp_batch_layout(vitems)
-        out = torch.empty((rows, vp.VP_ROW), dtype=torch.bfloat16 if code == vp.VP_OUT_BF16
-                          else torch.float32, device=dev)
+        out = torch.empty((rows, vp.row_width(wl.items[0].patch)),
+                          dtype=torch.bfloat16 if code == vp.VP_OUT_BF16 else torch.float32, device=dev)
     work = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     n_frames = sum(len(p[2]) for p in planned)
@@ -248,8 +253,9 @@ def main():
         f"({achieved / HBM_PEAK_GBPS:.1%} of 8 TB/s)")
     log("kernel ms per step: " + " ".join(f"{t:.3f}" for t in kern_ms))
 
-    tag = "p4" if args.patchify else (f"r{args.workload}" if args.resize else
-                                      (f"i{args.workload}" if args.positions else f"c{args.workload}"))
+    tag = "q4" if args.patch == 14 else (
+        "p4" if args.patchify else (f"r{args.workload}" if args.resize else
+                                    (f"i{args.workload}" if args.positions else f"c{args.workload}")))
     sha = kernel_source_sha()
     traffic = counter_traffic(tag, sha)
 

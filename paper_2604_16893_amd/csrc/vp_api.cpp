@@ -313,20 +313,21 @@ int32_t band_span(const AxisFilter& fx, int32_t band) {
 }
 
 // Whether an item can take the streaming kernel, and with which shape: the
-// output width is cut into bands of 16, 32, 48 or 64 columns (whole patches;
+// output width is cut into bands of 1 to 4 whole patches (16 to 64 columns,
+// or 14 to 56 for patch 14;
 // one single-wave workgroup each, one lane per column in the x pass), each
 // band's source pixels must fit 64 lanes of px pixels, and among the shapes
 // that fit, the one with the least estimated lane work is taken.  The LDS
 // budget is checked with float32 staging, so the routing does not depend on
 // the output type.
-bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
+bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t patch, StreamShape* sh) {
     if (m < 4 || m > vp::kSlotMax) return false;
     const int32_t mm = m;
     const int32_t kx = round_up(fx.taps, 4);
     // every load of a frame row (up to kSlotMax + 8 rows past the last one) stays below 4 GiB
     if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
     int64_t best = -1;
-    for (int32_t band = 64; band >= 16; band -= 16) {
+    for (int32_t band = 4 * patch; band >= patch; band -= patch) {
         const int32_t waves = (it.dst_w + band - 1) / band;
         const int32_t span = band_span(fx, band);
         for (int32_t px = 2; px <= 4; ++px) {
@@ -496,7 +497,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         d.route = vp::kRouteGeneric;
         int32_t m = 0;
         StreamShape sh;
-        if (P == vp::kPatch && slots_for(*fy, &d.sy_off, &m) && stream_shape(it, *fx, m, &sh)) {
+        if (slots_for(*fy, &d.sy_off, &m) && stream_shape(it, *fx, m, P, &sh)) {
             d.route = vp::kRouteStream;
             d.band = sh.band;
             d.row_px = 64 * sh.px;
@@ -561,7 +562,10 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         int64_t band = max_src_rows * d.h / d.H;
         const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
         band = std::max(band, min_band);
-        band = std::max<int64_t>((band + 3) / 4 * 4, 16);
+        // whole store groups: multiples of 4 rows for patch 16, whole
+        // patches (14 rows, stored as 4 + 4 + 4 + 2) for patch 14
+        const int64_t unit = d.patch == 16 ? 4 : d.patch;
+        band = std::max<int64_t>((band + unit - 1) / unit * unit, std::max<int64_t>(16, unit));
         band = std::min<int64_t>(band, d.h);
         for (int32_t tt = 0; tt < d.t; ++tt) {
             const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
@@ -618,6 +622,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         L.m = std::get<0>(key0);
         L.kx = std::get<1>(key0);
         L.px = std::get<2>(key0);
+        L.patch = P;
         for (size_t c0 = k0; c0 < k1; c0 += 8) {
             const size_t c1 = std::min(c0 + 8, k1);
             int32_t rounds = 0;

@@ -517,10 +517,11 @@ __device__ __forceinline__ void wave_lds_fence() {
 //   * every four output rows the stage holds, for each (patch, channel), the
 //     band's part of one 64-value run; it leaves as 16-byte stores, eight
 //     lanes per 128-byte run.
-template <int M, int KX, int PX, int OUT_BF16>
+template <int M, int KX, int PX, int OUT_BF16, int P>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
     M * PX > 12 || 3 * M * PX + KX >= 52 || (OUT_BF16 == 0 && M * PX >= 12) ? 4 : 5)))
 void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
+    static_assert(P == 16 || P == 14, "patch 16 or 14");
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
     constexpr int kRowPx = 64 * PX;
     constexpr int V = 3 * PX;                      // values per lane per source row
@@ -649,9 +650,14 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
         }
     };
 
-    // Store-out pieces of this lane: piece e = lane + 64 r of the band's
-    // (patch q, channel c, row ry, piece) runs, as a stage offset (-1: none)
-    // and an output offset relative to the merge-window row block.
+    // Patch 14: the stage is kept in output order, [c][patch q][4 rows][14],
+    // so that each (patch, channel) run of a row group is contiguous in both;
+    // the lane's column j0 + lane is column lane % 14 of patch lane / 14.
+    const int st14 = (lane / 14) * 56 + lane % 14;
+
+    // Store-out pieces of this lane (patch 16): piece e = lane + 64 r of the
+    // band's (patch q, channel c, row ry, piece) runs, as a stage offset
+    // (-1: none) and an output offset relative to the merge-window row block.
     constexpr int kPieces = 16 / S;
     constexpr int kPerPatch = 3 * 4 * kPieces;
     constexpr int kStoreIter = (4 * kPerPatch + 63) / 64;
@@ -672,9 +678,41 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
         }
     }
 
-    // x pass of output row i, normalise, stage; every 4th row: store.
+    // Patch 14 store-out of the row group that ends at output row i: rows
+    // g0 .. i of the patch rows of the band's patches, NP pieces of 4 values
+    // per (patch, channel) run (14 for 4 rows, 7 for the last 2 rows of a
+    // patch).  bf16 pieces are 8 bytes: the second temporal half of a run
+    // starts 196 values on, only 8-byte aligned.
+    auto store14 = [&](int i, auto np_tag) __attribute__((always_inline)) {
+        constexpr int NP = decltype(np_tag)::value;
+        using piece_t = typename std::conditional<OUT_BF16 != 0, uint2, uint4>::type;
+        const int g0 = (i % 14) & ~3;
+        const int bh = i / 28;
+        const int mh = (i / 14) & 1;
+        const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + bh) * it->wm * 4 + mh * 2;
+        elem_t* const obase = static_cast<elem_t*>(out) + win_row0 * (6 * P * P) + g0 * 14;
+        const int n_pieces = (nbw / 14) * 3 * NP;
+        for (int e = lane; e < n_pieces; e += 64) {
+            const int q = e / (3 * NP);
+            const int r2 = e - q * (3 * NP);
+            const int c = r2 / NP;
+            const int pc = r2 - c * NP;
+            const piece_t val = *reinterpret_cast<const piece_t*>(stage + (c * 4 + q) * 56 + pc * 4);
+            const int qa = j0 / 14 + q;
+            elem_t* dst = obase + ((qa >> 1) * 4 + (qa & 1)) * (6 * P * P) + c * 392 + pc * 4;
+            if (both) {
+                *reinterpret_cast<piece_t*>(dst) = val;
+                *reinterpret_cast<piece_t*>(dst + 196) = val;
+            } else {
+                *reinterpret_cast<piece_t*>(dst + dt_self * 196) = val;
+            }
+        }
+    };
+
+    // x pass of output row i, normalise, stage; at the end of every group of
+    // four rows of a patch (for patch 14 also after its last two): store.
     auto x_pass = [&](int i) __attribute__((always_inline)) {
-        const int yy = i & 3;
+        const int yy = P == 16 ? (i & 3) : ((i % 14) & 3);
         if (xlane) {
             float r0 = z0, r1 = z1, r2 = z2;
             const float4* src = row + sj;
@@ -697,18 +735,29 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             const float v0 = r0 * a0;
             const float v1 = r1 * a1;
             const float v2 = r2 * a2;
-            elem_t* st = stage + yy * 64 + lane;
+            constexpr int kCh = P == 16 ? 256 : 224;   // stage channel stride
+            elem_t* st = P == 16 ? stage + yy * 64 + lane : stage + st14 + yy * 14;
             if constexpr (OUT_BF16 != 0) {
                 st[0] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v0));
-                st[256] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
-                st[512] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
+                st[kCh] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
+                st[2 * kCh] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
             } else {
                 st[0] = v0;
-                st[256] = v1;
-                st[512] = v2;
+                st[kCh] = v1;
+                st[2 * kCh] = v2;
             }
         }
-        if (yy == 3) {
+        if constexpr (P == 14) {
+            const int y14 = i % 14;
+            if (y14 == 13 || yy == 3) {
+                wave_lds_fence();
+                if (y14 == 13)
+                    store14(i, std::integral_constant<int, 7>{});
+                else
+                    store14(i, std::integral_constant<int, 14>{});
+                wave_lds_fence();
+            }
+        } else if (yy == 3) {
             wave_lds_fence();
             // rows i-3 .. i: the lane's 16-byte pieces (precomputed below)
             const int yq = (i & 15) >> 2;
@@ -743,8 +792,8 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     // float copy of the byte would, without a conversion per value.  Pair p
     // (values 2p, 2p+1) starts at byte shift + 2p, inside dwords p/2 and
     // p/2 + 1: the selector is sel, plus 2 per byte for odd p.
-    constexpr int P = (V + 1) / 2;
-    auto unpack = [&](load_t cur, uint32_t s0, uint32_t (&hv)[P]) __attribute__((always_inline)) {
+    constexpr int kPairs = (V + 1) / 2;
+    auto unpack = [&](load_t cur, uint32_t s0, uint32_t (&hv)[kPairs]) __attribute__((always_inline)) {
         uint32_t d[kLoadDwords];
         d[0] = cur.x;
         d[1] = cur.y;
@@ -755,7 +804,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
         uint32_t s1;
         asm volatile("v_add_u32 %0, 0x20002, %1" : "=v"(s1) : "v"(s0));
 #pragma unroll
-        for (int p = 0; p < P; ++p) {
+        for (int p = 0; p < kPairs; ++p) {
             const int j = p >> 1;
             const int hi = j + 1 < kLoadDwords ? j + 1 : j;
             hv[p] = __builtin_amdgcn_perm(d[hi], d[j], (p & 1) ? s1 : s0);
@@ -764,7 +813,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
 
     // Source row y (its values in hv) into the slots; then closes the output
     // rows whose close row is y.
-    auto process_row = [&](int y, const uint32_t (&hv)[P], cptr<float> wr) __attribute__((always_inline)) {
+    auto process_row = [&](int y, const uint32_t (&hv)[kPairs], cptr<float> wr) __attribute__((always_inline)) {
         float v[V];
 #pragma unroll
         for (int q = 0; q < V; ++q) {
@@ -830,13 +879,13 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
             // unpack first: the next load then reuses the same registers
-            uint32_t hv[P];
+            uint32_t hv[kPairs];
             unpack(pf[k], sel[k], hv);
             // (keep the unpacking here, ahead of the load that reuses
             // pf[k]'s registers; otherwise it sinks into the conditional use
             // below and pf[k] has to be copied while its load is in flight)
 #pragma unroll
-            for (int q = 0; q < P; ++q) asm volatile("" : : "v"(hv[q]));
+            for (int q = 0; q < kPairs; ++q) asm volatile("" : : "v"(hv[q]));
             pf[k] = load_row(yb + kPrefetch, k);
             if (y >= y0 && y < y1) process_row(y, hv, wblk + k * kSlotWords);
         }
@@ -848,10 +897,16 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
                         const Norm& norm, hipStream_t stream) {
     const int lds = stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4);
     dim3 grid(static_cast<unsigned>(L.count)), block(64);
-    if (out_dtype == 1)
-        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1>), grid, block, lds, stream, plan, L.first, out, norm);
-    else
-        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 0>), grid, block, lds, stream, plan, L.first, out, norm);
+    if (L.patch == 14) {
+        if (out_dtype == 1)
+            hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1, 14>), grid, block, lds, stream, plan, L.first, out, norm);
+        else
+            hipLaunchKernelGGL((stream_kernel<M, KX, PX, 0, 14>), grid, block, lds, stream, plan, L.first, out, norm);
+    } else if (out_dtype == 1) {
+        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1, 16>), grid, block, lds, stream, plan, L.first, out, norm);
+    } else {
+        hipLaunchKernelGGL((stream_kernel<M, KX, PX, 0, 16>), grid, block, lds, stream, plan, L.first, out, norm);
+    }
     return static_cast<int>(hipGetLastError());
 }
 

@@ -132,6 +132,7 @@ constexpr uint32_t kNoWork = 0xffffffffu;
 struct StreamLaunch {
     int32_t first, count;
     int32_t m, kx, px;       // accumulator slots, column taps, pixels per lane
+    int32_t patch;           // patch edge of the batch (16 or 14)
     int64_t cost;            // host only: estimated work (source pixels read)
 };
 

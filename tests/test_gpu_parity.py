@@ -46,8 +46,9 @@ def plan_item(it: workloads.Item):
     if it.dims is not None:
         h, w = it.dims
     else:
-        h, w = vp.vp_smart_resize_dims(it.H, it.W, 32, it.min_pixels, it.max_pixels)
-        assert (h, w) == oracle.smart_resize(it.H, it.W, 32, it.min_pixels, it.max_pixels)
+        F = 2 * it.patch
+        h, w = vp.vp_smart_resize_dims(it.H, it.W, F, it.min_pixels, it.max_pixels)
+        assert (h, w) == oracle.smart_resize(it.H, it.W, F, it.min_pixels, it.max_pixels)
     s = it.sample
     if s["mode"] == "uniform":
         idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_UNIFORM, s["n"])
@@ -210,15 +211,15 @@ def _materialise(wl):
     return items, planned
 
 
-def _check_pairs(out, cu, b, item_dev, idx, h, w, pairs, wl, dtype):
+def _check_pairs(out, cu, b, item_dev, idx, h, w, pairs, wl, dtype, patch=16):
     """Whole frame pairs of item b against the oracle (frames copied from the device input)."""
-    rows_per_t = (h // 16) * (w // 16)
+    rows_per_t = (h // patch) * (w // patch)
     n = len(idx)
     padded = list(idx) + ([idx[-1]] if n % 2 else [])
     for tt in pairs:
         fids = [padded[2 * tt], padded[2 * tt + 1]]
         frames = item_dev[fids].cpu().numpy()
-        ref = oracle.preprocess_item(frames, [0, 1], h, w, wl.mean, wl.std)
+        ref = oracle.preprocess_item(frames, [0, 1], h, w, wl.mean, wl.std, patch=patch)
         lo = cu[b] + tt * rows_per_t
         assert_close(host_rows(out, lo, lo + rows_per_t, dtype), ref, dtype,
                      f"item {b} pair {tt}")
@@ -341,4 +342,22 @@ def test_patch14_small_cases_full(name, specs, dtype):
     for k, (f, idx, h, w) in enumerate(items):
         ref = oracle.preprocess_item(host[k], idx, h, w, mean, std, patch=14)
         assert_close(host_rows(out, cu[k], cu[k + 1], dtype), ref, dtype, f"{name} item {k}")
+
+
+def test_workload_q4_patch14_full_size():
+    """Configuration 4's 64 x 256 frames in the patch-14 geometry (252x448,
+    rows of 1176), in the launch configuration the benchmark times."""
+    wl = workloads.patch14_config()
+    log(wl.name)
+    items = []
+    for it in wl.items:
+        h, w, idx = plan_item(it)
+        assert (h, w) == (252, 448)
+        items.append((workloads.frames_torch(it, DEV, chunk=32), idx, h, w))
+    out, grid, cu = run_gpu(items, wl.mean, wl.std, wl.out_dtype, patch=14)
+    assert out.shape[0] == 64 * 128 * 18 * 32 and all_written(out)
+    rng = np.random.default_rng(14)
+    for b in [0, 63] + rng.choice(64, 2, replace=False).tolist():
+        f, idx, h, w = items[b]
+        _check_pairs(out, cu, b, f, idx, h, w, [0, int(rng.integers(1, 128)), 127], wl, "bf16", patch=14)
 

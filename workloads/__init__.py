@@ -101,6 +101,7 @@ class Item:
     max_pixels: Optional[int] = None
     min_pixels: int = 0
     rects: Optional[list] = None
+    patch: int = 16          # 16, or 14 for the Qwen2/2.5-VL geometry (smart_resize factor 2 * patch)
 
     @property
     def frame_bytes(self) -> int:
@@ -188,6 +189,17 @@ def config(k: int) -> Workload:
             "c4: 64 videos x 256 frames 720x1280 -> 256x448 (smart_resize@122880), bf16",
             items, MEAN_C4, STD_C4, "bf16")
     raise ValueError(k)
+
+
+def patch14_config() -> Workload:
+    """Configuration 4's frames in the Qwen2/2.5-VL geometry: patch 14, so
+    smart_resize with factor 28 under the same 122,880 px budget gives
+    252x448, and rows hold 3 x 2 x 14 x 14 = 1176 values."""
+    items = [Item("video", 256, 720, 1280, "gradnoise", 4000 + v, {"mode": "uniform", "n": 256},
+                  max_pixels=122880, patch=14)
+             for v in range(64)]
+    return Workload("q4: 64 videos x 256 frames 720x1280 -> 252x448 (smart_resize factor 28 "
+                    "@122880), patch 14, rows of 1176, bf16", items, MEAN_C4, STD_C4, "bf16")
 
 
 def patchify_config() -> Workload:
