@@ -333,7 +333,7 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t pa
         for (int32_t px = 2; px <= 4; ++px) {
             if (!vp::stream_shape_supported(mm, kx, px)) continue;
             if (span > 64 * px || kx > 64 * px) continue;
-            if (vp::stream_wave_bytes(px, kx, 4) > vp::kStreamLdsBudget) continue;
+            if (vp::stream_wave_bytes(px, kx, 4, patch) > vp::kStreamLdsBudget) continue;
             const int64_t cost = int64_t(waves) * (int64_t(it.src_h) * px * 3 * (mm + 1) +
                                                     int64_t(it.dst_h) * (3 * kx + 12));
             if (best < 0 || cost < best) {
@@ -525,7 +525,8 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     p->total_rows = rows;
 
     // Streaming units: one per (item, distinct frame of a pair, band of output
-    // rows).  A workgroup streams the source rows of its unit top to bottom,
+    // rows); for patch 14 one per (item, pair, band), its frames on the two
+    // waves of one workgroup.  A workgroup streams the source rows of its unit top to bottom,
     // so its life is about proportional to those rows.  To end the batch
     // evenly -- many kernel shapes run side by side, and a small launch lasts
     // as long as its longest unit -- no unit reads more than an eighth of the
@@ -563,13 +564,14 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
         band = std::max(band, min_band);
         // whole store groups: multiples of 4 rows for patch 16, whole
-        // patches (14 rows, stored as 4 + 4 + 4 + 2) for patch 14
+        // patch rows (14 output rows, stored at once) for patch 14
         const int64_t unit = d.patch == 16 ? 4 : d.patch;
-        band = std::max<int64_t>((band + unit - 1) / unit * unit, std::max<int64_t>(16, unit));
-        band = std::min<int64_t>(band, d.h);
+        band = std::max<int64_t>((band + unit - 1) / unit * unit, d.patch == 16 ? 16 : 2 * d.patch);
+        band = std::min<int64_t>(band, d.h);   // h is a multiple of 2P: every band ends on a whole group
         for (int32_t tt = 0; tt < d.t; ++tt) {
             const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
-            for (int32_t dt = 0; dt < (same ? 1 : 2); ++dt) {
+            const bool pair_units = d.patch == 14;   // both frames in one unit
+            for (int32_t dt = 0; dt < (same || pair_units ? 1 : 2); ++dt) {
                 for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
                     const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
                     Keyed k;
@@ -579,7 +581,8 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
                     k.unit.p = 2 * tt + dt;
                     k.unit.rows = i0 | (i1 << 16);
                     k.unit.flags = same ? 1 : 0;
-                    k.cost = int64_t(i1 - i0) * d.H / d.h * d.W;   // source pixels read, roughly
+                    k.cost = int64_t(i1 - i0) * d.H / d.h * d.W   // source pixels read, roughly
+                             * (pair_units && !same ? 2 : 1);
                     keyed.push_back(k);
                 }
             }

@@ -501,6 +501,14 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Workgroup barrier that orders LDS accesses only: global stores and
+// prefetch loads still in flight are not waited for.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // One workgroup streams one source frame (or a band of its output rows) top
 // to bottom; each of its waves owns one band of up to 64 output columns and
 // works alone -- no workgroup barrier anywhere:
@@ -514,11 +522,19 @@ __device__ __forceinline__ void wave_lds_fence() {
 //     conflicts), and the x pass follows at once: lane j = one output column,
 //     its KX weights in registers, one ds_read_b128 and three FMAs per tap,
 //     then the normalisation FMA and the conversion into the wave's stage;
-//   * every four output rows the stage holds, for each (patch, channel), the
-//     band's part of one 64-value run; it leaves as 16-byte stores, eight
-//     lanes per 128-byte run.
+//   * patch 16: every four output rows the stage holds, for each (patch,
+//     channel), the band's part of one 64-value run; it leaves as 16-byte
+//     stores, eight lanes per 128-byte run, whole cache lines;
+//   * patch 14: a 14-row run (392 bytes in bf16) is not a whole number of
+//     cache lines, and the two frames of a pair interleave every 196 values,
+//     so stores from one frame alone leave most lines part-written (the L2
+//     then fetches them from HBM, and writes them in 32-byte pieces).  The
+//     workgroup is therefore two waves, one per frame of the pair, over the
+//     same band, sharing a stage in output order, [patch][c][frame][14][14]:
+//     after every 14th row both waves write the band's finished output rows
+//     whole (the two patches of a merge window are one contiguous run).
 template <int M, int KX, int PX, int OUT_BF16, int P>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
+__global__ __launch_bounds__(P == 16 ? 64 : 128) __attribute__((amdgpu_waves_per_eu(
     M * PX > 12 || 3 * M * PX + KX >= 52 || (OUT_BF16 == 0 && M * PX >= 12) ? 4 : 5)))
 void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     static_assert(P == 16 || P == 14, "patch 16 or 14");
@@ -529,7 +545,9 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     constexpr int S = 16 / int(sizeof(elem_t));    // output columns per 16-byte store
     extern __shared__ __align__(16) unsigned char smem[];
 
-    const int lane = threadIdx.x;
+    const int lane = static_cast<int>(threadIdx.x) & 63;
+    // patch 14: wave 0 takes the pair's first frame, wave 1 its second
+    const int wv = P == 16 ? 0 : __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     // Workgroup -> (unit, column band), from the host's list (which places
     // the bands of one unit on one XCD)
     const uint32_t wg = as_const(plan.wgs)[wg0 + static_cast<int>(blockIdx.x)];
@@ -546,12 +564,13 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     const int j0 = wave * band;                    // first output column of this wave
     const int nbw = min(band, w - j0);             // its columns
     const int tt = u_p >> 1;
-    const int dt_self = u_p & 1;
+    const int dt_self = P == 16 ? (u_p & 1) : wv;   // patch 14 units start at the pair's first frame
     const bool both = (u_flags & 1) != 0;
 
-    unsigned char* wbase = smem;
-    float4* row = reinterpret_cast<float4*>(wbase);                                   // [kRowPx]
-    elem_t* stage = reinterpret_cast<elem_t*>(wbase + kRowPx * 16);                   // [3][4][64]
+    // patch 16: [row][stage [3][4][64]]; patch 14: [row of wave 0][row of
+    // wave 1][stage [4 patches][1176]]
+    float4* row = reinterpret_cast<float4*>(smem + wv * kRowPx * 16);                  // [kRowPx]
+    elem_t* stage = reinterpret_cast<elem_t*>(smem + (P == 16 ? 1 : 2) * kRowPx * 16);
 
     // x pass: output column j0 + lane keeps its KX column weights in registers.
     const cptr<int32_t> tables = as_const(plan.tables);
@@ -577,7 +596,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     // Source frame, read through buffer resources (loads past a resource's
     // range return 0).  Every load is dword-aligned: unaligned per-lane
     // loads cost about a third of the read bandwidth on gfx950.
-    const int f = as_const(plan.indices)[it->idx_off + u_p];
+    const int f = as_const(plan.indices)[it->idx_off + u_p + (P == 16 ? 0 : wv)];
     const uintptr_t fa = reinterpret_cast<uintptr_t>(it->frames + int64_t(f) * it->frame_bytes);
     const uint32_t lead = static_cast<uint32_t>(fa & 3u);
     // Range = the frame rounded up to whole dwords: the range check is per
@@ -650,10 +669,9 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
         }
     };
 
-    // Patch 14: the stage is kept in output order, [c][patch q][4 rows][14],
-    // so that each (patch, channel) run of a row group is contiguous in both;
-    // the lane's column j0 + lane is column lane % 14 of patch lane / 14.
-    const int st14 = (lane / 14) * 56 + lane % 14;
+    // Patch 14: the lane's column j0 + lane is column lane % 14 of the
+    // band's patch lane / 14, at this offset of the stage's patch-row origin.
+    const int st14 = (lane / 14) * (6 * P * P) + lane % 14;
 
     // Store-out pieces of this lane (patch 16): piece e = lane + 64 r of the
     // band's (patch q, channel c, row ry, piece) runs, as a stage offset
@@ -678,34 +696,25 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
         }
     }
 
-    // Patch 14 store-out of the row group that ends at output row i: rows
-    // g0 .. i of the patch rows of the band's patches, NP pieces of 4 values
-    // per (patch, channel) run (14 for 4 rows, 7 for the last 2 rows of a
-    // patch).  bf16 pieces are 8 bytes: the second temporal half of a run
-    // starts 196 values on, only 8-byte aligned.
-    auto store14 = [&](int i, auto np_tag) __attribute__((always_inline)) {
-        constexpr int NP = decltype(np_tag)::value;
-        using piece_t = typename std::conditional<OUT_BF16 != 0, uint2, uint4>::type;
-        const int g0 = (i % 14) & ~3;
-        const int bh = i / 28;
-        const int mh = (i / 14) & 1;
-        const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + bh) * it->wm * 4 + mh * 2;
-        elem_t* const obase = static_cast<elem_t*>(out) + win_row0 * (6 * P * P) + g0 * 14;
-        const int n_pieces = (nbw / 14) * 3 * NP;
-        for (int e = lane; e < n_pieces; e += 64) {
-            const int q = e / (3 * NP);
-            const int r2 = e - q * (3 * NP);
-            const int c = r2 / NP;
-            const int pc = r2 - c * NP;
-            const piece_t val = *reinterpret_cast<const piece_t*>(stage + (c * 4 + q) * 56 + pc * 4);
+    // Patch 14 store-out of patch row pr (output rows 14 pr .. 14 pr + 13):
+    // the band's output rows leave the stage whole, in 16-byte pieces shared
+    // out over both waves; consecutive pieces are consecutive in memory
+    // within each merge window.
+    auto store_rows = [&](int pr) __attribute__((always_inline)) {
+        constexpr int kRowElems = 6 * P * P;                           // 1176
+        constexpr int VPP = 16 / int(sizeof(elem_t));                  // values per piece
+        constexpr int PPR = kRowElems / VPP;                           // pieces per row
+        static_assert(kRowElems % VPP == 0, "rows are whole 16-byte pieces");
+        const int nq = nbw / 14;
+        const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + (pr >> 1)) * it->wm * 4 + (pr & 1) * 2;
+        using u4v = unsigned __attribute__((ext_vector_type(4)));
+        for (int e = static_cast<int>(threadIdx.x); e < nq * PPR; e += 128) {
+            const int q = e / PPR;
+            const int pc = e - q * PPR;
             const int qa = j0 / 14 + q;
-            elem_t* dst = obase + ((qa >> 1) * 4 + (qa & 1)) * (6 * P * P) + c * 392 + pc * 4;
-            if (both) {
-                *reinterpret_cast<piece_t*>(dst) = val;
-                *reinterpret_cast<piece_t*>(dst + 196) = val;
-            } else {
-                *reinterpret_cast<piece_t*>(dst + dt_self * 196) = val;
-            }
+            const u4v val = *reinterpret_cast<const u4v*>(stage + q * kRowElems + pc * VPP);
+            elem_t* dst = static_cast<elem_t*>(out) + (win_row0 + (qa >> 1) * 4 + (qa & 1)) * kRowElems + pc * VPP;
+            __builtin_nontemporal_store(val, reinterpret_cast<u4v*>(dst));
         }
     };
 
@@ -735,27 +744,32 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             const float v0 = r0 * a0;
             const float v1 = r1 * a1;
             const float v2 = r2 * a2;
-            constexpr int kCh = P == 16 ? 256 : 224;   // stage channel stride
-            elem_t* st = P == 16 ? stage + yy * 64 + lane : stage + st14 + yy * 14;
+            constexpr int kCh = P == 16 ? 256 : 2 * P * P;   // stage channel stride
+            elem_t* st = P == 16 ? stage + yy * 64 + lane : stage + st14 + (i % 14) * 14 + dt_self * (P * P);
+            elem_t e0, e1, e2;
             if constexpr (OUT_BF16 != 0) {
-                st[0] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v0));
-                st[kCh] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
-                st[2 * kCh] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
+                e0 = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v0));
+                e1 = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
+                e2 = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
             } else {
-                st[0] = v0;
-                st[kCh] = v1;
-                st[2 * kCh] = v2;
+                e0 = v0;
+                e1 = v1;
+                e2 = v2;
+            }
+            st[0] = e0;
+            st[kCh] = e1;
+            st[2 * kCh] = e2;
+            if (P == 14 && both) {   // one frame stands for both halves of the pair
+                st[P * P] = e0;
+                st[kCh + P * P] = e1;
+                st[2 * kCh + P * P] = e2;
             }
         }
         if constexpr (P == 14) {
-            const int y14 = i % 14;
-            if (y14 == 13 || yy == 3) {
-                wave_lds_fence();
-                if (y14 == 13)
-                    store14(i, std::integral_constant<int, 7>{});
-                else
-                    store14(i, std::integral_constant<int, 14>{});
-                wave_lds_fence();
+            if (i % 14 == 13) {
+                lds_barrier();
+                store_rows(i / 14);
+                lds_barrier();
             }
         } else if (yy == 3) {
             wave_lds_fence();
@@ -865,6 +879,17 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     // every prefetch register in place.  The first block's loads are issued
     // in row order, as the loop issues them, so that the oldest load is
     // always the next one needed.
+    if (P == 14 && both && wv == 1) {
+        // wave 1 of a pair whose frames are one: no frame to stream; it keeps
+        // step with wave 0's barriers (two per patch row) and stores its share
+        for (int pr = i0 / 14; pr < i1 / 14; ++pr) {
+            lds_barrier();
+            store_rows(pr);
+            lds_barrier();
+        }
+        return;
+    }
+
     const int yb0 = y0 & ~3;
     load_t pf[kPrefetch];
 #pragma unroll
@@ -895,8 +920,8 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
 template <int M, int KX, int PX>
 int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                         const Norm& norm, hipStream_t stream) {
-    const int lds = stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4);
-    dim3 grid(static_cast<unsigned>(L.count)), block(64);
+    const int lds = stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4, L.patch);
+    dim3 grid(static_cast<unsigned>(L.count)), block(L.patch == 14 ? 128 : 64);
     if (L.patch == 14) {
         if (out_dtype == 1)
             hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1, 14>), grid, block, lds, stream, plan, L.first, out, norm);
@@ -967,7 +992,7 @@ bool stream_shape_supported(int m, int kx, int px) {
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream) {
     if (L.count <= 0) return 0;
-    if (!stream_shape_supported(L.m, L.kx, L.px) || stream_wave_bytes(L.px, L.kx, 4) > kStreamLdsBudget)
+    if (!stream_shape_supported(L.m, L.kx, L.px) || stream_wave_bytes(L.px, L.kx, 4, L.patch) > kStreamLdsBudget)
         return static_cast<int>(hipErrorInvalidConfiguration);
 #define VP_STREAM_CASE(MM, KK, PP) \
     if (L.m == MM && L.kx == KK && L.px == PP) \
