@@ -640,11 +640,18 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     // sel[k]: the v_perm selector that moves bytes shift and shift + 1 of
     // the loaded dwords (shift = the lane's byte offset mod 4 in row phase k)
     // into the low bytes of two 16-bit halves and zeroes the high bytes.
+    // The x pass reads pixels [0, sx_start[last column] + KX) of the band's
+    // source span; a lane whose pixels all lie past that loads nothing: its
+    // offset is past every resource's range (such loads return zeros without
+    // a memory access), or, in a frame of 2 GiB or more, inside the frame.
+    // Neighbouring bands would otherwise fetch the same pixels twice.
+    const int span_px = sx_start[j0 + nbw - 1] + KX;
+    const bool lane_reads = PX * lane < span_px;
     uint32_t voff[kPrefetch], sel[kPrefetch];
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) {
         const uint32_t c = lane_off + static_cast<uint32_t>(k) * row_bytes;
-        voff[k] = c & ~3u;
+        voff[k] = lane_reads ? (c & ~3u) : 0x7FFFFFF0u;
         sel[k] = 0x0C000C00u | (c & 3u) | (((c & 3u) + 1u) << 16);
     }
     // Row yb + k of the block starting at yb: a resource based at the
