@@ -235,11 +235,12 @@ bool generic_subtile(const AxisFilter& fx, int32_t win, int32_t* rh, int32_t* cw
 // row y the table holds, per slot s < M, the weight of y in the output row
 // that has slot s at y (zero if that row does not read y), times 2^24 (the
 // kernel reads byte b as the f16 denormal b * 2^-24; the power of two is
-// exact both ways), then the close row of every output row.
+// exact both ways), then the close row of every output row.  With `fixed`
+// the weights are the int32 fixed-point weights of the uint8 writer instead.
 // Returns M, or -1 if the axis needs more than kSlotMax slots.
 constexpr float kSlotScale = 16777216.0f;   // 2^24
 
-int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
+int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words, bool fixed = false) {
     const int32_t n_in = f.n_in, n_out = f.n_out;
     const int32_t rows = n_in + vp::kSlotMax;
     std::vector<int32_t> close(n_out, 0);
@@ -267,8 +268,13 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
     (*words)[size_t(rows) * vp::kSlotWords + n_out] = INT32_MAX;   // close_row[n_out]: never reached
     float* w = reinterpret_cast<float*>(words->data());
     for (int32_t i = 0; i < n_out; ++i)
-        for (int32_t k = 0; k < f.count[i]; ++k)
-            w[size_t(f.start[i] + k) * vp::kSlotWords + i % m] = f.weight[size_t(i) * f.taps + k] * kSlotScale;
+        for (int32_t k = 0; k < f.count[i]; ++k) {
+            const size_t at = size_t(f.start[i] + k) * vp::kSlotWords + i % m;
+            if (fixed)
+                (*words)[at] = f.fixed[size_t(i) * f.taps + k];
+            else
+                w[at] = f.weight[size_t(i) * f.taps + k] * kSlotScale;
+        }
     std::memcpy(words->data() + size_t(rows) * vp::kSlotWords, close.data(), sizeof(int32_t) * n_out);
     return m;
 }
@@ -277,10 +283,11 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words) {
 // cut into bands of `band`; a band's source pixels start at the window start
 // of its first column, x0.  For column j: start[j] = (window start - x0),
 // lowered where needed so that start[j] + kx <= row_px, and the window's
-// weights shifted by the amount it was lowered, inside kx zero-padded taps.
+// weights shifted by the amount it was lowered, inside kx zero-padded taps
+// (with `fixed`, the int32 fixed-point weights of the uint8 writer).
 // The caller has checked that every window ends within row_px of its x0.
 void build_columns(const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px,
-                   std::vector<int32_t>* words) {
+                   std::vector<int32_t>* words, bool fixed = false) {
     words->assign(size_t(f.n_out) * (1 + kx), 0);
     int32_t* start = words->data();
     float* w = reinterpret_cast<float*>(words->data() + f.n_out);
@@ -290,8 +297,13 @@ void build_columns(const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px
         const int32_t s = l < row_px - kx ? l : row_px - kx;
         const int32_t shift = l - s;
         start[j] = s;
-        for (int32_t k = 0; k < f.count[j]; ++k)
-            w[size_t(j) * kx + shift + k] = f.weight[size_t(j) * f.taps + k];
+        for (int32_t k = 0; k < f.count[j]; ++k) {
+            const size_t at = size_t(j) * kx + shift + k;
+            if (fixed)
+                (*words)[f.n_out + at] = f.fixed[size_t(j) * f.taps + k];
+            else
+                w[at] = f.weight[size_t(j) * f.taps + k];
+        }
     }
 }
 
@@ -364,12 +376,13 @@ struct SlotEntry {
     int32_t m = -1;               // slots, or -1 if the axis needs too many
     std::vector<int32_t> words;
 };
-using ColumnKey = std::tuple<int32_t, int32_t, int32_t, int32_t, int32_t>;   // n_in, n_out, kx, band, row_px
+using ColumnKey = std::tuple<int32_t, int32_t, int32_t, int32_t, int32_t, bool>;   // n_in, n_out, kx, band, row_px, fixed
+using SlotKey = std::tuple<int32_t, int32_t, bool>;                                 // n_in, n_out, fixed
 
 constexpr size_t kTableCacheMax = 4096;
 std::mutex g_cache_mu;
 std::map<std::pair<int32_t, int32_t>, std::shared_ptr<const AxisEntry>> g_axis_cache;
-std::map<std::pair<int32_t, int32_t>, std::shared_ptr<const SlotEntry>> g_slot_cache;
+std::map<SlotKey, std::shared_ptr<const SlotEntry>> g_slot_cache;
 std::map<ColumnKey, std::shared_ptr<const std::vector<int32_t>>> g_column_cache;
 
 // The entry for `key`, built by `make` (outside the lock) on a miss.  If two
@@ -402,6 +415,92 @@ std::shared_ptr<const AxisEntry> make_axis_entry(int32_t n_in, int32_t n_out) {
     e->fixed_words.insert(e->fixed_words.end(), f.count.begin(), f.count.end());
     e->fixed_words.insert(e->fixed_words.end(), f.fixed.begin(), f.fixed.end());
     return e;
+}
+
+// One streaming work unit with its kernel shape, before the workgroup list
+// is laid out.
+struct Keyed {
+    std::tuple<int32_t, int32_t, int32_t> key;   // kernel shape (m, kx, px)
+    int32_t bands;                               // column bands (workgroups) of the unit
+    vp::StreamUnit unit;
+    int64_t cost;
+};
+
+// Output rows per streaming unit of an item: at most about max_src_rows
+// source rows, at least ten windows of source rows, a multiple of `group`
+// rows (the kernel's store group), and at least 16 rows (28 for groups of 14).
+int64_t unit_row_band(const vp::DevItem& d, int64_t max_src_rows, int64_t group) {
+    int64_t band = max_src_rows * d.h / d.H;
+    const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
+    band = std::max(band, min_band);
+    band = std::max<int64_t>((band + group - 1) / group * group, group == 4 ? 16 : 2 * group);
+    return std::min<int64_t>(band, d.h);   // h is a multiple of 2P: every band ends on a whole group
+}
+
+// Lays out the streaming units as launches and their workgroup lists.
+int32_t assemble_launches(const std::vector<Keyed>& keyed, int32_t P, Plan* p) {
+    // Units of one kernel shape form one launch, whatever their widths.  Its
+    // workgroups are listed explicitly: entry g (unit index | band << 20, or
+    // kNoWork) runs as workgroup g, and consecutive workgroups go to the
+    // eight XCDs in turn.  Units are taken eight at a time, and their bands
+    // are listed round by round (band 0 of all eight, then band 1, ...), so
+    // that all bands of one unit run on one XCD and share the source pixels
+    // of neighbouring bands through its L2; a unit with fewer bands than the
+    // others of its eight leaves empty entries.  Units are sorted by band
+    // count first, which keeps those rare.
+    if (keyed.size() > vp::kWgUnitMask + 1)
+        return fail(VP_ERR_CAPACITY, "batch has more than 2^20 streaming work units");
+    // order: by shape, then band count, then as generated (a grouping: the
+    // units of one item are consecutive and share both)
+    std::map<std::pair<std::tuple<int32_t, int32_t, int32_t>, int32_t>, std::vector<uint32_t>> groups;
+    for (size_t k = 0; k < keyed.size();) {
+        size_t k1 = k + 1;
+        while (k1 < keyed.size() && keyed[k1].key == keyed[k].key && keyed[k1].bands == keyed[k].bands) ++k1;
+        auto& g = groups[std::make_pair(keyed[k].key, keyed[k].bands)];
+        for (; k < k1; ++k) g.push_back(static_cast<uint32_t>(k));
+    }
+    std::vector<uint32_t> order;
+    order.reserve(keyed.size());
+    for (const auto& g : groups) order.insert(order.end(), g.second.begin(), g.second.end());
+    p->units.clear();
+    p->wgs.clear();
+    p->launches.clear();
+    p->units.reserve(keyed.size());
+    p->wgs.reserve(keyed.size() * 8);
+    for (size_t k0 = 0; k0 < order.size();) {
+        const auto& key0 = keyed[order[k0]].key;
+        size_t k1 = k0;
+        while (k1 < order.size() && keyed[order[k1]].key == key0) ++k1;
+        vp::StreamLaunch L{};
+        L.first = static_cast<int32_t>(p->wgs.size());
+        L.m = std::get<0>(key0);
+        L.kx = std::get<1>(key0);
+        L.px = std::get<2>(key0);
+        L.patch = P;
+        for (size_t c0 = k0; c0 < k1; c0 += 8) {
+            const size_t c1 = std::min(c0 + 8, k1);
+            int32_t rounds = 0;
+            for (size_t k = c0; k < c1; ++k) rounds = std::max(rounds, keyed[order[k]].bands);
+            const uint32_t u0 = static_cast<uint32_t>(p->units.size());
+            for (size_t k = c0; k < c1; ++k) {
+                const Keyed& e = keyed[order[k]];
+                p->units.push_back(e.unit);
+                L.cost += e.cost * e.bands;
+            }
+            for (int32_t r = 0; r < rounds; ++r)
+                for (size_t x = 0; x < 8; ++x) {
+                    const size_t k = c0 + x;
+                    p->wgs.push_back(k < c1 && r < keyed[order[k]].bands
+                                         ? (u0 + static_cast<uint32_t>(x)) | (static_cast<uint32_t>(r) << vp::kWgBandShift)
+                                         : vp::kNoWork);
+                }
+        }
+        L.count = static_cast<int32_t>(p->wgs.size()) - L.first;
+        p->launches.push_back(L);
+        k0 = k1;
+    }
+
+    return VP_OK;
 }
 
 int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
@@ -438,9 +537,9 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         *off = found->second.first;
         return &found->second.second->f;
     };
-    std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, std::shared_ptr<const SlotEntry>>> slot_tables;
+    std::map<SlotKey, std::pair<int32_t, std::shared_ptr<const SlotEntry>>> slot_tables;
     auto slots_for = [&](const AxisFilter& f, int32_t* off, int32_t* m) -> bool {
-        const auto key = std::make_pair(f.n_in, f.n_out);
+        const SlotKey key = std::make_tuple(f.n_in, f.n_out, false);
         auto found = slot_tables.find(key);
         if (found == slot_tables.end()) {
             auto e = cached(g_slot_cache, key, [&] {
@@ -457,7 +556,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     };
     std::map<ColumnKey, int32_t> column_tables;
     auto columns_for = [&](const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px) -> int32_t {
-        const ColumnKey key = std::make_tuple(f.n_in, f.n_out, kx, band, row_px);
+        const ColumnKey key = std::make_tuple(f.n_in, f.n_out, kx, band, row_px, false);
         auto found = column_tables.find(key);
         if (found == column_tables.end()) {
             auto e = cached(g_column_cache, key, [&] {
@@ -548,26 +647,15 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         }
     }
     const int64_t max_src_rows = wave_rows / (kWaveSlots * 8);
-    struct Keyed {
-        std::tuple<int32_t, int32_t, int32_t> key;   // kernel shape (m, kx, px)
-        int32_t bands;                               // column bands (workgroups) of the unit
-        vp::StreamUnit unit;
-        int64_t cost;
-    };
     std::vector<Keyed> keyed;
     keyed.reserve(static_cast<size_t>(stream_frames));
     for (int32_t b = 0; b < n; ++b) {
         const vp::DevItem& d = p->items[b];
         if (d.route != vp::kRouteStream) continue;
         const StreamShape& sh = shapes[b];
-        int64_t band = max_src_rows * d.h / d.H;
-        const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
-        band = std::max(band, min_band);
         // whole store groups: multiples of 4 rows for patch 16, whole
         // patch rows (14 output rows, stored at once) for patch 14
-        const int64_t unit = d.patch == 16 ? 4 : d.patch;
-        band = std::max<int64_t>((band + unit - 1) / unit * unit, d.patch == 16 ? 16 : 2 * d.patch);
-        band = std::min<int64_t>(band, d.h);   // h is a multiple of 2P: every band ends on a whole group
+        const int64_t band = unit_row_band(d, max_src_rows, d.patch == 16 ? 4 : d.patch);
         for (int32_t tt = 0; tt < d.t; ++tt) {
             const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
             const bool pair_units = d.patch == 14;   // both frames in one unit
@@ -588,66 +676,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
             }
         }
     }
-    // Units of one kernel shape form one launch, whatever their widths.  Its
-    // workgroups are listed explicitly: entry g (unit index | band << 20, or
-    // kNoWork) runs as workgroup g, and consecutive workgroups go to the
-    // eight XCDs in turn.  Units are taken eight at a time, and their bands
-    // are listed round by round (band 0 of all eight, then band 1, ...), so
-    // that all bands of one unit run on one XCD and share the source pixels
-    // of neighbouring bands through its L2; a unit with fewer bands than the
-    // others of its eight leaves empty entries.  Units are sorted by band
-    // count first, which keeps those rare.
-    if (keyed.size() > vp::kWgUnitMask + 1)
-        return fail(VP_ERR_CAPACITY, "batch has more than 2^20 streaming work units");
-    // order: by shape, then band count, then as generated (a grouping: the
-    // units of one item are consecutive and share both)
-    std::map<std::pair<std::tuple<int32_t, int32_t, int32_t>, int32_t>, std::vector<uint32_t>> groups;
-    for (size_t k = 0; k < keyed.size();) {
-        size_t k1 = k + 1;
-        while (k1 < keyed.size() && keyed[k1].key == keyed[k].key && keyed[k1].bands == keyed[k].bands) ++k1;
-        auto& g = groups[std::make_pair(keyed[k].key, keyed[k].bands)];
-        for (; k < k1; ++k) g.push_back(static_cast<uint32_t>(k));
-    }
-    std::vector<uint32_t> order;
-    order.reserve(keyed.size());
-    for (const auto& g : groups) order.insert(order.end(), g.second.begin(), g.second.end());
-    p->units.clear();
-    p->wgs.clear();
-    p->launches.clear();
-    p->units.reserve(keyed.size());
-    p->wgs.reserve(keyed.size() * 8);
-    for (size_t k0 = 0; k0 < order.size();) {
-        const auto& key0 = keyed[order[k0]].key;
-        size_t k1 = k0;
-        while (k1 < order.size() && keyed[order[k1]].key == key0) ++k1;
-        vp::StreamLaunch L{};
-        L.first = static_cast<int32_t>(p->wgs.size());
-        L.m = std::get<0>(key0);
-        L.kx = std::get<1>(key0);
-        L.px = std::get<2>(key0);
-        L.patch = P;
-        for (size_t c0 = k0; c0 < k1; c0 += 8) {
-            const size_t c1 = std::min(c0 + 8, k1);
-            int32_t rounds = 0;
-            for (size_t k = c0; k < c1; ++k) rounds = std::max(rounds, keyed[order[k]].bands);
-            const uint32_t u0 = static_cast<uint32_t>(p->units.size());
-            for (size_t k = c0; k < c1; ++k) {
-                const Keyed& e = keyed[order[k]];
-                p->units.push_back(e.unit);
-                L.cost += e.cost * e.bands;
-            }
-            for (int32_t r = 0; r < rounds; ++r)
-                for (size_t x = 0; x < 8; ++x) {
-                    const size_t k = c0 + x;
-                    p->wgs.push_back(k < c1 && r < keyed[order[k]].bands
-                                         ? (u0 + static_cast<uint32_t>(x)) | (static_cast<uint32_t>(r) << vp::kWgBandShift)
-                                         : vp::kNoWork);
-                }
-        }
-        L.count = static_cast<int32_t>(p->wgs.size()) - L.first;
-        p->launches.push_back(L);
-        k0 = k1;
-    }
+    if (const int32_t st = assemble_launches(keyed, P, p); st != VP_OK) return st;
 
     p->off_items = 0;
     p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
@@ -801,8 +830,34 @@ bool resize_tiles(const AxisFilter& fy, const AxisFilter& fx, int32_t* rb, int32
     return false;
 }
 
+// Shape of the uint8 streaming writer for an item, if it can take it: the
+// output width in bands of 64 columns (down to 16), each band's source span
+// within 64 lanes of px pixels, the column taps rounded up to 4, M slots.
+// The widest band that fits is taken: the horizontal pass costs the same per
+// output column whatever the band, and fewer bands unpack fewer pixels.
+bool resize_stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
+    if (m < 4 || m > vp::kSlotMax) return false;
+    const int32_t kx = round_up(fx.taps, 4);
+    if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
+    for (int32_t band = 64; band >= 16; band -= 16) {
+        const int32_t span = band_span(fx, band);
+        for (int32_t px = 2; px <= 4; ++px) {
+            if (!vp::resize_stream_supported(m, kx, px)) continue;
+            if (span > 64 * px || kx > 64 * px) continue;
+            sh->m = m;
+            sh->kx = kx;
+            sh->px = px;
+            sh->band = band;
+            sh->bands = (it.dst_w + band - 1) / band;
+            return true;
+        }
+    }
+    return false;
+}
+
 // Plan of vp_resize_batch: per item its frames in index order (no padding),
-// fixed-point tables, the output tile, and its output byte offset.
+// fixed-point tables, the route (streaming, or the tile kernel where an axis
+// does not fit the streaming shapes) and its output byte offset.
 int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
     if (items == nullptr) return fail(VP_ERR_NULL, "items is NULL");
     if (n < 1) return fail(VP_ERR_ARG, "n_items < 1");
@@ -821,19 +876,55 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
     p->launches.clear();
     p->generic_cost = 0;
     std::map<std::pair<int32_t, int32_t>, std::pair<int32_t, std::shared_ptr<const AxisEntry>>> axes;
+    auto append = [&](std::shared_ptr<const std::vector<int32_t>> words) -> int32_t {
+        const int32_t o = static_cast<int32_t>(p->table_words);
+        p->table_words += words->size();
+        p->tables.emplace_back(o, std::move(words));
+        return o;
+    };
     auto table_for = [&](int32_t n_in, int32_t n_out, int32_t* off) -> const AxisFilter* {
         const auto key = std::make_pair(n_in, n_out);
         auto found = axes.find(key);
         if (found == axes.end()) {
             auto e = cached(g_axis_cache, key, [&] { return make_axis_entry(n_in, n_out); });
-            const int32_t o = static_cast<int32_t>(p->table_words);
-            p->table_words += e->fixed_words.size();
-            p->tables.emplace_back(o, std::shared_ptr<const std::vector<int32_t>>(e, &e->fixed_words));
+            const int32_t o = append(std::shared_ptr<const std::vector<int32_t>>(e, &e->fixed_words));
             found = axes.emplace(key, std::make_pair(o, e)).first;
         }
         *off = found->second.first;
         return &found->second.second->f;
     };
+    std::map<SlotKey, std::pair<int32_t, std::shared_ptr<const SlotEntry>>> slot_tables;
+    auto slots_for = [&](const AxisFilter& f, int32_t* off, int32_t* m) -> bool {
+        const SlotKey key = std::make_tuple(f.n_in, f.n_out, true);
+        auto found = slot_tables.find(key);
+        if (found == slot_tables.end()) {
+            auto e = cached(g_slot_cache, key, [&] {
+                auto v = std::make_shared<SlotEntry>();
+                v->m = build_slots(f, &v->words, true);
+                return std::shared_ptr<const SlotEntry>(std::move(v));
+            });
+            const int32_t o = e->m > 0 ? append(std::shared_ptr<const std::vector<int32_t>>(e, &e->words)) : -1;
+            found = slot_tables.emplace(key, std::make_pair(o, e)).first;
+        }
+        *off = found->second.first;
+        *m = found->second.second->m;
+        return found->second.first >= 0;
+    };
+    std::map<ColumnKey, int32_t> column_tables;
+    auto columns_for = [&](const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px) -> int32_t {
+        const ColumnKey key = std::make_tuple(f.n_in, f.n_out, kx, band, row_px, true);
+        auto found = column_tables.find(key);
+        if (found == column_tables.end()) {
+            auto e = cached(g_column_cache, key, [&] {
+                auto v = std::make_shared<std::vector<int32_t>>();
+                build_columns(f, kx, band, row_px, v.get(), true);
+                return std::shared_ptr<const std::vector<int32_t>>(std::move(v));
+            });
+            found = column_tables.emplace(key, append(e)).first;
+        }
+        return found->second;
+    };
+    std::vector<StreamShape> shapes(n);
     int64_t bytes = 0, tiles = 0;
     for (int32_t b = 0; b < n; ++b) {
         const vp_item& it = items[b];
@@ -853,28 +944,73 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         const AxisFilter* fx = table_for(it.src_w, it.dst_w, &d.tx_off);
         d.ky = fy->taps;
         d.kx = fx->taps;
-        if (!resize_tiles(*fy, *fx, &d.rh, &d.cw))
-            return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
-                                             ": filter window too long for the uint8 writer's tiles");
-        d.hm = (it.dst_h + d.rh - 1) / d.rh;
-        d.wm = (it.dst_w + d.cw - 1) / d.cw;
-        d.route = vp::kRouteResize;
         d.patch = P;
         d.row_off = bytes;   // output byte offset of the item
         bytes += int64_t(it.n_idx) * it.dst_h * it.dst_w * 3;
-        tiles += int64_t(it.n_idx) * d.hm * d.wm;
+        int32_t m = 0;
+        StreamShape sh;
+        if (slots_for(*fy, &d.sy_off, &m) && resize_stream_shape(it, *fx, m, &sh)) {
+            d.route = vp::kRouteStream;
+            d.band = sh.band;
+            d.row_px = 64 * sh.px;
+            d.sx_off = columns_for(*fx, sh.kx, sh.band, d.row_px);
+            shapes[b] = sh;
+        } else {
+            if (!resize_tiles(*fy, *fx, &d.rh, &d.cw))
+                return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
+                                                 ": filter window too long for the uint8 writer's tiles");
+            d.hm = (it.dst_h + d.rh - 1) / d.rh;
+            d.wm = (it.dst_w + d.cw - 1) / d.cw;
+            d.route = vp::kRouteResize;
+            tiles += int64_t(it.n_idx) * d.hm * d.wm;
+            p->generic_cost += int64_t(8) * it.n_idx * it.src_h * it.src_w;   // about 8x the streaming cost per pixel
+        }
         if (tiles > INT32_MAX) return fail(VP_ERR_CAPACITY, "batch has more than 2^31-1 tiles");
         p->byte_off[b + 1] = bytes;
         p->prefix[b + 1] = static_cast<int32_t>(tiles);
     }
     p->total_rows = 0;
+
+    // Streaming units: one per (item, frame, band of output rows), the
+    // bands sized as for the float path (multiples of the kernel's store
+    // group of 4 rows).
+    constexpr int64_t kWaveSlots = 256 * 20;
+    int64_t wave_rows = 0;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp::DevItem& d = p->items[b];
+        if (d.route == vp::kRouteStream) wave_rows += int64_t(d.t) * shapes[b].bands * d.H;
+    }
+    const int64_t max_src_rows = wave_rows / (kWaveSlots * 8);
+    std::vector<Keyed> keyed;
+    for (int32_t b = 0; b < n; ++b) {
+        const vp::DevItem& d = p->items[b];
+        if (d.route != vp::kRouteStream) continue;
+        const StreamShape& sh = shapes[b];
+        const int64_t band = unit_row_band(d, max_src_rows, 4);
+        for (int32_t k = 0; k < d.t; ++k) {
+            for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
+                const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
+                Keyed e;
+                e.key = std::make_tuple(sh.m, sh.kx, sh.px);
+                e.bands = sh.bands;
+                e.unit.item = b;
+                e.unit.p = k;
+                e.unit.rows = i0 | (i1 << 16);
+                e.unit.flags = 0;
+                e.cost = int64_t(i1 - i0) * d.H / d.h * d.W;
+                keyed.push_back(e);
+            }
+        }
+    }
+    if (const int32_t st = assemble_launches(keyed, P, p); st != VP_OK) return st;
+
     p->off_items = 0;
     p->off_prefix = align_up(p->off_items + sizeof(vp::DevItem) * p->items.size());
     p->off_indices = align_up(p->off_prefix + sizeof(int32_t) * p->prefix.size());
     p->off_tables = align_up(p->off_indices + sizeof(int32_t) * p->indices.size());
     p->off_units = align_up(p->off_tables + sizeof(int32_t) * p->table_words);
-    p->off_wgs = p->off_units;
-    p->bytes = p->off_units;
+    p->off_wgs = align_up(p->off_units + sizeof(vp::StreamUnit) * p->units.size());
+    p->bytes = align_up(p->off_wgs + sizeof(uint32_t) * p->wgs.size());
     return VP_OK;
 }
 
@@ -1012,8 +1148,12 @@ int32_t side_for_device(int dev, Side** out) {
 // Runs the plan's launches: on the caller's stream if there is one, else
 // spread over the caller's stream and the side streams, largest estimated
 // work first onto the least loaded stream.
+// The plan's launches (the tile kernel, if it has tiles, and one per
+// streaming shape), spread over the caller's stream and the side streams by
+// estimated cost.  `resize`: the uint8 writer's kernels instead of the float
+// path's (out_dtype and norm unused).
 int32_t run_launches(const Plan& p, const vp::PlanView& view, void* out_rows, int32_t out_dtype,
-                     const vp::Norm& norm, hipStream_t stream) {
+                     const vp::Norm& norm, hipStream_t stream, bool resize = false) {
     struct Job {
         int32_t launch;   // index into p.launches, or -1 for the general kernel
         int64_t cost;
@@ -1023,7 +1163,11 @@ int32_t run_launches(const Plan& p, const vp::PlanView& view, void* out_rows, in
     for (size_t k = 0; k < p.launches.size(); ++k)
         jobs.push_back(Job{static_cast<int32_t>(k), p.launches[k].cost});
     auto launch = [&](const Job& j, hipStream_t st) -> int32_t {
-        if (j.launch < 0) {
+        if (resize) {
+            const int err = j.launch < 0 ? vp::launch_resize(view, out_rows, st)
+                                         : vp::launch_resize_stream(view, p.launches[j.launch], out_rows, st);
+            if (err != 0) return hip_fail(static_cast<hipError_t>(err), "uint8 writer launch");
+        } else if (j.launch < 0) {
             const int err = vp::launch_generic(view, out_rows, out_dtype, norm, st);
             if (err != 0) return hip_fail(static_cast<hipError_t>(err), "general kernel launch");
         } else {
@@ -1318,12 +1462,12 @@ int32_t vp_resize_batch(const vp_item* items, int32_t n_items, void* out_frames,
     view.tile_prefix = reinterpret_cast<const int32_t*>(ws + p.off_prefix);
     view.indices = reinterpret_cast<const int32_t*>(ws + p.off_indices);
     view.tables = reinterpret_cast<const int32_t*>(ws + p.off_tables);
-    view.units = nullptr;
-    view.wgs = nullptr;
+    view.units = reinterpret_cast<const vp::StreamUnit*>(ws + p.off_units);
+    view.wgs = reinterpret_cast<const uint32_t*>(ws + p.off_wgs);
     view.n_items = n_items;
     view.n_tiles = p.prefix[n_items];
-    const int err = vp::launch_resize(view, out_frames, stream);
-    if (err != 0) return hip_fail(static_cast<hipError_t>(err), "uint8 writer launch");
+    st = run_launches(p, view, out_frames, 0, vp::Norm{}, stream, true);
+    if (st != VP_OK) return st;
     if (t_stop != nullptr) {
         const hipError_t e = hipEventRecord(t_stop, stream);
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord (timing stop)");

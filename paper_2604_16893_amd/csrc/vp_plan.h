@@ -62,6 +62,11 @@ constexpr int stream_wave_bytes(int px, int kx, int elem_bytes, int patch = 16) 
                                  : 2 * 64 * px * 16 + 4 * 6 * patch * patch * elem_bytes;
 }
 
+// LDS of one uint8 streaming workgroup (one wave): its source row (64 * px
+// pixels, one int4 each) and the stage of four output rows of up to 64 RGB
+// pixels.
+constexpr int resize_stream_bytes(int px) { return 64 * px * 16 + 4 * 64 * 3; }
+
 // Kernel an item is routed to.
 enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1, kRoutePatch = 2, kRouteResize = 3 };
 
@@ -151,6 +156,9 @@ int launch_patchify(const PlanView& plan, void* out, int out_dtype, const Norm& 
 // uint8 cache writer over tile_prefix (items with route kRouteResize: rh x cw
 // output tiles, tables holding fixed-point weights); out is the byte buffer.
 int launch_resize(const PlanView& plan, void* out, hipStream_t stream);
+int launch_resize_stream(const PlanView& plan, const StreamLaunch& launch, void* out, hipStream_t stream);
+// Shapes (slots, column taps, pixels per lane) the uint8 streaming writer is built for.
+bool resize_stream_supported(int m, int kx, int px);
 // Position tables: one thread per output row; tile_prefix holds the items'
 // row offsets (cu).  vit / llm may be null.
 int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t rows,
