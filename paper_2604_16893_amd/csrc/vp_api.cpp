@@ -283,11 +283,10 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words, bool fixed
 // cut into bands of `band`; a band's source pixels start at the window start
 // of its first column, x0.  For column j: start[j] = (window start - x0),
 // lowered where needed so that start[j] + kx <= row_px, and the window's
-// weights shifted by the amount it was lowered, inside kx zero-padded taps
-// (with `fixed`, the int32 fixed-point weights of the uint8 writer).
+// weights shifted by the amount it was lowered, inside kx zero-padded taps.
 // The caller has checked that every window ends within row_px of its x0.
 void build_columns(const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px,
-                   std::vector<int32_t>* words, bool fixed = false) {
+                   std::vector<int32_t>* words) {
     words->assign(size_t(f.n_out) * (1 + kx), 0);
     int32_t* start = words->data();
     float* w = reinterpret_cast<float*>(words->data() + f.n_out);
@@ -297,14 +296,58 @@ void build_columns(const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px
         const int32_t s = l < row_px - kx ? l : row_px - kx;
         const int32_t shift = l - s;
         start[j] = s;
-        for (int32_t k = 0; k < f.count[j]; ++k) {
-            const size_t at = size_t(j) * kx + shift + k;
-            if (fixed)
-                (*words)[f.n_out + at] = f.fixed[size_t(j) * f.taps + k];
-            else
-                w[at] = f.weight[size_t(j) * f.taps + k];
-        }
+        for (int32_t k = 0; k < f.count[j]; ++k)
+            w[size_t(j) * kx + shift + k] = f.weight[size_t(j) * f.taps + k];
     }
+}
+
+// Column table of an x axis for the uint8 streaming writer.  The kernel
+// keeps each channel of a band's source row as signed bytes (value - 128),
+// and column j reads kx of them from a dword-aligned start s_j (its window
+// start relative to the band's x0, rounded down to a multiple of 4, lowered
+// so that s_j + kx <= row_px), with the window's weights shifted to match.
+// Each weight q splits into balanced base-256 digits, q = d2 2^16 + d1 2^8
+// + d0 with every digit in [-128, 127], so that byte dot products (dot4 of
+// four digits with four values) form the sums.  Per column: s_j / 4, then
+// 128 * (sum of q) + 2^21 (the offset of the values and the rounding term),
+// then for digits d0, d1, d2 the kx / 4 dwords of four taps' digits.
+// Returns false if a weight does not fit three digits.
+bool build_columns_dot(const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px,
+                       std::vector<int32_t>* words) {
+    const int32_t g = kx / 4;
+    const int32_t n = f.n_out;
+    words->assign(size_t(n) * (2 + 3 * g), 0);
+    int32_t* start = words->data();
+    int32_t* cterm = start + n;
+    int32_t* dig = cterm + n;
+    for (int32_t j = 0; j < n; ++j) {
+        const int32_t x0 = f.start[j / band * band];
+        const int32_t l = f.start[j] - x0;
+        const int32_t s = std::min(l & ~3, row_px - kx);
+        const int32_t shift = l - s;
+        if (s < 0 || shift + f.count[j] > kx) return false;
+        start[j] = s / 4;
+        int64_t sum = 0;
+        for (int32_t k = 0; k < f.count[j]; ++k) {
+            const int32_t q = f.fixed[size_t(j) * f.taps + k];
+            sum += q;
+            const int32_t d0 = ((q + 128) & 255) - 128;
+            const int32_t q1 = (q - d0) >> 8;
+            const int32_t d1 = ((q1 + 128) & 255) - 128;
+            const int32_t d2 = (q1 - d1) >> 8;
+            if (d2 < -128 || d2 > 127) return false;
+            const int32_t t = shift + k;
+            const int32_t d[3] = {d0, d1, d2};
+            for (int32_t c = 0; c < 3; ++c) {
+                uint32_t& w = reinterpret_cast<uint32_t&>(dig[(size_t(j) * 3 + c) * g + t / 4]);
+                w |= (static_cast<uint32_t>(d[c]) & 0xffu) << (8 * (t % 4));
+            }
+        }
+        const int64_t ct = 128 * sum + (int64_t(1) << 21);
+        if (ct > INT32_MAX || ct < INT32_MIN) return false;
+        cterm[j] = static_cast<int32_t>(ct);
+    }
+    return true;
 }
 
 struct StreamShape {
@@ -837,20 +880,17 @@ bool resize_tiles(const AxisFilter& fy, const AxisFilter& fx, int32_t* rb, int32
 // output column whatever the band, and fewer bands unpack fewer pixels.
 bool resize_stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
     if (m < 4 || m > vp::kSlotMax) return false;
-    const int32_t kx = round_up(fx.taps, 4);
+    const int32_t kx = round_up(fx.taps + 3, 4);   // any window start, rounded down to a dword
+    if (!vp::resize_stream_supported(m, kx, vp::kRsPx)) return false;
     if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
     for (int32_t band = 64; band >= 16; band -= 16) {
-        const int32_t span = band_span(fx, band);
-        for (int32_t px = 2; px <= 4; ++px) {
-            if (!vp::resize_stream_supported(m, kx, px)) continue;
-            if (span > 64 * px || kx > 64 * px) continue;
-            sh->m = m;
-            sh->kx = kx;
-            sh->px = px;
-            sh->band = band;
-            sh->bands = (it.dst_w + band - 1) / band;
-            return true;
-        }
+        if (band_span(fx, band) > 64 * vp::kRsPx) continue;
+        sh->m = m;
+        sh->kx = kx;
+        sh->px = vp::kRsPx;
+        sh->band = band;
+        sh->bands = (it.dst_w + band - 1) / band;
+        return true;
     }
     return false;
 }
@@ -911,16 +951,17 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         return found->second.first >= 0;
     };
     std::map<ColumnKey, int32_t> column_tables;
+    // the dot-product column table, or -1 if a weight does not fit its digits
     auto columns_for = [&](const AxisFilter& f, int32_t kx, int32_t band, int32_t row_px) -> int32_t {
         const ColumnKey key = std::make_tuple(f.n_in, f.n_out, kx, band, row_px, true);
         auto found = column_tables.find(key);
         if (found == column_tables.end()) {
             auto e = cached(g_column_cache, key, [&] {
                 auto v = std::make_shared<std::vector<int32_t>>();
-                build_columns(f, kx, band, row_px, v.get(), true);
+                if (!build_columns_dot(f, kx, band, row_px, v.get())) v->clear();
                 return std::shared_ptr<const std::vector<int32_t>>(std::move(v));
             });
-            found = column_tables.emplace(key, append(e)).first;
+            found = column_tables.emplace(key, e->empty() ? -1 : append(e)).first;
         }
         return found->second;
     };
@@ -949,11 +990,11 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         bytes += int64_t(it.n_idx) * it.dst_h * it.dst_w * 3;
         int32_t m = 0;
         StreamShape sh;
-        if (slots_for(*fy, &d.sy_off, &m) && resize_stream_shape(it, *fx, m, &sh)) {
+        if (slots_for(*fy, &d.sy_off, &m) && resize_stream_shape(it, *fx, m, &sh) &&
+            (d.sx_off = columns_for(*fx, sh.kx, sh.band, 64 * sh.px)) >= 0) {
             d.route = vp::kRouteStream;
             d.band = sh.band;
             d.row_px = 64 * sh.px;
-            d.sx_off = columns_for(*fx, sh.kx, sh.band, d.row_px);
             shapes[b] = sh;
         } else {
             if (!resize_tiles(*fy, *fx, &d.rh, &d.cw))

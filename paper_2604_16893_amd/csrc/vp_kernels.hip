@@ -950,24 +950,29 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 // One single-wave workgroup streams one sampled frame (or a band of its
 // output rows) top to bottom for one band of up to 64 output columns, in the
 // fixed-point order, horizontal pass first:
-//   * each source row arrives as in the float kernel (lane t loads PX
-//     pixels, four rows ahead); its bytes are unpacked to int32 with v_perm
-//     and written to the wave's LDS row, one int4 (r, g, b, -) per pixel;
-//   * lane j, output column j0 + j, forms the row's horizontal sums over KX
-//     taps (one 16-byte LDS read and three 24-bit multiply-adds per tap, its
-//     KX fixed-point weights in registers), rounds them to bytes, and adds
-//     them with wave-uniform weights into M rotating int32 accumulators, one
-//     per output row that is open at this row;
-//   * a closing output row is rounded to bytes into the wave's stage; every
-//     four rows the stage leaves as dword stores (a 64-column band row is
-//     192 bytes: three whole 64-byte sectors).
-// All sums are exact in int32: |q| < 2^23, values below 2^8, and the |q| of
-// a window sum to about 2^22.
-template <int M, int KX, int PX>
+//   * each source row arrives as in the float kernel (lane t loads pixels
+//     4t .. 4t + 3 of the band's span, four rows ahead); the lane aligns its
+//     12 bytes, gathers each channel's four bytes into one dword, offsets
+//     them to signed bytes (value - 128) and writes the three dwords to the
+//     wave's LDS row, kept as three byte planes;
+//   * lane j, output column j0 + j, reads KX / 4 dwords of each plane from
+//     its dword-aligned window start and forms the horizontal sum as byte
+//     dot products with the three base-256 digits of its weights (held in
+//     registers), d2 2^16 + d1 2^8 + d0, from a start value that restores
+//     the offset and adds the rounding term; the sum is rounded to a byte;
+//   * the bytes are added with wave-uniform weights into M rotating int32
+//     accumulators, one per output row open at this row; a closing output
+//     row is rounded to bytes into the wave's stage, and every four rows the
+//     stage leaves as dword stores (a 64-column band row is 192 bytes: three
+//     whole 64-byte sectors).
+// The horizontal sum is exact: its true value fits int32 (|q| of a window
+// sum to about 2^22, values below 2^8), so the partial sums, which wrap
+// modulo 2^32, end on it.
+template <int M, int KX>
 __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg0, uint8_t* out) {
-    constexpr int kRowPx = 64 * PX;
-    constexpr int kLoadDwords = PX == 4 ? 4 : 3;   // 3*PX bytes plus up to 3 of misalignment
-    constexpr int kStageRow = 3 * 64;              // stage bytes per output row
+    constexpr int G = KX / 4;                     // dwords per plane window
+    constexpr int kPlane = 64 * kRsPx;            // bytes per plane
+    constexpr int kStageRow = 3 * 64;             // stage bytes per output row
     extern __shared__ __align__(16) unsigned char smem[];
 
     const int lane = threadIdx.x;
@@ -985,27 +990,33 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     const int j0 = wave * band;
     const int nbw = min(band, w - j0);
 
-    int4* row = reinterpret_cast<int4*>(smem);                          // [kRowPx]
-    uint8_t* stage = smem + kRowPx * 16;                                // [4][kStageRow]
+    uint32_t* plane = reinterpret_cast<uint32_t*>(smem);   // [3][kPlane / 4]
+    uint8_t* stage = smem + 3 * kPlane;                     // [4][kStageRow]
 
-    // horizontal pass: column j0 + lane keeps its KX fixed-point weights
+    // column j0 + lane: window start (dword), start value, weight digits
     const cptr<int32_t> tables = as_const(plan.tables);
-    const cptr<int32_t> sx_start = tables + it->sx_off;
-    const cptr<int32_t> sx_q = sx_start + w;
+    const cptr<int32_t> cstart = tables + it->sx_off;
+    const cptr<int32_t> cterm = cstart + w;
+    const cptr<int32_t> cdig = cterm + w;
     const bool xlane = lane < nbw;
-    int sj = 0;
-    int32_t wx[KX];
+    int sw = 0, c0 = 0;
+    int32_t dg[3][G];
     {
         const int jx = xlane ? j0 + lane : w - 1;
-        const cptr<int32_t> src = sx_q + int64_t(jx) * KX;
-        if (xlane) sj = sx_start[jx];
+        const cptr<int32_t> src = cdig + int64_t(jx) * 3 * G;
+        if (xlane) {
+            sw = cstart[jx];
+            c0 = cterm[jx];
+        }
 #pragma unroll
-        for (int t = 0; t < KX; ++t) wx[t] = xlane ? src[t] : 0;
+        for (int d = 0; d < 3; ++d)
+#pragma unroll
+            for (int g = 0; g < G; ++g) dg[d][g] = xlane ? src[d * G + g] : 0;
     }
     const cptr<int32_t> xs = tables + it->tx_off;
     const int x0 = xs[j0];
     const cptr<int32_t> ys = tables + it->ty_off;
-    const cptr<int32_t> slot_q = tables + it->sy_off;                                   // [H + 6][8]
+    const cptr<int32_t> slot_q = tables + it->sy_off;                                       // [H + 6][8]
     const cptr<int32_t> close_row = tables + it->sy_off + (it->H + kSlotMax) * kSlotWords;  // [h]
 
     // the frame through buffer resources, as in the float kernel
@@ -1014,21 +1025,20 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     const uint32_t lead = static_cast<uint32_t>(fa & 3u);
     const uint32_t range = static_cast<uint32_t>((it->frame_bytes + lead + 3) & ~int64_t(3));
     const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
-    const uint32_t lane_off = lead + min(3u * static_cast<uint32_t>(x0 + PX * lane), row_bytes);
+    const uint32_t lane_off = lead + min(3u * static_cast<uint32_t>(x0 + kRsPx * lane), row_bytes);
     // lanes wholly past the pixels the horizontal pass reads load nothing
-    const int span_px = sx_start[j0 + nbw - 1] + KX;
-    const bool lane_reads = PX * lane < span_px;
-    uint32_t voff[kPrefetch], selb[kPrefetch];
+    const int span_px = 4 * cstart[j0 + nbw - 1] + KX;
+    const bool lane_reads = kRsPx * lane < span_px;
+    // voff[k]: the lane's dword-aligned offset in row phase k; sh[k]: its
+    // byte offset (v_alignbyte uses the low two bits)
+    uint32_t voff[kPrefetch], sh[kPrefetch];
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) {
         const uint32_t c = lane_off + static_cast<uint32_t>(k) * row_bytes;
         voff[k] = lane_reads ? (c & ~3u) : 0x7FFFFFF0u;
-        // v_perm selector: byte (c & 3) + m of the loaded dword pair into the
-        // low byte, zeros above (m = value index mod 4 is added per row)
-        selb[k] = 0x0C0C0C00u | (c & 3u);
+        sh[k] = c & 3u;
     }
-    using load_t = typename std::conditional<kLoadDwords == 4, uint4, uint3>::type;
-    auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> load_t {
+    auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> uint4 {
         const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
         const int64_t left = int64_t(range) - int64_t(o);
         const uint32_t n = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(left > 0 ? left : 0));
@@ -1037,13 +1047,8 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
         const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
         const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
             reinterpret_cast<void*>((uintptr_t(b_hi) << 32) | b_lo), (short)0, static_cast<int>(n), 0x00020000);
-        if constexpr (kLoadDwords == 4) {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b128(rb, voff[k], 0, 0);
-            return make_uint4(r[0], r[1], r[2], r[3]);
-        } else {
-            const auto r = __builtin_amdgcn_raw_buffer_load_b96(rb, voff[k], 0, 0);
-            return make_uint3(r[0], r[1], r[2]);
-        }
+        const auto r = __builtin_amdgcn_raw_buffer_load_b128(rb, voff[k], 0, 0);
+        return make_uint4(r[0], r[1], r[2], r[3]);
     };
 
     int32_t acc[M][3];
@@ -1069,61 +1074,45 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
         }
     };
 
-    auto process_row = [&](int y, load_t cur, uint32_t sb, cptr<int32_t> wr) __attribute__((always_inline)) {
-        uint32_t d[kLoadDwords + 1];
-        d[0] = cur.x;
-        d[1] = cur.y;
-        d[2] = cur.z;
-        if constexpr (kLoadDwords == 4) d[3] = cur.w;
-        d[kLoadDwords] = d[kLoadDwords - 1];
-        uint32_t sm[4];
-        sm[0] = sb;
-#pragma unroll
-        for (int m = 1; m < 4; ++m) sm[m] = sb + static_cast<uint32_t>(m);
-        // the lane's pixels into the LDS row
-#pragma unroll
-        for (int q = 0; q < PX; ++q) {
-            int32_t c3[3];
+    auto process_row = [&](int y, uint4 cur, uint32_t s8, cptr<int32_t> wr) __attribute__((always_inline)) {
+        // the lane's 12 bytes from its byte offset: r0 g0 b0 r1 | g1 b1 r2 g2 | b2 r3 g3 b3
+        const uint32_t a0 = __builtin_amdgcn_alignbyte(cur.y, cur.x, s8);
+        const uint32_t a1 = __builtin_amdgcn_alignbyte(cur.z, cur.y, s8);
+        const uint32_t a2 = __builtin_amdgcn_alignbyte(cur.w, cur.z, s8);
+        // per channel the four bytes in pixel order, then offset to signed
+        const uint32_t rr = __builtin_amdgcn_perm(a2, __builtin_amdgcn_perm(a1, a0, 0x00060300u), 0x05020100u);
+        const uint32_t gg = __builtin_amdgcn_perm(a2, __builtin_amdgcn_perm(a1, a0, 0x00070401u), 0x06020100u);
+        const uint32_t bb = __builtin_amdgcn_perm(__builtin_amdgcn_perm(a2, a1, 0x07040100u), a0, 0x07060502u);
+        plane[lane] = rr ^ 0x80808080u;
+        plane[kPlane / 4 + lane] = gg ^ 0x80808080u;
+        plane[2 * kPlane / 4 + lane] = bb ^ 0x80808080u;
+        wave_lds_fence();
+        // horizontal pass, rounded to bytes
+        int32_t h[3] = {0, 0, 0};
+        if (xlane) {
 #pragma unroll
             for (int c = 0; c < 3; ++c) {
-                const int v = 3 * q + c;
-                c3[c] = static_cast<int32_t>(__builtin_amdgcn_perm(d[(v >> 2) + 1], d[v >> 2], sm[v & 3]));
-            }
-            using i3 = int __attribute__((ext_vector_type(3)));
-            *reinterpret_cast<i3*>(row + PX * lane + q) = i3{c3[0], c3[1], c3[2]};
-        }
-        wave_lds_fence();
-        // horizontal pass, rounded to bytes (the sums start at the rounding
-        // term 2^21)
-        int32_t h0 = 0, h1 = 0, h2v = 0;
-        if (xlane) {
-            int32_t r0 = 1 << 21, r1 = 1 << 21, r2 = 1 << 21;
-            const int4* src = row + sj;
+                const uint32_t* pw = plane + c * (kPlane / 4) + sw;
+                int32_t s2 = 0, s1 = 0, s0 = c0;
 #pragma unroll
-            for (int g = 0; g < KX; g += 4) {
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int4 pv = src[g + t];
-                    asm volatile("" : : "v"(pv.w));
-                    r0 += __mul24(wx[g + t], pv.x);
-                    r1 += __mul24(wx[g + t], pv.y);
-                    r2 += __mul24(wx[g + t], pv.z);
+                for (int g = 0; g < G; ++g) {
+                    const int32_t v = static_cast<int32_t>(pw[g]);
+                    s2 = __builtin_amdgcn_sdot4(dg[2][g], v, s2, false);
+                    s1 = __builtin_amdgcn_sdot4(dg[1][g], v, s1, false);
+                    s0 = __builtin_amdgcn_sdot4(dg[0][g], v, s0, false);
                 }
+                const uint32_t sum = ((static_cast<uint32_t>(s2) << 8) + static_cast<uint32_t>(s1)) * 256u +
+                                     static_cast<uint32_t>(s0);
+                h[c] = min(max(static_cast<int32_t>(sum) >> 22, 0), 255);
             }
-            __builtin_amdgcn_sched_barrier(0);
-            h0 = min(max(r0 >> 22, 0), 255);
-            h1 = min(max(r1 >> 22, 0), 255);
-            h2v = min(max(r2 >> 22, 0), 255);
         }
         wave_lds_fence();
         // vertical pass: every open slot takes this row with its weight
 #pragma unroll
         for (int s = 0; s < M; ++s) {
             const int32_t ws = wr[s];
-            acc[s][0] += __mul24(ws, h0);
-            acc[s][1] += __mul24(ws, h1);
-            acc[s][2] += __mul24(ws, h2v);
+#pragma unroll
+            for (int c = 0; c < 3; ++c) acc[s][c] += __mul24(ws, h[c]);
         }
         while (y == next_close && base < i1) {   // wave-uniform
             const bool keep = base >= i0;
@@ -1132,9 +1121,9 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
                 if (slot == s) {
                     if (keep && xlane) {
                         uint8_t* st = stage + (base & 3) * kStageRow + 3 * lane;
-                        st[0] = static_cast<uint8_t>(min(max((acc[s][0] + (1 << 21)) >> 22, 0), 255));
-                        st[1] = static_cast<uint8_t>(min(max((acc[s][1] + (1 << 21)) >> 22, 0), 255));
-                        st[2] = static_cast<uint8_t>(min(max((acc[s][2] + (1 << 21)) >> 22, 0), 255));
+#pragma unroll
+                        for (int c = 0; c < 3; ++c)
+                            st[c] = static_cast<uint8_t>(min(max((acc[s][c] + (1 << 21)) >> 22, 0), 255));
                     }
                     acc[s][0] = acc[s][1] = acc[s][2] = 0;
                 }
@@ -1151,7 +1140,7 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     };
 
     const int yb0 = y0 & ~3;
-    load_t pf[kPrefetch];
+    uint4 pf[kPrefetch];
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) {
         pf[k] = load_row(yb0, k);
@@ -1162,19 +1151,20 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
 #pragma unroll
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
-            const load_t cur = pf[k];
+            const uint4 cur = pf[k];
             pf[k] = load_row(yb + kPrefetch, k);
-            if (y >= y0 && y < y1) process_row(y, cur, selb[k], wblk + k * kSlotWords);
+            if (y >= y0 && y < y1) process_row(y, cur, sh[k], wblk + k * kSlotWords);
         }
     }
 }
 
-template <int M, int KX, int PX>
+template <int M, int KX>
 int launch_resize_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
-    hipLaunchKernelGGL((resize_stream_kernel<M, KX, PX>), dim3(static_cast<unsigned>(L.count)), dim3(64),
-                       resize_stream_bytes(PX), stream, plan, L.first, static_cast<uint8_t*>(out));
+    hipLaunchKernelGGL((resize_stream_kernel<M, KX>), dim3(static_cast<unsigned>(L.count)), dim3(64),
+                       resize_stream_bytes(), stream, plan, L.first, static_cast<uint8_t*>(out));
     return static_cast<int>(hipGetLastError());
 }
+
 }  // namespace
 
 int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t rows,
@@ -1194,18 +1184,16 @@ int launch_resize(const PlanView& plan, void* out, hipStream_t stream) {
 }
 
 bool resize_stream_supported(int m, int kx, int px) {
-    return m >= 4 && m <= 6 && (kx == 4 || kx == 8 || kx == 12 || kx == 16) && px >= 2 && px <= 4;
+    return m >= 4 && m <= 6 && kx >= 8 && kx <= 20 && kx % 4 == 0 && px == kRsPx;
 }
 
 int launch_resize_stream(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
     if (L.count <= 0) return 0;
     if (!resize_stream_supported(L.m, L.kx, L.px)) return static_cast<int>(hipErrorInvalidConfiguration);
-#define VP_RS_CASE(MM, KK, PP) \
-    if (L.m == MM && L.kx == KK && L.px == PP) return launch_resize_stream_shape<MM, KK, PP>(plan, L, out, stream);
-#define VP_RS_KX(MM, PP) VP_RS_CASE(MM, 4, PP) VP_RS_CASE(MM, 8, PP) VP_RS_CASE(MM, 12, PP) VP_RS_CASE(MM, 16, PP)
-    VP_RS_KX(4, 2) VP_RS_KX(5, 2) VP_RS_KX(6, 2)
-    VP_RS_KX(4, 3) VP_RS_KX(5, 3) VP_RS_KX(6, 3)
-    VP_RS_KX(4, 4) VP_RS_KX(5, 4) VP_RS_KX(6, 4)
+#define VP_RS_CASE(MM, KK) \
+    if (L.m == MM && L.kx == KK) return launch_resize_stream_shape<MM, KK>(plan, L, out, stream);
+#define VP_RS_KX(MM) VP_RS_CASE(MM, 8) VP_RS_CASE(MM, 12) VP_RS_CASE(MM, 16) VP_RS_CASE(MM, 20)
+    VP_RS_KX(4) VP_RS_KX(5) VP_RS_KX(6)
 #undef VP_RS_KX
 #undef VP_RS_CASE
     return static_cast<int>(hipErrorInvalidConfiguration);

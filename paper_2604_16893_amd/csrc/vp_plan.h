@@ -62,10 +62,12 @@ constexpr int stream_wave_bytes(int px, int kx, int elem_bytes, int patch = 16) 
                                  : 2 * 64 * px * 16 + 4 * 6 * patch * patch * elem_bytes;
 }
 
-// LDS of one uint8 streaming workgroup (one wave): its source row (64 * px
-// pixels, one int4 each) and the stage of four output rows of up to 64 RGB
-// pixels.
-constexpr int resize_stream_bytes(int px) { return 64 * px * 16 + 4 * 64 * 3; }
+// uint8 streaming writer: pixels per lane (a band's source span is at most
+// 64 * kRsPx pixels), and the LDS of one workgroup (one wave): its source
+// row as three byte planes and the stage of four output rows of up to 64
+// RGB pixels.
+constexpr int kRsPx = 4;
+constexpr int resize_stream_bytes() { return 3 * 64 * kRsPx + 4 * 64 * 3; }
 
 // Kernel an item is routed to.
 enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1, kRoutePatch = 2, kRouteResize = 3 };
