@@ -660,8 +660,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> load_t {
         // (the block is wave-uniform; say so, or the descriptor would be built per lane)
         const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
-        const int64_t left = int64_t(range) - int64_t(o);
-        const uint32_t n = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(left > 0 ? left : 0));
+        const uint32_t n = __builtin_amdgcn_readfirstlane(range > o ? range - o : 0u);
         const uintptr_t bp = fa - lead + o;
         const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
         const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
@@ -1040,8 +1039,7 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     }
     auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> uint4 {
         const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
-        const int64_t left = int64_t(range) - int64_t(o);
-        const uint32_t n = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(left > 0 ? left : 0));
+        const uint32_t n = __builtin_amdgcn_readfirstlane(range > o ? range - o : 0u);
         const uintptr_t bp = fa - lead + o;
         const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
         const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
@@ -1087,24 +1085,26 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
         plane[kPlane / 4 + lane] = gg ^ 0x80808080u;
         plane[2 * kPlane / 4 + lane] = bb ^ 0x80808080u;
         wave_lds_fence();
-        // horizontal pass, rounded to bytes
-        int32_t h[3] = {0, 0, 0};
-        if (xlane) {
+        // horizontal pass, rounded to bytes: digit by digit, each sum
+        // starting from the previous one times 2^8 (idle lanes have zero
+        // weights and start value, and form 0)
+        int32_t h[3];
 #pragma unroll
-            for (int c = 0; c < 3; ++c) {
-                const uint32_t* pw = plane + c * (kPlane / 4) + sw;
-                int32_t s2 = 0, s1 = 0, s0 = c0;
+        for (int c = 0; c < 3; ++c) {
+            const uint32_t* pw = plane + c * (kPlane / 4) + sw;
+            int32_t v[G];
 #pragma unroll
-                for (int g = 0; g < G; ++g) {
-                    const int32_t v = static_cast<int32_t>(pw[g]);
-                    s2 = __builtin_amdgcn_sdot4(dg[2][g], v, s2, false);
-                    s1 = __builtin_amdgcn_sdot4(dg[1][g], v, s1, false);
-                    s0 = __builtin_amdgcn_sdot4(dg[0][g], v, s0, false);
-                }
-                const uint32_t sum = ((static_cast<uint32_t>(s2) << 8) + static_cast<uint32_t>(s1)) * 256u +
-                                     static_cast<uint32_t>(s0);
-                h[c] = min(max(static_cast<int32_t>(sum) >> 22, 0), 255);
-            }
+            for (int g = 0; g < G; ++g) v[g] = static_cast<int32_t>(pw[g]);
+            int32_t sum = 0;
+#pragma unroll
+            for (int g = 0; g < G; ++g) sum = __builtin_amdgcn_sdot4(dg[2][g], v[g], sum, false);
+            sum = static_cast<int32_t>(static_cast<uint32_t>(sum) << 8);
+#pragma unroll
+            for (int g = 0; g < G; ++g) sum = __builtin_amdgcn_sdot4(dg[1][g], v[g], sum, false);
+            sum = static_cast<int32_t>((static_cast<uint32_t>(sum) << 8) + static_cast<uint32_t>(c0));
+#pragma unroll
+            for (int g = 0; g < G; ++g) sum = __builtin_amdgcn_sdot4(dg[0][g], v[g], sum, false);
+            h[c] = min(max(sum >> 22, 0), 255);
         }
         wave_lds_fence();
         // vertical pass: every open slot takes this row with its weight
