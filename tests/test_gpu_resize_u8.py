@@ -32,10 +32,10 @@ def _free_memory():
     torch.cuda.empty_cache()
 
 
-def run(items, sentinel=8):
+def run(items, sentinel=8, patch=16):
     """items: list of (device frames, indices, h, w).  Returns the output
     buffer (without the sentinel bytes) and frame_off."""
-    vitems = [vp.Item(f, idx, h, w) for f, idx, h, w in items]
+    vitems = [vp.Item(f, idx, h, w, patch) for f, idx, h, w in items]
     off, ws = vp.vp_resize_layout(vitems)
     total = int(off[-1])
     out = torch.full((total + sentinel,), 0xA5, dtype=torch.uint8, device=DEV)
@@ -117,3 +117,24 @@ def test_resize_u8_rollout_workload_full_size():
 
 def test_resize_u8_ragged_workload_full_size():
     _sampled_workload_check(workloads.config(3), 10, 52)
+
+
+def test_resize_u8_patch14_widths():
+    """Sizes on the patch-14 grid (multiples of 28): column bands of 64 that
+    end in a 60-column band (252) or a 48-column one (112), so the stage
+    leaves 45 and 36 dwords per band row."""
+    specs = [(1, 333, 257, [0], 308, 252), (3, 70, 90, [2, 0, 1], 56, 112), (2, 720, 1280, [1, 0], 252, 448)]
+    items, hosts = [], []
+    for k, (n, H, W, idx, h, w) in enumerate(specs):
+        it, fd = _video(470 + k, n, H, W)
+        items.append((fd, np.asarray(idx, np.int32), h, w))
+        hosts.append(workloads.frames_np(it))
+    log(f"case patch14_widths: {[(s[0], s[1], s[2], s[4], s[5]) for s in specs]}")
+    out, off = run(items, patch=14)
+    for k, (fd, idx, h, w) in enumerate(items):
+        got = frames_of(out, off, k, len(idx), h, w).cpu().numpy()
+        ref = oracle.resize_u8_item(hosts[k], idx, h, w, patch=14)
+        diff = int((got != ref).sum())
+        log(f"patch14_widths item {k}: {diff} differing bytes of {ref.size}")
+        assert diff == 0
+
