@@ -325,6 +325,9 @@ PATCH14 = [
     ("p14_identity_f32", [(2, 56, 84, [1, 0], 56, 84)], "f32"),
     ("p14_ragged_bf16", [(5, 70, 90, [4, 1, 3], 56, 112), (1, 333, 257, [0], 308, 252),
                          (3, 480, 854, [0, 1, 2], 112, 196)], "bf16"),
+    # an image and an odd count in fp32: one wave of the pair writes both
+    # temporal halves of the (twice as large) stage
+    ("p14_image_odd_f32", [(1, 333, 257, [0], 308, 252), (4, 150, 260, [3, 0, 2], 84, 140)], "f32"),
 ]
 
 
