@@ -236,8 +236,9 @@ bool generic_subtile(const AxisFilter& fx, int32_t win, int32_t* rh, int32_t* cw
 // that has slot s at y (zero if that row does not read y), times 2^24 (the
 // kernel reads byte b as the f16 denormal b * 2^-24; the power of two is
 // exact both ways), then the close row of every output row.  With `fixed`
-// the weights are the int32 fixed-point weights of the uint8 writer instead.
-// Returns M, or -1 if the axis needs more than kSlotMax slots.
+// the weights are the int32 fixed-point weights of the uint8 writer instead,
+// which keeps up to kSlotWords slots (three registers each).
+// Returns M, or -1 if the axis needs more slots than that.
 constexpr float kSlotScale = 16777216.0f;   // 2^24
 
 int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words, bool fixed = false) {
@@ -262,7 +263,7 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words, bool fixed
         open += delta[y];
         most = open > most ? open : most;
     }
-    if (most > vp::kSlotMax) return -1;
+    if (most > (fixed ? vp::kSlotWords : vp::kSlotMax)) return -1;
     const int32_t m = most < 4 ? 4 : most;
     words->assign(size_t(rows) * vp::kSlotWords + n_out + 1, 0);
     (*words)[size_t(rows) * vp::kSlotWords + n_out] = INT32_MAX;   // close_row[n_out]: never reached
@@ -879,7 +880,7 @@ bool resize_tiles(const AxisFilter& fy, const AxisFilter& fx, int32_t* rb, int32
 // The widest band that fits is taken: the horizontal pass costs the same per
 // output column whatever the band, and fewer bands unpack fewer pixels.
 bool resize_stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
-    if (m < 4 || m > vp::kSlotMax) return false;
+    if (m < 4 || m > vp::kSlotWords) return false;
     const int32_t kx = round_up(fx.taps + 3, 4);   // any window start, rounded down to a dword
     if (!vp::resize_stream_supported(m, kx, vp::kRsPx)) return false;
     if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;

@@ -1184,7 +1184,7 @@ int launch_resize(const PlanView& plan, void* out, hipStream_t stream) {
 }
 
 bool resize_stream_supported(int m, int kx, int px) {
-    return m >= 4 && m <= 6 && kx >= 8 && kx <= 20 && kx % 4 == 0 && px == kRsPx;
+    return m >= 4 && m <= kSlotWords && kx >= 8 && kx <= 20 && kx % 4 == 0 && px == kRsPx;
 }
 
 int launch_resize_stream(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
@@ -1193,7 +1193,7 @@ int launch_resize_stream(const PlanView& plan, const StreamLaunch& L, void* out,
 #define VP_RS_CASE(MM, KK) \
     if (L.m == MM && L.kx == KK) return launch_resize_stream_shape<MM, KK>(plan, L, out, stream);
 #define VP_RS_KX(MM) VP_RS_CASE(MM, 8) VP_RS_CASE(MM, 12) VP_RS_CASE(MM, 16) VP_RS_CASE(MM, 20)
-    VP_RS_KX(4) VP_RS_KX(5) VP_RS_KX(6)
+    VP_RS_KX(4) VP_RS_KX(5) VP_RS_KX(6) VP_RS_KX(7) VP_RS_KX(8)
 #undef VP_RS_KX
 #undef VP_RS_CASE
     return static_cast<int>(hipErrorInvalidConfiguration);

@@ -60,6 +60,8 @@ CASES = [
     # name, [(n_src, H, W, indices, h, w)]
     ("downscale_2x", [(3, 64, 96, [2, 0], 32, 48 + 16)]),
     ("upscale_1_6x", [(2, 40, 50, [1, 0, 1], 64, 96)]),
+    ("upscale_2x_eight_slots", [(2, 48, 80, [1, 0], 96, 160)]),
+    ("upscale_2_5x_tiles", [(1, 64, 64, [0], 160, 160)]),
     ("identity", [(2, 64, 96, [1], 64, 96)]),
     ("mixed_axes", [(2, 100, 60, [0, 1], 64, 96)]),
     ("odd_width_854", [(2, 60, 854, [1, 0], 32, 640)]),
