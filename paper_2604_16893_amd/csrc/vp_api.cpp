@@ -236,9 +236,9 @@ bool generic_subtile(const AxisFilter& fx, int32_t win, int32_t* rh, int32_t* cw
 // that has slot s at y (zero if that row does not read y), times 2^24 (the
 // kernel reads byte b as the f16 denormal b * 2^-24; the power of two is
 // exact both ways), then the close row of every output row.  With `fixed`
-// the weights are the int32 fixed-point weights of the uint8 writer instead,
-// which keeps up to kSlotWords slots (three registers each).
-// Returns M, or -1 if the axis needs more slots than that.
+// the weights are the int32 fixed-point weights of the uint8 writer instead.
+// Returns M, or -1 if the axis needs more than kSlotWords slots (which
+// kernel shapes take that many is up to the caller).
 constexpr float kSlotScale = 16777216.0f;   // 2^24
 
 int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words, bool fixed = false) {
@@ -263,7 +263,7 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words, bool fixed
         open += delta[y];
         most = open > most ? open : most;
     }
-    if (most > (fixed ? vp::kSlotWords : vp::kSlotMax)) return -1;
+    if (most > vp::kSlotWords) return -1;
     const int32_t m = most < 4 ? 4 : most;
     words->assign(size_t(rows) * vp::kSlotWords + n_out + 1, 0);
     (*words)[size_t(rows) * vp::kSlotWords + n_out] = INT32_MAX;   // close_row[n_out]: never reached
@@ -377,7 +377,7 @@ int32_t band_span(const AxisFilter& fx, int32_t band) {
 // budget is checked with float32 staging, so the routing does not depend on
 // the output type.
 bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t patch, StreamShape* sh) {
-    if (m < 4 || m > vp::kSlotMax) return false;
+    if (m < 4 || m > vp::kSlotWords) return false;
     const int32_t mm = m;
     const int32_t kx = round_up(fx.taps, 4);
     // every load of a frame row (up to kSlotMax + 8 rows past the last one) stays below 4 GiB

@@ -1231,8 +1231,11 @@ int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& n
 // per lane where the accumulators still fit the registers of a 1024-thread
 // block (M <= 5).
 bool stream_shape_supported(int m, int kx, int px) {
-    if (m < 4 || m > 6 || (kx != 4 && kx != 8 && kx != 12 && kx != 16)) return false;
-    return px == 2 || (px == 3 && m <= 5);
+    if (m < 4 || (kx != 4 && kx != 8 && kx != 12 && kx != 16)) return false;
+    if (m <= 6) return px == 2 || (px == 3 && m <= 5);
+    // 7 or 8 open rows: vertical upscales up to about 2x, whose x axis has
+    // short windows too
+    return m <= kSlotWords && px == 2 && kx <= 8;
 }
 
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
@@ -1247,6 +1250,7 @@ int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int ou
     VP_STREAM_CASE(MM, 4, PP) VP_STREAM_CASE(MM, 8, PP) VP_STREAM_CASE(MM, 12, PP) VP_STREAM_CASE(MM, 16, PP)
     VP_STREAM_KX(4, 2) VP_STREAM_KX(5, 2) VP_STREAM_KX(6, 2)
     VP_STREAM_KX(4, 3) VP_STREAM_KX(5, 3)
+    VP_STREAM_CASE(7, 4, 2) VP_STREAM_CASE(7, 8, 2) VP_STREAM_CASE(8, 4, 2) VP_STREAM_CASE(8, 8, 2)
 #undef VP_STREAM_KX
 #undef VP_STREAM_CASE
     return static_cast<int>(hipErrorInvalidValue);

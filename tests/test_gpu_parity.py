@@ -140,11 +140,12 @@ SMALL = [
     ("partial_band", [(2, 300, 450, [1, 0], 128, 160)], "bf16"),
     ("unaligned_frames", [(4, 75, 101, [1, 2, 3], 64, 96)], "f32"),
     ("narrow_frame", [(2, 100, 40, [0, 1], 64, 32)], "f32"),
-    # a mild vertical upscale on the streaming kernel (several output rows
-    # close on one source row); a stronger one on the general kernel, with an
-    # odd count whose padded pair is one frame twice
+    # vertical upscales on the streaming kernel (several output rows close
+    # on one source row; 2x keeps eight rows open); a stronger one on the
+    # general kernel, with an odd count whose padded pair is one frame twice
     ("upscale_stream", [(2, 60, 70, [1, 0], 64, 96)], "f32"),
-    ("upscale_general_odd", [(3, 40, 50, [2, 0, 1], 64, 96)], "bf16"),
+    ("upscale_2x_eight_slots", [(2, 48, 80, [1, 0], 96, 160), (1, 120, 160, [0], 224, 288)], "bf16"),
+    ("upscale_general_odd", [(3, 24, 40, [2, 0, 1], 64, 96)], "bf16"),
 ]
 
 
