@@ -535,7 +535,7 @@ __device__ __forceinline__ void lds_barrier() {
 //     whole (the two patches of a merge window are one contiguous run).
 template <int M, int KX, int PX, int OUT_BF16, int P>
 __global__ __launch_bounds__(P == 16 ? 64 : 128) __attribute__((amdgpu_waves_per_eu(
-    M * PX > 12 || 3 * M * PX + KX >= 52 || (OUT_BF16 == 0 && M * PX >= 12) ? 4 : 5)))
+    M * PX > 12 || KX >= 20 || 3 * M * PX + KX >= 52 || (OUT_BF16 == 0 && M * PX >= 12) ? 4 : 5)))
 void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     static_assert(P == 16 || P == 14, "patch 16 or 14");
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
@@ -1184,7 +1184,7 @@ int launch_resize(const PlanView& plan, void* out, hipStream_t stream) {
 }
 
 bool resize_stream_supported(int m, int kx, int px) {
-    return m >= 4 && m <= kSlotWords && kx >= 8 && kx <= 20 && kx % 4 == 0 && px == kRsPx;
+    return m >= 4 && m <= kSlotWords && kx >= 8 && kx <= 32 && kx % 4 == 0 && px == kRsPx;
 }
 
 int launch_resize_stream(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
@@ -1192,7 +1192,8 @@ int launch_resize_stream(const PlanView& plan, const StreamLaunch& L, void* out,
     if (!resize_stream_supported(L.m, L.kx, L.px)) return static_cast<int>(hipErrorInvalidConfiguration);
 #define VP_RS_CASE(MM, KK) \
     if (L.m == MM && L.kx == KK) return launch_resize_stream_shape<MM, KK>(plan, L, out, stream);
-#define VP_RS_KX(MM) VP_RS_CASE(MM, 8) VP_RS_CASE(MM, 12) VP_RS_CASE(MM, 16) VP_RS_CASE(MM, 20)
+#define VP_RS_KX(MM) VP_RS_CASE(MM, 8) VP_RS_CASE(MM, 12) VP_RS_CASE(MM, 16) VP_RS_CASE(MM, 20) \
+    VP_RS_CASE(MM, 24) VP_RS_CASE(MM, 28) VP_RS_CASE(MM, 32)
     VP_RS_KX(4) VP_RS_KX(5) VP_RS_KX(6) VP_RS_KX(7) VP_RS_KX(8)
 #undef VP_RS_KX
 #undef VP_RS_CASE
@@ -1231,11 +1232,12 @@ int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& n
 // per lane where the accumulators still fit the registers of a 1024-thread
 // block (M <= 5).
 bool stream_shape_supported(int m, int kx, int px) {
-    if (m < 4 || (kx != 4 && kx != 8 && kx != 12 && kx != 16)) return false;
-    if (m <= 6) return px == 2 || (px == 3 && m <= 5);
-    // 7 or 8 open rows: vertical upscales up to about 2x, whose x axis has
-    // short windows too
-    return m <= kSlotWords && px == 2 && kx <= 8;
+    if (m < 4 || kx < 4 || kx > 32 || kx % 4 != 0) return false;
+    if (m > 6)   // 7 or 8 open rows: vertical upscales up to about 2x, whose x axis has short windows too
+        return m <= kSlotWords && px == 2 && kx <= 8;
+    if (kx <= 16) return px == 2 || (px == 3 && m <= 5);
+    // windows of 17 to 32 taps: x downscales of about 3.75x to 7.5x
+    return px == 2 || (px == 3 && m <= 5 && kx <= 24);
 }
 
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
@@ -1251,6 +1253,11 @@ int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int ou
     VP_STREAM_KX(4, 2) VP_STREAM_KX(5, 2) VP_STREAM_KX(6, 2)
     VP_STREAM_KX(4, 3) VP_STREAM_KX(5, 3)
     VP_STREAM_CASE(7, 4, 2) VP_STREAM_CASE(7, 8, 2) VP_STREAM_CASE(8, 4, 2) VP_STREAM_CASE(8, 8, 2)
+#define VP_STREAM_LONG(MM, PP) \
+    VP_STREAM_CASE(MM, 20, PP) VP_STREAM_CASE(MM, 24, PP) VP_STREAM_CASE(MM, 28, PP) VP_STREAM_CASE(MM, 32, PP)
+    VP_STREAM_LONG(4, 2) VP_STREAM_LONG(5, 2) VP_STREAM_LONG(6, 2)
+    VP_STREAM_CASE(4, 20, 3) VP_STREAM_CASE(4, 24, 3) VP_STREAM_CASE(5, 20, 3) VP_STREAM_CASE(5, 24, 3)
+#undef VP_STREAM_LONG
 #undef VP_STREAM_KX
 #undef VP_STREAM_CASE
     return static_cast<int>(hipErrorInvalidValue);

@@ -146,6 +146,12 @@ SMALL = [
     ("upscale_stream", [(2, 60, 70, [1, 0], 64, 96)], "f32"),
     ("upscale_2x_eight_slots", [(2, 48, 80, [1, 0], 96, 160), (1, 120, 160, [0], 224, 288)], "bf16"),
     ("upscale_general_odd", [(3, 24, 40, [2, 0, 1], 64, 96)], "bf16"),
+    # long x windows (downscales of 4x to 7x): 28 taps with two pixels per
+    # lane in 16-column bands, 20 taps with three in 32-column bands, and a
+    # 4K-wide frame (24 taps)
+    ("long_window_28", [(2, 90, 1600, [1, 0], 32, 256)], "f32"),
+    ("long_window_20_px3", [(3, 200, 1800, [2, 0], 64, 384)], "bf16"),
+    ("long_window_4k_width", [(2, 540, 3840, [0, 1], 96, 672)], "bf16"),
 ]
 
 
@@ -329,6 +335,7 @@ PATCH14 = [
     # an image and an odd count in fp32: one wave of the pair writes both
     # temporal halves of the (twice as large) stage
     ("p14_image_odd_f32", [(1, 333, 257, [0], 308, 252), (4, 150, 260, [3, 0, 2], 84, 140)], "f32"),
+    ("p14_long_window", [(2, 540, 3840, [1, 0], 84, 672)], "bf16"),
 ]
 
 

@@ -67,6 +67,7 @@ CASES = [
     ("odd_width_854", [(2, 60, 854, [1, 0], 32, 640)]),
     ("tall_strong_downscale", [(2, 2400, 100, [1, 0], 64, 32)]),
     ("wide_strong_downscale", [(1, 300, 3000, [0], 32, 96)]),
+    ("long_window_4k_width", [(2, 540, 3840, [1, 0], 96, 672)]),
     ("single_pixel", [(1, 1, 1, [0], 32, 32)]),
     ("ragged_batch", [(4, 75, 101, [3, 1, 2], 64, 96), (1, 333, 257, [0], 320, 256),
                       (5, 120, 200, [4, 0], 96, 160)]),
