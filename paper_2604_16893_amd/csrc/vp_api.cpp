@@ -351,6 +351,58 @@ bool build_columns_dot(const AxisFilter& f, int32_t kx, int32_t band, int32_t ro
     return true;
 }
 
+// Column table of an x axis for the uint8 writer's MFMA form.  Output
+// columns go in bands of 64, each of four blocks of 16; block b's window is
+// the 64 source pixels from the window start of its first column, and the
+// horizontal sums of a block are a 16 x 16 x 64 byte matrix product per
+// channel and weight digit.  Per band: the four window starts (absolute
+// source pixels), then for each block and digit d2, d1, d0 the B operand of
+// v_mfma_i32_16x16x64_i8 for every lane l (column l % 16 of the block, window
+// taps 16 (l / 16) .. 16 (l / 16) + 15) as four dwords of digit bytes.  After
+// the bands, per column the start value 128 * (sum of q) + 2^21.  Returns
+// false if a block's columns do not fit its window or a weight its digits.
+bool build_columns_mfma(const AxisFilter& f, std::vector<int32_t>* words) {
+    const int32_t n = f.n_out;
+    const int32_t bands = (n + 63) / 64;
+    words->assign(size_t(bands) * vp::kRsMfmaBandWords + n, 0);
+    int32_t* cterm = words->data() + size_t(bands) * vp::kRsMfmaBandWords;
+    for (int32_t bd = 0; bd < bands; ++bd) {
+        int32_t* bw = words->data() + size_t(bd) * vp::kRsMfmaBandWords;
+        for (int32_t blk = 0; blk < 4; ++blk) {
+            const int32_t j0 = bd * 64 + blk * 16;
+            const int32_t xb = j0 < n ? f.start[j0] : (blk > 0 ? bw[blk - 1] : 0);
+            bw[blk] = xb;
+            for (int32_t nn = 0; nn < 16 && j0 + nn < n; ++nn) {
+                const int32_t j = j0 + nn;
+                if (f.start[j] + f.count[j] - xb > 64) return false;
+                int64_t sum = 0;
+                for (int32_t t = 0; t < f.count[j]; ++t) {
+                    const int32_t q = f.fixed[size_t(j) * f.taps + t];
+                    sum += q;
+                    const int32_t d0 = ((q + 128) & 255) - 128;
+                    const int32_t q1 = (q - d0) >> 8;
+                    const int32_t d1 = ((q1 + 128) & 255) - 128;
+                    const int32_t d2 = (q1 - d1) >> 8;
+                    if (d2 < -128 || d2 > 127) return false;
+                    const int32_t k = f.start[j] + t - xb;        // tap position in the window
+                    const int32_t lane = (k / 16) * 16 + nn;       // the lane holding (k, column nn)
+                    const int32_t byte = k % 16;
+                    const int32_t d[3] = {d2, d1, d0};
+                    for (int32_t dg = 0; dg < 3; ++dg) {
+                        uint32_t& w = reinterpret_cast<uint32_t&>(
+                            bw[4 + ((blk * 3 + dg) * 64 + lane) * 4 + byte / 4]);
+                        w |= (static_cast<uint32_t>(d[dg]) & 0xffu) << (8 * (byte % 4));
+                    }
+                }
+                const int64_t ct = 128 * sum + (int64_t(1) << 21);
+                if (ct > INT32_MAX || ct < INT32_MIN) return false;
+                cterm[j] = static_cast<int32_t>(ct);
+            }
+        }
+    }
+    return true;
+}
+
 struct StreamShape {
     int32_t m = 0, kx = 0, px = 0, band = 0, bands = 0;
 };
@@ -966,6 +1018,21 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         }
         return found->second;
     };
+    std::map<std::pair<int32_t, int32_t>, int32_t> mfma_tables;
+    // the MFMA column table, or -1 if a block's columns do not fit its window
+    auto mfma_columns_for = [&](const AxisFilter& f) -> int32_t {
+        const ColumnKey key = std::make_tuple(f.n_in, f.n_out, vp::kRsMfmaWindow, 64, 0, true);
+        auto found = mfma_tables.find(std::make_pair(f.n_in, f.n_out));
+        if (found == mfma_tables.end()) {
+            auto e = cached(g_column_cache, key, [&] {
+                auto v = std::make_shared<std::vector<int32_t>>();
+                if (!build_columns_mfma(f, v.get())) v->clear();
+                return std::shared_ptr<const std::vector<int32_t>>(std::move(v));
+            });
+            found = mfma_tables.emplace(std::make_pair(f.n_in, f.n_out), e->empty() ? -1 : append(e)).first;
+        }
+        return found->second;
+    };
     std::vector<StreamShape> shapes(n);
     int64_t bytes = 0, tiles = 0;
     for (int32_t b = 0; b < n; ++b) {
@@ -991,7 +1058,24 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         bytes += int64_t(it.n_idx) * it.dst_h * it.dst_w * 3;
         int32_t m = 0;
         StreamShape sh;
-        if (slots_for(*fy, &d.sy_off, &m) && resize_stream_shape(it, *fx, m, &sh) &&
+        const bool slots = slots_for(*fy, &d.sy_off, &m);
+        // The MFMA form costs about the same per source row whatever the
+        // window; byte dot products cost in proportion to it.  Measured, the
+        // MFMA form wins from 16 dot-product taps (windows of 10 or more).
+        const bool long_x = round_up(fx->taps + 3, 4) >= 16;
+        if (slots && long_x && m >= 4 && m <= vp::kSlotWords && (d.sx_off = mfma_columns_for(*fx)) >= 0 &&
+            int64_t(it.src_h + vp::kSlotMax + 20) * it.src_w * 3 + 256 < (int64_t(1) << 32)) {
+            // the MFMA form: bands of 64 columns, blocks of 16 with 64-pixel windows
+            d.route = vp::kRouteStream;
+            d.band = 64;
+            d.row_px = 0;
+            sh.m = m;
+            sh.kx = vp::kRsMfmaWindow;
+            sh.px = vp::kRsPx;
+            sh.band = 64;
+            sh.bands = (it.dst_w + 63) / 64;
+            shapes[b] = sh;
+        } else if (slots && resize_stream_shape(it, *fx, m, &sh) &&
             (d.sx_off = columns_for(*fx, sh.kx, sh.band, 64 * sh.px)) >= 0) {
             d.route = vp::kRouteStream;
             d.band = sh.band;

@@ -1158,6 +1158,205 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     }
 }
 
+// The uint8 writer's MFMA form, for x axes whose 16-column blocks read at
+// most 64 source pixels (downscales up to about 3x).  One single-wave
+// workgroup per (frame, band of output rows, band of 64 output columns), as
+// above, but source rows go in chunks of 16:
+//   * horizontal pass, per block of 16 columns and per channel: lane l loads
+//     its own 16 pixels of source row (chunk + l % 16) from the block's
+//     window (16 (l / 16) .. +15), de-interleaves them into one channel's
+//     signed bytes (value - 128): the A operand of v_mfma_i32_16x16x64_i8
+//     (rows x window taps); the B operands are the block's weight digits
+//     (taps x columns), held in registers.  Three products, one per digit,
+//     from zero, zero and the start value, give the sums exactly (each stays
+//     below 2^30); they are combined, rounded to bytes and packed four rows
+//     per dword into LDS, [channel][column][16 rows];
+//   * vertical pass: lane j reads its column's 16 bytes per channel and
+//     adds the chunk's rows into the M rotating slots as before.
+template <int M>
+__global__ __launch_bounds__(64) void resize_mfma_kernel(PlanView plan, int wg0, uint8_t* out) {
+    using v4i = int __attribute__((ext_vector_type(4)));
+    constexpr int kStageRow = 3 * 64;
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    const int lane = threadIdx.x;
+    const uint32_t wg = as_const(plan.wgs)[wg0 + static_cast<int>(blockIdx.x)];
+    if (wg == kNoWork) return;
+    const int u = static_cast<int>(wg & kWgUnitMask);
+    const int wave = static_cast<int>(wg >> kWgBandShift);
+    const cptr<StreamUnit> up = as_const(plan.units) + u;
+    const int u_item = up->item, u_k = up->p, u_rows = up->rows;
+    const cptr<DevItem> it = as_const(plan.items) + u_item;
+    const int i0 = u_rows & 0xffff;
+    const int i1 = u_rows >> 16;
+    const int w = it->w;
+    const int j0 = wave * 64;
+    const int nbw = min(64, w - j0);
+    const bool xlane = lane < nbw;
+
+    uint8_t* hbuf = smem;                         // [3][64 columns][16 rows]
+    uint8_t* stage = smem + 3 * 64 * 16;          // [4][kStageRow]
+
+    const cptr<int32_t> tables = as_const(plan.tables);
+    const cptr<int32_t> band_tab = tables + it->sx_off + wave * kRsMfmaBandWords;
+    const cptr<int32_t> cterm = tables + it->sx_off + ((w + 63) / 64) * kRsMfmaBandWords;
+    // B operands (weight digits) and start values of the lane's columns
+    v4i wt[4][3];
+    int32_t cb[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+#pragma unroll
+        for (int d = 0; d < 3; ++d) {
+            const cptr<int32_t> src = band_tab + 4 + ((b * 3 + d) * 64 + lane) * 4;
+            wt[b][d] = v4i{src[0], src[1], src[2], src[3]};
+        }
+        const int j = j0 + 16 * b + (lane & 15);
+        cb[b] = j < w ? cterm[j] : 0;
+    }
+    const cptr<int32_t> ys = tables + it->ty_off;
+    const cptr<int32_t> slot_q = tables + it->sy_off;
+    const cptr<int32_t> close_row = tables + it->sy_off + (it->H + kSlotMax) * kSlotWords;
+
+    // the frame through one buffer resource (loads past it return zeros)
+    const int f = as_const(plan.indices)[it->idx_off + u_k];
+    const uintptr_t fa = reinterpret_cast<uintptr_t>(it->frames + int64_t(f) * it->frame_bytes);
+    const uint32_t lead = static_cast<uint32_t>(fa & 3u);
+    const uint32_t range = static_cast<uint32_t>((it->frame_bytes + lead + 3) & ~int64_t(3));
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(fa - lead), (short)0, static_cast<int>(range), 0x00020000);
+    const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
+
+    int32_t acc[M][3];
+#pragma unroll
+    for (int s = 0; s < M; ++s) acc[s][0] = acc[s][1] = acc[s][2] = 0;
+    const int y0 = ys[i0];
+    const int y1 = close_row[i1 - 1] + 1;
+    int base = i0;
+    while (base > 0 && close_row[base - 1] >= y0) --base;
+    int slot = base % M;
+    int next_close = close_row[base];
+
+    auto flush = [&](int i) __attribute__((always_inline)) {
+        const int nd = 3 * nbw / 4;
+        uint8_t* const ob = out + it->row_off + ((int64_t(u_k) * it->h + (i - 3)) * w + j0) * 3;
+        for (int e = lane; e < 4 * nd; e += 64) {
+            const int r = e / nd;
+            const int d = e - r * nd;
+            const uint32_t v = *reinterpret_cast<const uint32_t*>(stage + r * kStageRow + 4 * d);
+            __builtin_nontemporal_store(v, reinterpret_cast<uint32_t*>(ob + int64_t(r) * w * 3 + 4 * d));
+        }
+    };
+
+    const int g = lane >> 4;          // k group of the lane: window taps 16 g .. 16 g + 15
+    for (int yc = y0 & ~15; yc < y1; yc += 16) {
+        // ---- horizontal pass of source rows yc .. yc + 15
+        const uint32_t rowoff = lead + static_cast<uint32_t>(yc + (lane & 15)) * row_bytes;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const uint32_t o = rowoff + 3u * static_cast<uint32_t>(band_tab[b] + 16 * g);
+            const uint32_t oa = o & ~3u;
+            const uint32_t sh = o & 3u;
+            const auto l0 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, oa, 0, 0);
+            const auto l1 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, oa + 16, 0, 0);
+            const auto l2 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, oa + 32, 0, 0);
+            const uint32_t l3 = __builtin_amdgcn_raw_buffer_load_b32(rsrc, oa + 48, 0, 0);
+            const uint32_t raw[13] = {l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3],
+                                      l2[0], l2[1], l2[2], l2[3], l3};
+            uint32_t a[12];
+#pragma unroll
+            for (int q = 0; q < 12; ++q) a[q] = __builtin_amdgcn_alignbyte(raw[q + 1], raw[q], sh);
+            // channel planes of the lane's 16 pixels, as signed bytes
+            v4i pc[3];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t x0w = a[3 * k], x1w = a[3 * k + 1], x2w = a[3 * k + 2];
+                pc[0][k] = static_cast<int>(__builtin_amdgcn_perm(x2w, __builtin_amdgcn_perm(x1w, x0w, 0x00060300u), 0x05020100u) ^ 0x80808080u);
+                pc[1][k] = static_cast<int>(__builtin_amdgcn_perm(x2w, __builtin_amdgcn_perm(x1w, x0w, 0x00070401u), 0x06020100u) ^ 0x80808080u);
+                pc[2][k] = static_cast<int>(__builtin_amdgcn_perm(__builtin_amdgcn_perm(x2w, x1w, 0x07040100u), x0w, 0x07060502u) ^ 0x80808080u);
+            }
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                const v4i zero = {0, 0, 0, 0};
+                const v4i cs = {cb[b], cb[b], cb[b], cb[b]};
+                const v4i s2 = __builtin_amdgcn_mfma_i32_16x16x64_i8(pc[c], wt[b][0], zero, 0, 0, 0);
+                const v4i s1 = __builtin_amdgcn_mfma_i32_16x16x64_i8(pc[c], wt[b][1], zero, 0, 0, 0);
+                const v4i s0 = __builtin_amdgcn_mfma_i32_16x16x64_i8(pc[c], wt[b][2], cs, 0, 0, 0);
+                // D[row 4 g + r][column l % 16]: rows 4g .. 4g + 3 of the lane's column
+                uint32_t hb[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const uint32_t sum = (static_cast<uint32_t>(s2[r]) << 16) + (static_cast<uint32_t>(s1[r]) << 8) +
+                                         static_cast<uint32_t>(s0[r]);
+                    hb[r] = static_cast<uint32_t>(min(max(static_cast<int32_t>(sum) >> 22, 0), 255));
+                }
+                // packed with v_perm: left to itself the compiler fuses two of
+                // the clamps with the packing into a 16-bit v_ashr_pk_u8_i32 and
+                // ORs the other two bytes over its undefined upper half
+                const uint32_t packed = __builtin_amdgcn_perm(hb[1], hb[0], 0x0C0C0400u) |
+                                        __builtin_amdgcn_perm(hb[3], hb[2], 0x04000C0Cu);
+                *reinterpret_cast<uint32_t*>(hbuf + c * 1024 + (16 * b + (lane & 15)) * 16 + 4 * g) = packed;
+            }
+        }
+        wave_lds_fence();
+        // ---- vertical pass over the chunk's rows
+        uint4 hv[3];
+#pragma unroll
+        for (int c = 0; c < 3; ++c) hv[c] = *reinterpret_cast<const uint4*>(hbuf + c * 1024 + lane * 16);
+        wave_lds_fence();
+        const cptr<int32_t> wblk = slot_q + yc * kSlotWords;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int y = yc + r;
+            if (y < y0 || y >= y1) continue;   // wave-uniform
+            const uint32_t dw = r >> 2;
+            const uint32_t sel = 8u * static_cast<uint32_t>(r & 3);
+            int32_t h[3];
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                const uint32_t word = dw == 0 ? hv[c].x : dw == 1 ? hv[c].y : dw == 2 ? hv[c].z : hv[c].w;
+                h[c] = static_cast<int32_t>(__builtin_amdgcn_ubfe(word, sel, 8));
+            }
+            const cptr<int32_t> wr = wblk + r * kSlotWords;
+#pragma unroll
+            for (int s = 0; s < M; ++s) {
+                const int32_t ws = wr[s];
+#pragma unroll
+                for (int c = 0; c < 3; ++c) acc[s][c] += __mul24(ws, h[c]);
+            }
+            while (y == next_close && base < i1) {   // wave-uniform
+                const bool keep = base >= i0;
+#pragma unroll
+                for (int s = 0; s < M; ++s) {
+                    if (slot == s) {
+                        if (keep && xlane) {
+                            uint8_t* st = stage + (base & 3) * kStageRow + 3 * lane;
+#pragma unroll
+                            for (int c = 0; c < 3; ++c)
+                                st[c] = static_cast<uint8_t>(min(max((acc[s][c] + (1 << 21)) >> 22, 0), 255));
+                        }
+                        acc[s][0] = acc[s][1] = acc[s][2] = 0;
+                    }
+                }
+                if (keep && (base & 3) == 3) {
+                    wave_lds_fence();
+                    flush(base);
+                    wave_lds_fence();
+                }
+                ++base;
+                slot = slot + 1 == M ? 0 : slot + 1;
+                next_close = close_row[base];
+            }
+        }
+    }
+}
+
+template <int M>
+int launch_resize_mfma_shape(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
+    hipLaunchKernelGGL((resize_mfma_kernel<M>), dim3(static_cast<unsigned>(L.count)), dim3(64),
+                       resize_mfma_bytes(), stream, plan, L.first, static_cast<uint8_t*>(out));
+    return static_cast<int>(hipGetLastError());
+}
+
 template <int M, int KX>
 int launch_resize_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
     hipLaunchKernelGGL((resize_stream_kernel<M, KX>), dim3(static_cast<unsigned>(L.count)), dim3(64),
@@ -1189,6 +1388,17 @@ bool resize_stream_supported(int m, int kx, int px) {
 
 int launch_resize_stream(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
     if (L.count <= 0) return 0;
+    if (L.kx == kRsMfmaWindow) {
+        if (L.px != kRsPx) return static_cast<int>(hipErrorInvalidConfiguration);
+        switch (L.m) {
+            case 4: return launch_resize_mfma_shape<4>(plan, L, out, stream);
+            case 5: return launch_resize_mfma_shape<5>(plan, L, out, stream);
+            case 6: return launch_resize_mfma_shape<6>(plan, L, out, stream);
+            case 7: return launch_resize_mfma_shape<7>(plan, L, out, stream);
+            case 8: return launch_resize_mfma_shape<8>(plan, L, out, stream);
+            default: return static_cast<int>(hipErrorInvalidConfiguration);
+        }
+    }
     if (!resize_stream_supported(L.m, L.kx, L.px)) return static_cast<int>(hipErrorInvalidConfiguration);
 #define VP_RS_CASE(MM, KK) \
     if (L.m == MM && L.kx == KK) return launch_resize_stream_shape<MM, KK>(plan, L, out, stream);

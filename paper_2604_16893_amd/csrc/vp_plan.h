@@ -68,6 +68,13 @@ constexpr int stream_wave_bytes(int px, int kx, int elem_bytes, int patch = 16) 
 // RGB pixels.
 constexpr int kRsPx = 4;
 constexpr int resize_stream_bytes() { return 3 * 64 * kRsPx + 4 * 64 * 3; }
+// The writer's MFMA form (launch shape kx = kRsMfmaWindow): column table words
+// per band of 64 columns (four window starts, then 4 blocks x 3 digits x 64
+// lanes x 4 dwords), and its LDS: the horizontal pass's bytes of 16 source
+// rows for 64 columns and 3 channels, and the stage.
+constexpr int kRsMfmaWindow = 64;
+constexpr int kRsMfmaBandWords = 4 + 4 * 3 * 64 * 4;
+constexpr int resize_mfma_bytes() { return 3 * 64 * 16 + 4 * 64 * 3; }
 
 // Kernel an item is routed to.
 enum Route : int32_t { kRouteGeneric = 0, kRouteStream = 1, kRoutePatch = 2, kRouteResize = 3 };

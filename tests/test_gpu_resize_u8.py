@@ -68,6 +68,12 @@ CASES = [
     ("tall_strong_downscale", [(2, 2400, 100, [1, 0], 64, 32)]),
     ("wide_strong_downscale", [(1, 300, 3000, [0], 32, 96)]),
     ("long_window_4k_width", [(2, 540, 3840, [1, 0], 96, 672)]),
+    # x downscale of 3.9x: 16-column blocks read more than 64 pixels, so the
+    # byte dot-product kernel takes it instead of the matrix-core one
+    ("dot4_kernel_3_9x", [(2, 100, 1000, [0, 1], 64, 256)]),
+    # matrix-core horizontal pass (windows of 10+ taps) with a vertical
+    # upscale that keeps seven rows open
+    ("mfma_seven_slots", [(2, 40, 240, [1, 0], 64, 96)]),
     ("single_pixel", [(1, 1, 1, [0], 32, 32)]),
     ("ragged_batch", [(4, 75, 101, [3, 1, 2], 64, 96), (1, 333, 257, [0], 320, 256),
                       (5, 120, 200, [4, 0], 96, 160)]),
