@@ -74,6 +74,9 @@ CASES = [
     # matrix-core horizontal pass (windows of 10+ taps) with a vertical
     # upscale that keeps seven rows open
     ("mfma_seven_slots", [(2, 40, 240, [1, 0], 64, 96)]),
+    # matrix-core form on rows and frames that start off 4-byte boundaries
+    # (3 W = 783 bytes per row, 58,725 bytes per frame)
+    ("mfma_unaligned_rows", [(3, 75, 261, [2, 0, 1], 32, 96)]),
     ("single_pixel", [(1, 1, 1, [0], 32, 32)]),
     ("ragged_batch", [(4, 75, 101, [3, 1, 2], 64, 96), (1, 333, 257, [0], 320, 256),
                       (5, 120, 200, [4, 0], 96, 160)]),
