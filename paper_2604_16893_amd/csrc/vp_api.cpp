@@ -353,7 +353,8 @@ bool build_columns_dot(const AxisFilter& f, int32_t kx, int32_t band, int32_t ro
 
 // Column table of an x axis for the uint8 writer's MFMA form.  Output
 // columns go in bands of 64, each of four blocks of 16; block b's window is
-// the 64 source pixels from the window start of its first column, and the
+// the 64 source pixels from the window start of its first column (for a
+// band's last block: the 64 that end where its columns' taps end), and the
 // horizontal sums of a block are a 16 x 16 x 64 byte matrix product per
 // channel and weight digit.  Per band: the four window starts (absolute
 // source pixels), then for each block and digit d2, d1, d0 the B operand of
@@ -370,7 +371,16 @@ bool build_columns_mfma(const AxisFilter& f, std::vector<int32_t>* words) {
         int32_t* bw = words->data() + size_t(bd) * vp::kRsMfmaBandWords;
         for (int32_t blk = 0; blk < 4; ++blk) {
             const int32_t j0 = bd * 64 + blk * 16;
-            const int32_t xb = j0 < n ? f.start[j0] : (blk > 0 ? bw[blk - 1] : 0);
+            int32_t xb = j0 < n ? f.start[j0] : (blk > 0 ? bw[blk - 1] : 0);
+            // the band's last block ends its window where its columns' taps
+            // end: its pixels past that belong to the next band, whose own
+            // wave reads them
+            const bool last = j0 < n && (blk == 3 || j0 + 16 >= n);
+            if (last) {
+                int32_t end = 0;
+                for (int32_t j = j0; j < j0 + 16 && j < n; ++j) end = std::max(end, f.start[j] + f.count[j]);
+                xb = std::max(0, std::min(xb, end - 64));
+            }
             bw[blk] = xb;
             for (int32_t nn = 0; nn < 16 && j0 + nn < n; ++nn) {
                 const int32_t j = j0 + nn;
