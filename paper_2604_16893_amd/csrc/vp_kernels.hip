@@ -735,16 +735,20 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             for (int g = 0; g < KX; g += 4) {
                 // four taps at a time: bounds the LDS values held in registers
                 __builtin_amdgcn_sched_barrier(0);
+                float4 q[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) q[k] = src[g + k];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    const float4 q = src[g + k];
-                    // read the whole 16-byte slot: on gfx950 a 16-byte LDS
-                    // read is cheaper than a 12-byte one
-                    asm volatile("" : : "v"(q.w));
-                    r0 = fmaf(wx[g + k], q.x, r0);
-                    r1 = fmaf(wx[g + k], q.y, r1);
-                    r2 = fmaf(wx[g + k], q.z, r2);
+                    r0 = fmaf(wx[g + k], q[k].x, r0);
+                    r1 = fmaf(wx[g + k], q[k].y, r1);
+                    r2 = fmaf(wx[g + k], q[k].z, r2);
                 }
+                // the whole 16-byte slots are read (on gfx950 a 16-byte LDS
+                // read is cheaper than a 12-byte one); using the fourth words
+                // once per group, not per read, lets the four reads issue
+                // back to back under one wait
+                asm volatile("" : : "v"(q[0].w), "v"(q[1].w), "v"(q[2].w), "v"(q[3].w));
             }
             __builtin_amdgcn_sched_barrier(0);
             const float v0 = r0 * a0;
