@@ -152,6 +152,10 @@ SMALL = [
     ("long_window_28", [(2, 90, 1600, [1, 0], 32, 256)], "f32"),
     ("long_window_20_px3", [(3, 200, 1800, [2, 0], 64, 384)], "bf16"),
     ("long_window_4k_width", [(2, 540, 3840, [0, 1], 96, 672)], "bf16"),
+    # windows of 2 mod 4 taps (the last group of the x pass holds two):
+    # 10 taps with two and with three pixels per lane
+    ("taps10_px2", [(2, 180, 640, [1, 0], 96, 288)], "f32"),
+    ("taps10_px3", [(3, 90, 300, [2, 0], 32, 128)], "bf16"),
 ]
 
 
@@ -336,6 +340,7 @@ PATCH14 = [
     # temporal halves of the (twice as large) stage
     ("p14_image_odd_f32", [(1, 333, 257, [0], 308, 252), (4, 150, 260, [3, 0, 2], 84, 140)], "f32"),
     ("p14_long_window", [(2, 540, 3840, [1, 0], 84, 672)], "bf16"),
+    ("p14_taps10_px3", [(3, 180, 640, [0, 2], 84, 280)], "f32"),
 ]
 
 
