@@ -846,7 +846,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
 
     // Source row y (its values in hv) into the slots; then closes the output
     // rows whose close row is y.
-    auto process_row = [&](int y, const uint32_t (&hv)[kPairs], cptr<float> wr) __attribute__((always_inline)) {
+    auto process_row = [&](int y, const uint32_t (&hv)[kPairs], const float (&wr)[M]) __attribute__((always_inline)) {
         float v[V];
 #pragma unroll
         for (int q = 0; q < V; ++q) {
@@ -918,7 +918,16 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     }
 
     for (int yb = yb0; yb < y1; yb += kPrefetch) {
+        // the block's slot weights, loaded together ahead of its rows: one
+        // wait for scalar loads per block, not per row (a block starts at a
+        // row below H and the table has kSlotMax rows past the frame's
+        // last, so all four rows are inside it)
         const cptr<float> wblk = slot_w + yb * kSlotWords;
+        float wk[kPrefetch][M];
+#pragma unroll
+        for (int k = 0; k < kPrefetch; ++k)
+#pragma unroll
+            for (int s = 0; s < M; ++s) wk[k][s] = wblk[k * kSlotWords + s];
 #pragma unroll
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
@@ -931,7 +940,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
 #pragma unroll
             for (int q = 0; q < kPairs; ++q) asm volatile("" : : "v"(hv[q]));
             pf[k] = load_row(yb + kPrefetch, k);
-            if (y >= y0 && y < y1) process_row(y, hv, wblk + k * kSlotWords);
+            if (y >= y0 && y < y1) process_row(y, hv, wk[k]);
         }
     }
 }
@@ -1085,7 +1094,7 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
         }
     };
 
-    auto process_row = [&](int y, uint4 cur, uint32_t s8, cptr<int32_t> wr) __attribute__((always_inline)) {
+    auto process_row = [&](int y, uint4 cur, uint32_t s8, const int32_t (&wr)[M]) __attribute__((always_inline)) {
         // the lane's 12 bytes from its byte offset: r0 g0 b0 r1 | g1 b1 r2 g2 | b2 r3 g3 b3
         const uint32_t a0 = __builtin_amdgcn_alignbyte(cur.y, cur.x, s8);
         const uint32_t a1 = __builtin_amdgcn_alignbyte(cur.z, cur.y, s8);
@@ -1160,13 +1169,20 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
         __builtin_amdgcn_sched_barrier(0);
     }
     for (int yb = yb0; yb < y1; yb += kPrefetch) {
+        // the block's slot weights, read together (a block starts below H,
+        // and the table has kSlotMax rows past the frame's last)
         const cptr<int32_t> wblk = slot_q + yb * kSlotWords;
+        int32_t wk[kPrefetch][M];
+#pragma unroll
+        for (int k = 0; k < kPrefetch; ++k)
+#pragma unroll
+            for (int s = 0; s < M; ++s) wk[k][s] = wblk[k * kSlotWords + s];
 #pragma unroll
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
             const uint4 cur = pf[k];
             pf[k] = load_row(yb + kPrefetch, k);
-            if (y >= y0 && y < y1) process_row(y, cur, sh[k], wblk + k * kSlotWords);
+            if (y >= y0 && y < y1) process_row(y, cur, sh[k], wk[k]);
         }
     }
 }
@@ -1317,9 +1333,18 @@ __global__ __launch_bounds__(64) void resize_mfma_kernel(PlanView plan, int wg0,
         for (int c = 0; c < 3; ++c) hv[c] = *reinterpret_cast<const uint4*>(hbuf + c * 1024 + lane * 16);
         wave_lds_fence();
         const cptr<int32_t> wblk = slot_q + yc * kSlotWords;
+        int32_t wk[4][M];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int y = yc + r;
+            if ((r & 3) == 0 && y < y1) {
+                // the next four rows' slot weights, read together (y < y1 <= H,
+                // and the table has kSlotMax rows past the frame's last)
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+#pragma unroll
+                    for (int s = 0; s < M; ++s) wk[k][s] = wblk[(r + k) * kSlotWords + s];
+            }
             if (y < y0 || y >= y1) continue;   // wave-uniform
             const uint32_t dw = r >> 2;
             const uint32_t sel = 8u * static_cast<uint32_t>(r & 3);
@@ -1329,10 +1354,9 @@ __global__ __launch_bounds__(64) void resize_mfma_kernel(PlanView plan, int wg0,
                 const uint32_t word = dw == 0 ? hv[c].x : dw == 1 ? hv[c].y : dw == 2 ? hv[c].z : hv[c].w;
                 h[c] = static_cast<int32_t>(__builtin_amdgcn_ubfe(word, sel, 8));
             }
-            const cptr<int32_t> wr = wblk + r * kSlotWords;
 #pragma unroll
             for (int s = 0; s < M; ++s) {
-                const int32_t ws = wr[s];
+                const int32_t ws = wk[r & 3][s];
 #pragma unroll
                 for (int c = 0; c < 3; ++c) acc[s][c] += __mul24(ws, h[c]);
             }
