@@ -265,8 +265,10 @@ int32_t build_slots(const AxisFilter& f, std::vector<int32_t>* words, bool fixed
     }
     if (most > vp::kSlotWords) return -1;
     const int32_t m = most < 4 ? 4 : most;
-    words->assign(size_t(rows) * vp::kSlotWords + n_out + 1, 0);
-    (*words)[size_t(rows) * vp::kSlotWords + n_out] = INT32_MAX;   // close_row[n_out]: never reached
+    // close_row[n_out] and [n_out + 1]: never reached (kernels read one close row ahead)
+    words->assign(size_t(rows) * vp::kSlotWords + n_out + 2, 0);
+    (*words)[size_t(rows) * vp::kSlotWords + n_out] = INT32_MAX;
+    (*words)[size_t(rows) * vp::kSlotWords + n_out + 1] = INT32_MAX;
     float* w = reinterpret_cast<float*>(words->data());
     for (int32_t i = 0; i < n_out; ++i)
         for (int32_t k = 0; k < f.count[i]; ++k) {

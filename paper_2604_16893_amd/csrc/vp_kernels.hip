@@ -565,6 +565,11 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     const int nbw = min(band, w - j0);             // its columns
     const int tt = u_p >> 1;
     const int dt_self = P == 16 ? (u_p & 1) : wv;   // patch 14 units start at the pair's first frame
+    // the item's row geometry, held in scalar registers (as constant-memory
+    // loads the compiler would re-read them at every store-out)
+    int64_t it_row_off = it->row_off;
+    int it_hm = it->hm, it_wm = it->wm;
+    asm volatile("" : "+s"(it_row_off), "+s"(it_hm), "+s"(it_wm));
     const bool both = (u_flags & 1) != 0;
 
     // patch 16: [row][stage [3][4][64]]; patch 14: [row of wave 0][row of
@@ -631,6 +636,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     while (base > 0 && close_row[base - 1] >= y0) --base;
     int slot = base % M;
     int next_close = close_row[base];
+    int after_close = close_row[base + 1];   // read one ahead (the table ends in two sentinels)
 
     // Rows are visited in blocks of four starting at a multiple of 4, so
     // that y % 4 = k is known at every step: the lane's byte offset inside
@@ -712,7 +718,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
         constexpr int PPR = kRowElems / VPP;                           // pieces per row
         static_assert(kRowElems % VPP == 0, "rows are whole 16-byte pieces");
         const int nq = nbw / 14;
-        const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + (pr >> 1)) * it->wm * 4 + (pr & 1) * 2;
+        const int64_t win_row0 = it_row_off + (int64_t(tt) * it_hm + (pr >> 1)) * it_wm * 4 + (pr & 1) * 2;
         using u4v = unsigned __attribute__((ext_vector_type(4)));
         for (int e = static_cast<int>(threadIdx.x); e < nq * PPR; e += 128) {
             const int q = e / PPR;
@@ -796,7 +802,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             const int yq = (i & 15) >> 2;
             const int bh = i >> 5;
             const int mh = (i >> 4) & 1;
-            const int64_t win_row0 = it->row_off + (int64_t(tt) * it->hm + bh) * it->wm * 4 + mh * 2;
+            const int64_t win_row0 = it_row_off + (int64_t(tt) * it_hm + bh) * it_wm * 4 + mh * 2;
             elem_t* const obase = static_cast<elem_t*>(out) + win_row0 * kRow + yq * 64;
 #pragma unroll
             for (int r = 0; r < kStoreIter; ++r) {
@@ -888,7 +894,8 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             }
             ++base;
             slot = slot + 1 == M ? 0 : slot + 1;
-            next_close = close_row[base];
+            next_close = after_close;
+            after_close = close_row[base + 1];
         }
     };
 
@@ -1081,11 +1088,17 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     while (base > 0 && close_row[base - 1] >= y0) --base;
     int slot = base % M;
     int next_close = close_row[base];
+    int after_close = close_row[base + 1];   // read one ahead (the table ends in two sentinels)
 
     // rows i - 3 .. i of the band leave the stage as dwords
+    // the item's output offset and height, held in scalar registers (as
+    // constant-memory loads the compiler would re-read them at every flush)
+    int64_t it_row_off = it->row_off;
+    int it_h = it->h;
+    asm volatile("" : "+s"(it_row_off), "+s"(it_h));
     auto flush = [&](int i) __attribute__((always_inline)) {
         const int nd = 3 * nbw / 4;   // dwords per band row (nbw is a multiple of 4)
-        uint8_t* const ob = out + it->row_off + ((int64_t(u_k) * it->h + (i - 3)) * w + j0) * 3;
+        uint8_t* const ob = out + it_row_off + ((int64_t(u_k) * it_h + (i - 3)) * w + j0) * 3;
         for (int e = lane; e < 4 * nd; e += 64) {
             const int r = e / nd;
             const int d = e - r * nd;
@@ -1157,7 +1170,8 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
             }
             ++base;
             slot = slot + 1 == M ? 0 : slot + 1;
-            next_close = close_row[base];
+            next_close = after_close;
+            after_close = close_row[base + 1];
         }
     };
 
@@ -1264,10 +1278,16 @@ __global__ __launch_bounds__(64) void resize_mfma_kernel(PlanView plan, int wg0,
     while (base > 0 && close_row[base - 1] >= y0) --base;
     int slot = base % M;
     int next_close = close_row[base];
+    int after_close = close_row[base + 1];   // read one ahead (the table ends in two sentinels)
 
+    // the item's output offset and height, held in scalar registers (as
+    // constant-memory loads the compiler would re-read them at every flush)
+    int64_t it_row_off = it->row_off;
+    int it_h = it->h;
+    asm volatile("" : "+s"(it_row_off), "+s"(it_h));
     auto flush = [&](int i) __attribute__((always_inline)) {
         const int nd = 3 * nbw / 4;
-        uint8_t* const ob = out + it->row_off + ((int64_t(u_k) * it->h + (i - 3)) * w + j0) * 3;
+        uint8_t* const ob = out + it_row_off + ((int64_t(u_k) * it_h + (i - 3)) * w + j0) * 3;
         for (int e = lane; e < 4 * nd; e += 64) {
             const int r = e / nd;
             const int d = e - r * nd;
@@ -1381,7 +1401,8 @@ __global__ __launch_bounds__(64) void resize_mfma_kernel(PlanView plan, int wg0,
                 }
                 ++base;
                 slot = slot + 1 == M ? 0 : slot + 1;
-                next_close = close_row[base];
+                next_close = after_close;
+                after_close = close_row[base + 1];
             }
         }
     }
