@@ -773,7 +773,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
                     const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
                     Keyed k;
                     k.key = std::make_tuple(sh.m, sh.kx, sh.px);
-                    k.bands = sh.bands;
+                    k.bands = d.patch == 14 ? (sh.bands + 1) / 2 : sh.bands;   // patch 14: bands in pairs
                     k.unit.item = b;
                     k.unit.p = 2 * tt + dt;
                     k.unit.rows = i0 | (i1 << 16);

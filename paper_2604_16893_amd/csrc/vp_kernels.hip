@@ -529,12 +529,13 @@ __device__ __forceinline__ void lds_barrier() {
 //     cache lines, and the two frames of a pair interleave every 196 values,
 //     so stores from one frame alone leave most lines part-written (the L2
 //     then fetches them from HBM, and writes them in 32-byte pieces).  The
-//     workgroup is therefore two waves, one per frame of the pair, over the
-//     same band, sharing a stage in output order, [patch][c][frame][14][14]:
-//     after every 14th row both waves write the band's finished output rows
-//     whole (the two patches of a merge window are one contiguous run).
+//     workgroup is therefore four waves: the pair's two frames over two
+//     neighbouring bands, which then also read their shared source pixels
+//     in step.  They share a stage in output order, [patch][c][frame][14][14]:
+//     after every 14th row the four waves write the bands' finished output
+//     rows whole (the two patches of a merge window are one contiguous run).
 template <int M, int KX, int PX, int OUT_BF16, int P>
-__global__ __launch_bounds__(P == 16 ? 64 : 128) __attribute__((amdgpu_waves_per_eu(
+__global__ __launch_bounds__(P == 16 ? 64 : 256) __attribute__((amdgpu_waves_per_eu(
     M * PX > 12 || KX >= 20 || 3 * M * PX + KX >= 52 || (OUT_BF16 == 0 && M * PX >= 12) ? 4 : 5)))
 void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     static_assert(P == 16 || P == 14, "patch 16 or 14");
@@ -546,8 +547,10 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     extern __shared__ __align__(16) unsigned char smem[];
 
     const int lane = static_cast<int>(threadIdx.x) & 63;
-    // patch 14: wave 0 takes the pair's first frame, wave 1 its second
+    // patch 14: four waves, two neighbouring bands x the pair's two frames;
+    // wave wv takes frame wv & 1 of band wv >> 1 of the workgroup's two
     const int wv = P == 16 ? 0 : __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int fw = wv & 1;
     // Workgroup -> (unit, column band), from the host's list (which places
     // the bands of one unit on one XCD)
     const uint32_t wg = as_const(plan.wgs)[wg0 + static_cast<int>(blockIdx.x)];
@@ -561,10 +564,13 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     const int i1 = u_rows >> 16;
     const int w = it->w;
     const int band = it->band;
-    const int j0 = wave * band;                    // first output column of this wave
-    const int nbw = min(band, w - j0);             // its columns
+    // patch 14: the list names the workgroup's pair of bands
+    const int j0_wg = P == 16 ? wave * band : 2 * wave * band;   // the workgroup's first column
+    const int nbw_wg = min(P == 16 ? band : 2 * band, w - j0_wg);   // and its columns
+    const int j0 = P == 16 ? j0_wg : j0_wg + (wv >> 1) * band;  // first output column of this wave
+    const int nbw = min(band, w - j0);             // its columns (none: a missing second band)
     const int tt = u_p >> 1;
-    const int dt_self = P == 16 ? (u_p & 1) : wv;   // patch 14 units start at the pair's first frame
+    const int dt_self = P == 16 ? (u_p & 1) : fw;   // patch 14 units start at the pair's first frame
     // the item's row geometry, held in scalar registers (as constant-memory
     // loads the compiler would re-read them at every store-out)
     int64_t it_row_off = it->row_off;
@@ -572,10 +578,44 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     asm volatile("" : "+s"(it_row_off), "+s"(it_hm), "+s"(it_wm));
     const bool both = (u_flags & 1) != 0;
 
-    // patch 16: [row][stage [3][4][64]]; patch 14: [row of wave 0][row of
-    // wave 1][stage [4 patches][1176]]
+    // patch 16: [row][stage [3][4][64]]; patch 14: [row of each of the four
+    // waves][stage [8 patches][1176]]
     float4* row = reinterpret_cast<float4*>(smem + wv * kRowPx * 16);                  // [kRowPx]
-    elem_t* stage = reinterpret_cast<elem_t*>(smem + (P == 16 ? 1 : 2) * kRowPx * 16);
+    elem_t* stage = reinterpret_cast<elem_t*>(smem + (P == 16 ? 1 : 4) * kRowPx * 16);
+
+    // Patch 14 store-out of patch row pr (output rows 14 pr .. 14 pr + 13):
+    // the workgroup's output rows leave the stage whole, in 16-byte pieces
+    // shared out over its four waves; consecutive pieces are consecutive in
+    // memory within each merge window.
+    auto store_rows = [&](int pr) __attribute__((always_inline)) {
+        constexpr int kRowElems = 6 * P * P;                           // 1176
+        constexpr int VPP = 16 / int(sizeof(elem_t));                  // values per piece
+        constexpr int PPR = kRowElems / VPP;                           // pieces per row
+        static_assert(kRowElems % VPP == 0, "rows are whole 16-byte pieces");
+        const int nq = nbw_wg / 14;
+        const int64_t win_row0 = it_row_off + (int64_t(tt) * it_hm + (pr >> 1)) * it_wm * 4 + (pr & 1) * 2;
+        using u4v = unsigned __attribute__((ext_vector_type(4)));
+        for (int e = static_cast<int>(threadIdx.x); e < nq * PPR; e += 256) {
+            const int q = e / PPR;
+            const int pc = e - q * PPR;
+            const int qa = j0_wg / 14 + q;
+            const u4v val = *reinterpret_cast<const u4v*>(stage + q * kRowElems + pc * VPP);
+            elem_t* dst = static_cast<elem_t*>(out) + (win_row0 + (qa >> 1) * 4 + (qa & 1)) * kRowElems + pc * VPP;
+            __builtin_nontemporal_store(val, reinterpret_cast<u4v*>(dst));
+        }
+    };
+    if (P == 14 && (nbw <= 0 || (both && fw == 1))) {
+        // a wave with no frame to stream (the second frame of a pair whose
+        // frames are one, or a band past the item's last) reads no table; it
+        // keeps step with the other waves' barriers (two per patch row) and
+        // stores its share of the rows
+        for (int pr = i0 / 14; pr < i1 / 14; ++pr) {
+            lds_barrier();
+            store_rows(pr);
+            lds_barrier();
+        }
+        return;
+    }
 
     // x pass: output column j0 + lane keeps its KX column weights in registers.
     const cptr<int32_t> tables = as_const(plan.tables);
@@ -601,7 +641,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     // Source frame, read through buffer resources (loads past a resource's
     // range return 0).  Every load is dword-aligned: unaligned per-lane
     // loads cost about a third of the read bandwidth on gfx950.
-    const int f = as_const(plan.indices)[it->idx_off + u_p + (P == 16 ? 0 : wv)];
+    const int f = as_const(plan.indices)[it->idx_off + u_p + (P == 16 ? 0 : fw)];
     const uintptr_t fa = reinterpret_cast<uintptr_t>(it->frames + int64_t(f) * it->frame_bytes);
     const uint32_t lead = static_cast<uint32_t>(fa & 3u);
     // Range = the frame rounded up to whole dwords: the range check is per
@@ -683,7 +723,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
 
     // Patch 14: the lane's column j0 + lane is column lane % 14 of the
     // band's patch lane / 14, at this offset of the stage's patch-row origin.
-    const int st14 = (lane / 14) * (6 * P * P) + lane % 14;
+    const int st14 = ((j0 - j0_wg) / 14 + lane / 14) * (6 * P * P) + lane % 14;
 
     // Store-out pieces of this lane (patch 16): piece e = lane + 64 r of the
     // band's (patch q, channel c, row ry, piece) runs, as a stage offset
@@ -707,28 +747,6 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             dst_off[r] = ((qa >> 1) * 4 + (qa & 1)) * kRow + (c * 2) * 256 + ry * 16 + piece * S;
         }
     }
-
-    // Patch 14 store-out of patch row pr (output rows 14 pr .. 14 pr + 13):
-    // the band's output rows leave the stage whole, in 16-byte pieces shared
-    // out over both waves; consecutive pieces are consecutive in memory
-    // within each merge window.
-    auto store_rows = [&](int pr) __attribute__((always_inline)) {
-        constexpr int kRowElems = 6 * P * P;                           // 1176
-        constexpr int VPP = 16 / int(sizeof(elem_t));                  // values per piece
-        constexpr int PPR = kRowElems / VPP;                           // pieces per row
-        static_assert(kRowElems % VPP == 0, "rows are whole 16-byte pieces");
-        const int nq = nbw / 14;
-        const int64_t win_row0 = it_row_off + (int64_t(tt) * it_hm + (pr >> 1)) * it_wm * 4 + (pr & 1) * 2;
-        using u4v = unsigned __attribute__((ext_vector_type(4)));
-        for (int e = static_cast<int>(threadIdx.x); e < nq * PPR; e += 128) {
-            const int q = e / PPR;
-            const int pc = e - q * PPR;
-            const int qa = j0 / 14 + q;
-            const u4v val = *reinterpret_cast<const u4v*>(stage + q * kRowElems + pc * VPP);
-            elem_t* dst = static_cast<elem_t*>(out) + (win_row0 + (qa >> 1) * 4 + (qa & 1)) * kRowElems + pc * VPP;
-            __builtin_nontemporal_store(val, reinterpret_cast<u4v*>(dst));
-        }
-    };
 
     // x pass of output row i, normalise, stage; at the end of every group of
     // four rows of a patch (for patch 14 also after its last two): store.
@@ -905,16 +923,6 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     // every prefetch register in place.  The first block's loads are issued
     // in row order, as the loop issues them, so that the oldest load is
     // always the next one needed.
-    if (P == 14 && both && wv == 1) {
-        // wave 1 of a pair whose frames are one: no frame to stream; it keeps
-        // step with wave 0's barriers (two per patch row) and stores its share
-        for (int pr = i0 / 14; pr < i1 / 14; ++pr) {
-            lds_barrier();
-            store_rows(pr);
-            lds_barrier();
-        }
-        return;
-    }
 
     const int yb0 = y0 & ~3;
     load_t pf[kPrefetch];
@@ -956,7 +964,7 @@ template <int M, int KX, int PX>
 int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                         const Norm& norm, hipStream_t stream) {
     const int lds = stream_wave_bytes(PX, KX, out_dtype == 1 ? 2 : 4, L.patch);
-    dim3 grid(static_cast<unsigned>(L.count)), block(L.patch == 14 ? 128 : 64);
+    dim3 grid(static_cast<unsigned>(L.count)), block(L.patch == 14 ? 256 : 64);
     if (L.patch == 14) {
         if (out_dtype == 1)
             hipLaunchKernelGGL((stream_kernel<M, KX, PX, 1, 14>), grid, block, lds, stream, plan, L.first, out, norm);

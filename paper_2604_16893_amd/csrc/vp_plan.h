@@ -55,11 +55,12 @@ constexpr int kStreamLdsBudget = 64 * 1024;   // LDS of one streaming workgroup 
 
 // LDS of one streaming workgroup.  Patch 16 (one wave): its source row (64 *
 // px float4 pixels) and the stage of four output rows (3 channels x 4 rows x
-// 64 columns).  Patch 14 (two waves, one per frame of a pair): two source
-// rows and the stage of up to four whole output rows of 1176 values.
+// 64 columns).  Patch 14 (four waves: a pair's two frames over two bands):
+// four source rows and the stage of up to eight whole output rows of 1176
+// values.
 constexpr int stream_wave_bytes(int px, int kx, int elem_bytes, int patch = 16) {
     return (void)kx, patch == 16 ? 64 * px * 16 + 3 * 4 * 64 * elem_bytes
-                                 : 2 * 64 * px * 16 + 4 * 6 * patch * patch * elem_bytes;
+                                 : 4 * 64 * px * 16 + 8 * 6 * patch * patch * elem_bytes;
 }
 
 // uint8 streaming writer: pixels per lane (a band's source span is at most
