@@ -24,6 +24,9 @@
 //   * every four output rows the stage holds the band's part of one
 //     64-value run (four patch rows of 16) of every (patch, channel) block;
 //     those leave as 16-byte stores, eight lanes per 128-byte run.
+//   * patch 14 is the exception to independent waves: a workgroup is four
+//     waves (two neighbouring bands x a pair's two frames) that meet at a
+//     barrier once per patch row, to write whole output rows.
 //
 // General kernel (any scale factor): one workgroup per merge window of one
 // frame pair; y pass from global memory into an LDS column tile, x pass,
