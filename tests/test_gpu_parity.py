@@ -341,6 +341,10 @@ PATCH14 = [
     ("p14_image_odd_f32", [(1, 333, 257, [0], 308, 252), (4, 150, 260, [3, 0, 2], 84, 140)], "f32"),
     ("p14_long_window", [(2, 540, 3840, [1, 0], 84, 672)], "bf16"),
     ("p14_taps10_px3", [(3, 180, 640, [0, 2], 84, 280)], "f32"),
+    # items one band wide: the workgroup's second band is missing, and its
+    # waves only keep step with the barriers (with an image in the batch,
+    # whose pair is one frame twice)
+    ("p14_single_band", [(2, 60, 70, [1, 0], 56, 56), (1, 40, 30, [0], 56, 28)], "bf16"),
 ]
 
 
