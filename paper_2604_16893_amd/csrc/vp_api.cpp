@@ -443,8 +443,8 @@ int32_t band_span(const AxisFilter& fx, int32_t band) {
 bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t patch, StreamShape* sh) {
     if (m < 4 || m > vp::kSlotWords) return false;
     const int32_t mm = m;
-    // windows up to 16 taps round up to an even count, longer ones to a multiple of 4
-    const int32_t kx = fx.taps <= 16 ? round_up(fx.taps, 2) : round_up(fx.taps, 4);
+    // windows up to 16 taps run their own tap count (at least 4), longer ones a multiple of 4
+    const int32_t kx = fx.taps <= 16 ? std::max<int32_t>(fx.taps, 4) : round_up(fx.taps, 4);
     // every load of a frame row (up to kSlotMax + 8 rows past the last one) stays below 4 GiB
     if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
     int64_t best = -1;

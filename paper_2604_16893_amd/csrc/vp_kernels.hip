@@ -760,8 +760,8 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             const float4* src = row + sj;
 #pragma unroll
             for (int g = 0; g < KX; g += 4) {
-                // four taps at a time (two in a last group when KX is 2 mod 4):
-                // bounds the LDS values held in registers
+                // four taps at a time (KX mod 4 in a last group): bounds the
+                // LDS values held in registers
                 __builtin_amdgcn_sched_barrier(0);
                 constexpr int kLast = KX % 4 == 0 ? 4 : KX % 4;
                 const int n = g + 4 <= KX ? 4 : kLast;
@@ -783,8 +783,12 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
                 // back under one wait
                 if (n == 4)
                     asm volatile("" : : "v"(q[0].w), "v"(q[1].w), "v"(q[2].w), "v"(q[3].w));
-                else
+                else if (n == 3)
+                    asm volatile("" : : "v"(q[0].w), "v"(q[1].w), "v"(q[2].w));
+                else if (n == 2)
                     asm volatile("" : : "v"(q[0].w), "v"(q[1].w));
+                else
+                    asm volatile("" : : "v"(q[0].w));
             }
             __builtin_amdgcn_sched_barrier(0);
             const float v0 = r0 * a0;
@@ -1509,9 +1513,9 @@ int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& n
 
 // Compiled shapes: every (M, KX) with 2 pixels per lane, and with 3 pixels
 // per lane where the accumulators still fit the registers of a 1024-thread
-// block (M <= 5).  KX is even up to 16 taps and a multiple of 4 beyond.
+// block (M <= 5).  KX is any tap count from 4 to 16, and a multiple of 4 beyond.
 bool stream_shape_supported(int m, int kx, int px) {
-    if (m < 4 || kx < 4 || kx > 32 || kx % (kx <= 16 ? 2 : 4) != 0) return false;
+    if (m < 4 || kx < 4 || kx > 32 || (kx > 16 && kx % 4 != 0)) return false;
     if (m > 6)   // 7 or 8 open rows: vertical upscales up to about 2x, whose x axis has short windows too
         return m <= kSlotWords && px == 2 && kx <= 8;
     if (kx <= 16) return px == 2 || (px == 3 && m <= 5);
@@ -1528,12 +1532,14 @@ int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int ou
     if (L.m == MM && L.kx == KK && L.px == PP) \
         return launch_stream_shape<MM, KK, PP>(plan, L, out, out_dtype, norm, stream);
 #define VP_STREAM_KX(MM, PP) \
-    VP_STREAM_CASE(MM, 4, PP) VP_STREAM_CASE(MM, 6, PP) VP_STREAM_CASE(MM, 8, PP) VP_STREAM_CASE(MM, 10, PP) \
-    VP_STREAM_CASE(MM, 12, PP) VP_STREAM_CASE(MM, 14, PP) VP_STREAM_CASE(MM, 16, PP)
+    VP_STREAM_CASE(MM, 4, PP) VP_STREAM_CASE(MM, 5, PP) VP_STREAM_CASE(MM, 6, PP) VP_STREAM_CASE(MM, 7, PP) \
+    VP_STREAM_CASE(MM, 8, PP) VP_STREAM_CASE(MM, 9, PP) VP_STREAM_CASE(MM, 10, PP) VP_STREAM_CASE(MM, 11, PP) \
+    VP_STREAM_CASE(MM, 12, PP) VP_STREAM_CASE(MM, 13, PP) VP_STREAM_CASE(MM, 14, PP) VP_STREAM_CASE(MM, 15, PP) \
+    VP_STREAM_CASE(MM, 16, PP)
     VP_STREAM_KX(4, 2) VP_STREAM_KX(5, 2) VP_STREAM_KX(6, 2)
     VP_STREAM_KX(4, 3) VP_STREAM_KX(5, 3)
-    VP_STREAM_CASE(7, 4, 2) VP_STREAM_CASE(7, 6, 2) VP_STREAM_CASE(7, 8, 2)
-    VP_STREAM_CASE(8, 4, 2) VP_STREAM_CASE(8, 6, 2) VP_STREAM_CASE(8, 8, 2)
+    VP_STREAM_CASE(7, 4, 2) VP_STREAM_CASE(7, 5, 2) VP_STREAM_CASE(7, 6, 2) VP_STREAM_CASE(7, 7, 2) VP_STREAM_CASE(7, 8, 2)
+    VP_STREAM_CASE(8, 4, 2) VP_STREAM_CASE(8, 5, 2) VP_STREAM_CASE(8, 6, 2) VP_STREAM_CASE(8, 7, 2) VP_STREAM_CASE(8, 8, 2)
 #define VP_STREAM_LONG(MM, PP) \
     VP_STREAM_CASE(MM, 20, PP) VP_STREAM_CASE(MM, 24, PP) VP_STREAM_CASE(MM, 28, PP) VP_STREAM_CASE(MM, 32, PP)
     VP_STREAM_LONG(4, 2) VP_STREAM_LONG(5, 2) VP_STREAM_LONG(6, 2)

@@ -152,10 +152,12 @@ SMALL = [
     ("long_window_28", [(2, 90, 1600, [1, 0], 32, 256)], "f32"),
     ("long_window_20_px3", [(3, 200, 1800, [2, 0], 64, 384)], "bf16"),
     ("long_window_4k_width", [(2, 540, 3840, [0, 1], 96, 672)], "bf16"),
-    # windows of 2 mod 4 taps (the last group of the x pass holds two):
-    # 10 taps with two and with three pixels per lane
-    ("taps10_px2", [(2, 180, 640, [1, 0], 96, 288)], "f32"),
+    # tap counts that are not a multiple of 4 (the x pass's last group
+    # holds 1 to 3 taps): 9 taps with two pixels per lane, 10 with three,
+    # 7 in bf16
+    ("taps9_px2", [(2, 180, 640, [1, 0], 96, 288)], "f32"),
     ("taps10_px3", [(3, 90, 300, [2, 0], 32, 128)], "bf16"),
+    ("taps7_bf16", [(2, 120, 854, [1, 0], 64, 512)], "bf16"),
 ]
 
 
