@@ -450,6 +450,7 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t pa
     int64_t best = -1;
     for (int32_t band = 4 * patch; band >= patch; band -= patch) {
         const int32_t waves = (it.dst_w + band - 1) / band;
+        if (waves > vp::kWgBandMax) continue;   // the band index field of a workgroup entry
         const int32_t span = band_span(fx, band);
         for (int32_t px = 2; px <= 4; ++px) {
             if (!vp::stream_shape_supported(mm, kx, px)) continue;
@@ -775,9 +776,9 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
                     k.key = std::make_tuple(sh.m, sh.kx, sh.px);
                     k.bands = d.patch == 14 ? (sh.bands + 1) / 2 : sh.bands;   // patch 14: bands in pairs
                     k.unit.item = b;
-                    k.unit.p = 2 * tt + dt;
-                    k.unit.rows = i0 | (i1 << 16);
-                    k.unit.flags = same ? 1 : 0;
+                    k.unit.p_flags = (2 * tt + dt) | (same ? vp::kUnitBoth : 0);
+                    k.unit.i0 = i0;
+                    k.unit.i1 = i1;
                     k.cost = int64_t(i1 - i0) * d.H / d.h * d.W   // source pixels read, roughly
                              * (pair_units && !same ? 2 : 1);
                     keyed.push_back(k);
@@ -951,6 +952,7 @@ bool resize_stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, Str
     if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 64 >= (int64_t(1) << 32)) return false;
     for (int32_t band = 64; band >= 16; band -= 16) {
         if (band_span(fx, band) > 64 * vp::kRsPx) continue;
+        if ((it.dst_w + band - 1) / band > vp::kWgBandMax) continue;
         sh->m = m;
         sh->kx = kx;
         sh->px = vp::kRsPx;
@@ -1076,7 +1078,8 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         // window; byte dot products cost in proportion to it.  Measured, the
         // MFMA form wins from 16 dot-product taps (windows of 10 or more).
         const bool long_x = round_up(fx->taps + 3, 4) >= 16;
-        if (slots && long_x && m >= 4 && m <= vp::kSlotWords && (d.sx_off = mfma_columns_for(*fx)) >= 0 &&
+        if (slots && long_x && m >= 4 && m <= vp::kSlotWords && (it.dst_w + 63) / 64 <= vp::kWgBandMax &&
+            (d.sx_off = mfma_columns_for(*fx)) >= 0 &&
             int64_t(it.src_h + vp::kSlotMax + 20) * it.src_w * 3 + 256 < (int64_t(1) << 32)) {
             // the MFMA form: bands of 64 columns, blocks of 16 with 64-pixel windows
             d.route = vp::kRouteStream;
@@ -1133,9 +1136,9 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
                 e.key = std::make_tuple(sh.m, sh.kx, sh.px);
                 e.bands = sh.bands;
                 e.unit.item = b;
-                e.unit.p = k;
-                e.unit.rows = i0 | (i1 << 16);
-                e.unit.flags = 0;
+                e.unit.p_flags = k;
+                e.unit.i0 = i0;
+                e.unit.i1 = i1;
                 e.cost = int64_t(i1 - i0) * d.H / d.h * d.W;
                 keyed.push_back(e);
             }

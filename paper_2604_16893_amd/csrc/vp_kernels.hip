@@ -40,6 +40,22 @@
 
 #include "vp_plan.h"
 
+// The streaming kernels' many template shapes are compiled in VP_PARTS
+// translation units: this file is compiled once per part with
+// -DVP_PART=k.  Part 0 holds the launchers and the kernels of a single
+// shape; every part instantiates its share of the streaming shapes and
+// exports a dispatcher for them (launch_stream_part<k>,
+// launch_resize_stream_part<k>).  Built as one unit (no -D), part 0 is all.
+#ifndef VP_PART
+#define VP_PART 0
+#endif
+#ifndef VP_PARTS
+#define VP_PARTS 1
+#endif
+static_assert(VP_PARTS >= 1 && VP_PARTS <= 8 && VP_PART >= 0 && VP_PART < VP_PARTS, "kernel parts");
+#define VP_CAT2(a, b) a##b
+#define VP_CAT(a, b) VP_CAT2(a, b)
+
 namespace vp {
 namespace {
 
@@ -54,6 +70,8 @@ template <class T>
 __device__ __forceinline__ cptr<T> as_const(const T* p) {
     return (cptr<T>)(p);
 }
+
+#if VP_PART == 0   // the kernels of a single shape: part 0 only
 
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
@@ -486,6 +504,8 @@ __global__ __launch_bounds__(256) void patchify14_kernel(PlanView plan, void* ou
     }
 }
 
+#endif  // VP_PART == 0
+
 // ===========================================================================
 // Streaming kernel
 // ===========================================================================
@@ -561,10 +581,9 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     const int u = static_cast<int>(wg & kWgUnitMask);
     const int wave = static_cast<int>(wg >> kWgBandShift);
     const cptr<StreamUnit> up = as_const(plan.units) + u;
-    const int u_item = up->item, u_p = up->p, u_rows = up->rows, u_flags = up->flags;
+    const int u_item = up->item, u_pf = up->p_flags, i0 = up->i0, i1 = up->i1;
+    const int u_p = u_pf & (kUnitBoth - 1);
     const cptr<DevItem> it = as_const(plan.items) + u_item;
-    const int i0 = u_rows & 0xffff;
-    const int i1 = u_rows >> 16;
     const int w = it->w;
     const int band = it->band;
     // patch 14: the list names the workgroup's pair of bands
@@ -579,7 +598,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     int64_t it_row_off = it->row_off;
     int it_hm = it->hm, it_wm = it->wm;
     asm volatile("" : "+s"(it_row_off), "+s"(it_hm), "+s"(it_wm));
-    const bool both = (u_flags & 1) != 0;
+    const bool both = (u_pf & kUnitBoth) != 0;
 
     // patch 16: [row][stage [3][4][64]]; patch 14: [row of each of the four
     // waves][stage [8 patches][1176]]
@@ -1024,10 +1043,9 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     const int u = static_cast<int>(wg & kWgUnitMask);
     const int wave = static_cast<int>(wg >> kWgBandShift);
     const cptr<StreamUnit> up = as_const(plan.units) + u;
-    const int u_item = up->item, u_k = up->p, u_rows = up->rows;
+    const int u_item = up->item, u_k = up->p_flags, i0 = up->i0, i1 = up->i1;
     const cptr<DevItem> it = as_const(plan.items) + u_item;
-    const int i0 = u_rows & 0xffff;
-    const int i1 = u_rows >> 16;
+
     const int w = it->w;
     const int band = it->band;
     const int j0 = wave * band;
@@ -1243,10 +1261,9 @@ __global__ __launch_bounds__(64) void resize_mfma_kernel(PlanView plan, int wg0,
     const int u = static_cast<int>(wg & kWgUnitMask);
     const int wave = static_cast<int>(wg >> kWgBandShift);
     const cptr<StreamUnit> up = as_const(plan.units) + u;
-    const int u_item = up->item, u_k = up->p, u_rows = up->rows;
+    const int u_item = up->item, u_k = up->p_flags, i0 = up->i0, i1 = up->i1;
     const cptr<DevItem> it = as_const(plan.items) + u_item;
-    const int i0 = u_rows & 0xffff;
-    const int i1 = u_rows >> 16;
+
     const int w = it->w;
     const int j0 = wave * 64;
     const int nbw = min(64, w - j0);
@@ -1437,6 +1454,132 @@ int launch_resize_stream_shape(const PlanView& plan, const StreamLaunch& L, void
     return static_cast<int>(hipGetLastError());
 }
 
+// One streaming shape of this part: its launch, or -1 if the launch is not
+// of this shape or the shape belongs to another part.
+template <int MM, int KK, int PP, int ID>
+int stream_case(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
+                const Norm& norm, hipStream_t stream) {
+    if constexpr (ID % VP_PARTS == VP_PART) {
+        if (L.m == MM && L.kx == KK && L.px == PP)
+            return launch_stream_shape<MM, KK, PP>(plan, L, out, out_dtype, norm, stream);
+    }
+    return -1;
+}
+
+template <int MM, int KK, int ID>
+int resize_case(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
+    if constexpr (ID % VP_PARTS == VP_PART) {
+        if (L.m == MM && L.kx == KK) {
+            if constexpr (KK == kRsMfmaWindow)
+                return launch_resize_mfma_shape<MM>(plan, L, out, stream);
+            else
+                return launch_resize_stream_shape<MM, KK>(plan, L, out, stream);
+        }
+    }
+    return -1;
+}
+
+}  // namespace
+
+// This part's streaming shapes (-1: the launch's shape is not one of them).
+int VP_CAT(launch_stream_part, VP_PART)(const PlanView& plan, const StreamLaunch& L, void* out,
+                                        int out_dtype, const Norm& norm, hipStream_t stream) {
+#define VP_STREAM_CASE(MM, KK, PP)                                                               \
+    if (const int r = stream_case<MM, KK, PP, __COUNTER__>(plan, L, out, out_dtype, norm, stream); \
+        r != -1)                                                                                 \
+        return r;
+#define VP_STREAM_KX(MM, PP) \
+    VP_STREAM_CASE(MM, 4, PP) VP_STREAM_CASE(MM, 5, PP) VP_STREAM_CASE(MM, 6, PP) VP_STREAM_CASE(MM, 7, PP) \
+    VP_STREAM_CASE(MM, 8, PP) VP_STREAM_CASE(MM, 9, PP) VP_STREAM_CASE(MM, 10, PP) VP_STREAM_CASE(MM, 11, PP) \
+    VP_STREAM_CASE(MM, 12, PP) VP_STREAM_CASE(MM, 13, PP) VP_STREAM_CASE(MM, 14, PP) VP_STREAM_CASE(MM, 15, PP) \
+    VP_STREAM_CASE(MM, 16, PP)
+    VP_STREAM_KX(4, 2) VP_STREAM_KX(5, 2) VP_STREAM_KX(6, 2)
+    VP_STREAM_KX(4, 3) VP_STREAM_KX(5, 3)
+    VP_STREAM_CASE(7, 4, 2) VP_STREAM_CASE(7, 5, 2) VP_STREAM_CASE(7, 6, 2) VP_STREAM_CASE(7, 7, 2) VP_STREAM_CASE(7, 8, 2)
+    VP_STREAM_CASE(8, 4, 2) VP_STREAM_CASE(8, 5, 2) VP_STREAM_CASE(8, 6, 2) VP_STREAM_CASE(8, 7, 2) VP_STREAM_CASE(8, 8, 2)
+#define VP_STREAM_LONG(MM, PP) \
+    VP_STREAM_CASE(MM, 20, PP) VP_STREAM_CASE(MM, 24, PP) VP_STREAM_CASE(MM, 28, PP) VP_STREAM_CASE(MM, 32, PP)
+    VP_STREAM_LONG(4, 2) VP_STREAM_LONG(5, 2) VP_STREAM_LONG(6, 2)
+    VP_STREAM_CASE(4, 20, 3) VP_STREAM_CASE(4, 24, 3) VP_STREAM_CASE(5, 20, 3) VP_STREAM_CASE(5, 24, 3)
+#undef VP_STREAM_LONG
+#undef VP_STREAM_KX
+#undef VP_STREAM_CASE
+    return -1;
+}
+
+int VP_CAT(launch_resize_stream_part, VP_PART)(const PlanView& plan, const StreamLaunch& L, void* out,
+                                               hipStream_t stream) {
+#define VP_RS_CASE(MM, KK) \
+    if (const int r = resize_case<MM, KK, __COUNTER__>(plan, L, out, stream); r != -1) return r;
+#define VP_RS_KX(MM) VP_RS_CASE(MM, 8) VP_RS_CASE(MM, 12) VP_RS_CASE(MM, 16) VP_RS_CASE(MM, 20) \
+    VP_RS_CASE(MM, 24) VP_RS_CASE(MM, 28) VP_RS_CASE(MM, 32) VP_RS_CASE(MM, kRsMfmaWindow)
+    VP_RS_KX(4) VP_RS_KX(5) VP_RS_KX(6) VP_RS_KX(7) VP_RS_KX(8)
+#undef VP_RS_KX
+#undef VP_RS_CASE
+    return -1;
+}
+
+#if VP_PART == 0
+
+// Every part's dispatchers (parts 1 .. VP_PARTS - 1 are other translation units).
+#define VP_DECLARE_PART(n)                                                                          \
+    int launch_stream_part##n(const PlanView&, const StreamLaunch&, void*, int, const Norm&, hipStream_t); \
+    int launch_resize_stream_part##n(const PlanView&, const StreamLaunch&, void*, hipStream_t);
+VP_DECLARE_PART(0) VP_DECLARE_PART(1) VP_DECLARE_PART(2) VP_DECLARE_PART(3)
+VP_DECLARE_PART(4) VP_DECLARE_PART(5) VP_DECLARE_PART(6) VP_DECLARE_PART(7)
+#undef VP_DECLARE_PART
+
+namespace {
+using StreamPartFn = int (*)(const PlanView&, const StreamLaunch&, void*, int, const Norm&, hipStream_t);
+using ResizePartFn = int (*)(const PlanView&, const StreamLaunch&, void*, hipStream_t);
+const StreamPartFn kStreamParts[VP_PARTS] = {
+    launch_stream_part0,
+#if VP_PARTS > 1
+    launch_stream_part1,
+#endif
+#if VP_PARTS > 2
+    launch_stream_part2,
+#endif
+#if VP_PARTS > 3
+    launch_stream_part3,
+#endif
+#if VP_PARTS > 4
+    launch_stream_part4,
+#endif
+#if VP_PARTS > 5
+    launch_stream_part5,
+#endif
+#if VP_PARTS > 6
+    launch_stream_part6,
+#endif
+#if VP_PARTS > 7
+    launch_stream_part7,
+#endif
+};
+const ResizePartFn kResizeParts[VP_PARTS] = {
+    launch_resize_stream_part0,
+#if VP_PARTS > 1
+    launch_resize_stream_part1,
+#endif
+#if VP_PARTS > 2
+    launch_resize_stream_part2,
+#endif
+#if VP_PARTS > 3
+    launch_resize_stream_part3,
+#endif
+#if VP_PARTS > 4
+    launch_resize_stream_part4,
+#endif
+#if VP_PARTS > 5
+    launch_resize_stream_part5,
+#endif
+#if VP_PARTS > 6
+    launch_resize_stream_part6,
+#endif
+#if VP_PARTS > 7
+    launch_resize_stream_part7,
+#endif
+};
 }  // namespace
 
 int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t rows,
@@ -1461,25 +1604,11 @@ bool resize_stream_supported(int m, int kx, int px) {
 
 int launch_resize_stream(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
     if (L.count <= 0) return 0;
-    if (L.kx == kRsMfmaWindow) {
-        if (L.px != kRsPx) return static_cast<int>(hipErrorInvalidConfiguration);
-        switch (L.m) {
-            case 4: return launch_resize_mfma_shape<4>(plan, L, out, stream);
-            case 5: return launch_resize_mfma_shape<5>(plan, L, out, stream);
-            case 6: return launch_resize_mfma_shape<6>(plan, L, out, stream);
-            case 7: return launch_resize_mfma_shape<7>(plan, L, out, stream);
-            case 8: return launch_resize_mfma_shape<8>(plan, L, out, stream);
-            default: return static_cast<int>(hipErrorInvalidConfiguration);
-        }
-    }
-    if (!resize_stream_supported(L.m, L.kx, L.px)) return static_cast<int>(hipErrorInvalidConfiguration);
-#define VP_RS_CASE(MM, KK) \
-    if (L.m == MM && L.kx == KK) return launch_resize_stream_shape<MM, KK>(plan, L, out, stream);
-#define VP_RS_KX(MM) VP_RS_CASE(MM, 8) VP_RS_CASE(MM, 12) VP_RS_CASE(MM, 16) VP_RS_CASE(MM, 20) \
-    VP_RS_CASE(MM, 24) VP_RS_CASE(MM, 28) VP_RS_CASE(MM, 32)
-    VP_RS_KX(4) VP_RS_KX(5) VP_RS_KX(6) VP_RS_KX(7) VP_RS_KX(8)
-#undef VP_RS_KX
-#undef VP_RS_CASE
+    if (L.kx == kRsMfmaWindow ? (L.px != kRsPx || L.m < 4 || L.m > kSlotWords)
+                              : !resize_stream_supported(L.m, L.kx, L.px))
+        return static_cast<int>(hipErrorInvalidConfiguration);
+    for (const ResizePartFn part : kResizeParts)
+        if (const int r = part(plan, L, out, stream); r != -1) return r;
     return static_cast<int>(hipErrorInvalidConfiguration);
 }
 
@@ -1528,26 +1657,11 @@ int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int ou
     if (L.count <= 0) return 0;
     if (!stream_shape_supported(L.m, L.kx, L.px) || stream_wave_bytes(L.px, L.kx, 4, L.patch) > kStreamLdsBudget)
         return static_cast<int>(hipErrorInvalidConfiguration);
-#define VP_STREAM_CASE(MM, KK, PP) \
-    if (L.m == MM && L.kx == KK && L.px == PP) \
-        return launch_stream_shape<MM, KK, PP>(plan, L, out, out_dtype, norm, stream);
-#define VP_STREAM_KX(MM, PP) \
-    VP_STREAM_CASE(MM, 4, PP) VP_STREAM_CASE(MM, 5, PP) VP_STREAM_CASE(MM, 6, PP) VP_STREAM_CASE(MM, 7, PP) \
-    VP_STREAM_CASE(MM, 8, PP) VP_STREAM_CASE(MM, 9, PP) VP_STREAM_CASE(MM, 10, PP) VP_STREAM_CASE(MM, 11, PP) \
-    VP_STREAM_CASE(MM, 12, PP) VP_STREAM_CASE(MM, 13, PP) VP_STREAM_CASE(MM, 14, PP) VP_STREAM_CASE(MM, 15, PP) \
-    VP_STREAM_CASE(MM, 16, PP)
-    VP_STREAM_KX(4, 2) VP_STREAM_KX(5, 2) VP_STREAM_KX(6, 2)
-    VP_STREAM_KX(4, 3) VP_STREAM_KX(5, 3)
-    VP_STREAM_CASE(7, 4, 2) VP_STREAM_CASE(7, 5, 2) VP_STREAM_CASE(7, 6, 2) VP_STREAM_CASE(7, 7, 2) VP_STREAM_CASE(7, 8, 2)
-    VP_STREAM_CASE(8, 4, 2) VP_STREAM_CASE(8, 5, 2) VP_STREAM_CASE(8, 6, 2) VP_STREAM_CASE(8, 7, 2) VP_STREAM_CASE(8, 8, 2)
-#define VP_STREAM_LONG(MM, PP) \
-    VP_STREAM_CASE(MM, 20, PP) VP_STREAM_CASE(MM, 24, PP) VP_STREAM_CASE(MM, 28, PP) VP_STREAM_CASE(MM, 32, PP)
-    VP_STREAM_LONG(4, 2) VP_STREAM_LONG(5, 2) VP_STREAM_LONG(6, 2)
-    VP_STREAM_CASE(4, 20, 3) VP_STREAM_CASE(4, 24, 3) VP_STREAM_CASE(5, 20, 3) VP_STREAM_CASE(5, 24, 3)
-#undef VP_STREAM_LONG
-#undef VP_STREAM_KX
-#undef VP_STREAM_CASE
+    for (const StreamPartFn part : kStreamParts)
+        if (const int r = part(plan, L, out, out_dtype, norm, stream); r != -1) return r;
     return static_cast<int>(hipErrorInvalidValue);
 }
+
+#endif  // VP_PART == 0
 
 }  // namespace vp

@@ -110,17 +110,18 @@ struct DevItem {
 static_assert(sizeof(DevItem) == 104, "DevItem layout");
 
 // One streaming work unit: output rows [i0, i1) of padded frame position p
-// of an item; one single-wave workgroup per column band of the unit.
-// flags bit 0: the pair's two frames are the same source frame (an image,
-// or an odd count padded with its last index), so the unit writes both
-// temporal halves of the rows.
+// of an item; one workgroup per column band of the unit.  Bit kUnitBoth of
+// p_flags: the pair's two frames are the same source frame (an image, or an
+// odd count padded with its last index), so the unit writes both temporal
+// halves of the rows.  p < 2^30 always: every frame pair owns at least four
+// of the batch's at most 2^31 - 1 rows.
 struct StreamUnit {
     int32_t item;
-    int32_t p;
-    int32_t rows;    // i0 | (i1 << 16)
-    int32_t flags;
+    int32_t p_flags;   // p | kUnitBoth if the pair's frames are one
+    int32_t i0, i1;    // output rows [i0, i1) of the frame
 };
 static_assert(sizeof(StreamUnit) == 16, "StreamUnit layout");
+constexpr int32_t kUnitBoth = 1 << 30;
 
 struct PlanView {
     const DevItem* items;
@@ -140,9 +141,10 @@ struct Norm {
 };
 
 // Streaming workgroup entries: unit index in the low 20 bits, column band
-// above; kNoWork marks an empty workgroup.
+// (at most kWgBandMax) above; kNoWork marks an empty workgroup.
 constexpr uint32_t kWgUnitMask = (1u << 20) - 1;
 constexpr int kWgBandShift = 20;
+constexpr int kWgBandMax = (1 << (32 - kWgBandShift)) - 2;   // keeps entries below kNoWork
 constexpr uint32_t kNoWork = 0xffffffffu;
 
 // One launch of the streaming kernel: workgroups wgs[first, first + count),
