@@ -19,11 +19,17 @@
  *
  * Conventions shared by every entry point:
  *  - Return value: a vp_status code; VP_OK (0) on success.  No function
- *    throws, aborts or prints.  On any non-OK status nothing has been
- *    enqueued on the stream and no output buffer has been written, except
- *    that *out_count / *workspace_bytes style size outputs report the size
- *    that would have been needed (strict failure: never truncate or pad,
- *    Section 3.2.2).
+ *    throws, aborts or prints.  Every argument is validated on the host
+ *    before anything is enqueued, so on any non-OK status other than
+ *    VP_ERR_HIP nothing has been enqueued on the stream and no output
+ *    buffer has been written, except that *out_count / *workspace_bytes
+ *    style size outputs report the size that would have been needed (strict
+ *    failure: never truncate or pad, Section 3.2.2).
+ *  - VP_ERR_HIP is the one exception: a HIP runtime call failed after the
+ *    checks passed.  Whatever the call had enqueued before that point (the
+ *    plan copy into the workspace, earlier kernel launches) stays enqueued
+ *    and the stream still orders after it, but the outputs are undefined.
+ *    The message names the failing runtime call.
  *  - vp_last_error_message() returns a thread-local, human-readable detail
  *    of the last non-OK status on the calling thread.
  *  - All functions are thread-safe.  Calls that enqueue work on the same

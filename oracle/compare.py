@@ -17,11 +17,17 @@ BF16_ULPS = 1
 
 
 def bf16_bits_rne(y: np.ndarray) -> np.ndarray:
-    """Round-to-nearest-even bfloat16 bit patterns of double values (via float32)."""
-    f = np.asarray(y, dtype=np.float64).astype(np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    u = (u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)
-    return u.astype(np.uint16)
+    """Round-to-nearest-even bfloat16 bit patterns of double values, rounded
+    once, straight from the double (no float32 step, which could round a
+    value onto a bfloat16 tie first).  bfloat16 keeps 8 significant bits and
+    float32's exponent range; values below the smallest normal (2^-126) round
+    on the subnormal grid of 2^-133.  Finite inputs only."""
+    y = np.asarray(y, dtype=np.float64)
+    m, e = np.frexp(y)                          # y = m * 2^e, 0.5 <= |m| < 1 (m = 0 for y = 0)
+    e = np.maximum(e, -125)                     # the smallest normal 2^-126 has e = -125
+    q = np.rint(np.ldexp(y, 8 - e))             # significand on the 8-bit grid, ties to even (exact)
+    v = np.ldexp(q, e - 8).astype(np.float32)   # a bfloat16 value: exact in float32
+    return (v.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
 
 
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
@@ -50,3 +56,15 @@ def check_bf16(gpu_bits: np.ndarray, ref: np.ndarray) -> dict:
     good &= np.isfinite(g)
     return dict(ok=bool(good.all()), n_bad=int((~good).sum()), max_ulps=int(ulps.max()) if ulps.size else 0,
                 max_err=float(np.nanmax(err)) if err.size else 0.0, n=int(err.size))
+
+
+def merge(results) -> dict:
+    """One result from the results of several parts of an output (the parts
+    are checked separately, e.g. one frame pair at a time)."""
+    results = list(results)
+    out = dict(ok=all(r["ok"] for r in results), n_bad=sum(r["n_bad"] for r in results),
+               max_err=max((r["max_err"] for r in results), default=0.0),
+               n=sum(r["n"] for r in results))
+    if any("max_ulps" in r for r in results):
+        out["max_ulps"] = max((r.get("max_ulps", 0) for r in results), default=0)
+    return out

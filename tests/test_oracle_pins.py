@@ -575,6 +575,35 @@ def test_resize_u8_equals_pillow_bicubic(H, W, h, w):
         assert np.array_equal(oracle.resize_u8(img, h, w), ref)
 
 
+# Float resampling at the workloads' shapes: the 240x320, 480x854, 1080x1920
+# and 720x1280 videos, the three video sizes of the mixed batch, two of its
+# images (one upscaled) and a small upscale.
+PIL_FLOAT_SHAPES = [
+    (240, 320, 128, 160), (480, 854, 352, 640), (1080, 1920, 448, 800), (720, 1280, 256, 448),
+    (360, 640, 320, 576), (720, 1280, 320, 576), (333, 257, 320, 256), (1000, 712, 992, 704),
+    (40, 50, 64, 96),
+]
+
+
+@pytest.mark.parametrize("H,W,h,w", PIL_FLOAT_SHAPES)
+def test_resize_frame_equals_pillow_float_bicubic(H, W, h, w):
+    """The float resampling (no rounding or clamping between passes) agrees
+    with Pillow's BICUBIC resize of 32-bit float images ('F' mode), an
+    independent implementation of the same antialiased Keys filter, per
+    channel.  Pillow keeps its intermediate and result in float32, which
+    puts its values within a few 1e-5 pixel levels of the double-precision
+    ones; a wrong filter parameter, window or normalisation is off by far
+    more than the 1e-4 allowed."""
+    PIL = pytest.importorskip("PIL.Image")
+    rng = np.random.default_rng(H * 31 + W * 7 + h)
+    frame = rng.integers(0, 256, size=(H, W, 3), dtype=np.uint8)
+    ours = oracle.resize_frame(frame, h, w)
+    for c in range(3):
+        ref = np.asarray(PIL.fromarray(frame[:, :, c].astype(np.float32), "F").resize((w, h), PIL.BICUBIC),
+                         dtype=np.float64)
+        assert np.abs(ours[c] - ref).max() <= 1e-4
+
+
 def test_fixed_weights_are_rounded_float_weights():
     # exact 2x downscale interior: the dyadic weights scale to integers
     lo, q = oracle.fixed_weights(320, 160, 40)
