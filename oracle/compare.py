@@ -52,9 +52,12 @@ def check_bf16(gpu_bits: np.ndarray, ref: np.ndarray) -> dict:
     g = bf16_to_f64(gpu_bits)
     err = np.abs(g - ref)
     ulps = np.abs(_ordered(gpu_bits) - _ordered(bf16_bits_rne(ref)))
-    good = (ulps <= BF16_ULPS) | (err <= F32_ATOL)
+    beyond_floor = ~(err <= F32_ATOL)
+    good = (ulps <= BF16_ULPS) | ~beyond_floor
     good &= np.isfinite(g)
-    return dict(ok=bool(good.all()), n_bad=int((~good).sum()), max_ulps=int(ulps.max()) if ulps.size else 0,
+    # max_ulps: the largest ulp distance where the absolute floor does not apply
+    return dict(ok=bool(good.all()), n_bad=int((~good).sum()),
+                max_ulps=int(ulps[beyond_floor].max()) if beyond_floor.any() else 0,
                 max_err=float(np.nanmax(err)) if err.size else 0.0, n=int(err.size))
 
 

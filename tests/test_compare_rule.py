@@ -70,7 +70,7 @@ def test_check_bf16_tolerance():
     two_ulp = one_ulp.copy()
     two_ulp[0] = 0x3F82
     r = compare.check_bf16(two_ulp, y)
-    assert not r["ok"] and r["n_bad"] == 1
+    assert not r["ok"] and r["n_bad"] == 1 and r["max_ulps"] == 2
     # far in ulps but within the absolute floor of 2e-5: passes
     tiny = np.array([1.5e-5])
     assert compare.check_bf16(compare.bf16_bits_rne(np.array([0.0])), tiny)["ok"]
