@@ -229,6 +229,33 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
                             void* workspace, int64_t workspace_bytes, hipStream_t stream);
 
 /*
+ * vp_preprocess_batch for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and outputs, with no workspace argument.
+ * The plan goes to a fixed array of device memory inside the library,
+ * VP_NOALLOC_PLAN_BYTES (16 MiB) per device, held by every device the
+ * library runs on until the process ends; it is copied there on `stream`
+ * from pageable host memory, and every kernel runs on `stream` itself (no
+ * side streams).  The call allocates no device memory, creates no stream or
+ * event, and makes no hipMalloc, hipHostMalloc or hipFree call; its first
+ * call on a device looks up that device's copy of the array.
+ * All calls on one device share the array, which keeps the last call's plan:
+ * calls whose work can overlap on one device (different streams, or other
+ * threads, without synchronisation between them) race and give undefined
+ * output.  Calls on one stream are ordered and safe.
+ * Arguments, outputs, ownership and asynchrony otherwise as for
+ * vp_preprocess_batch.
+ * Errors: as vp_preprocess_batch, with VP_ERR_CAPACITY when the batch's plan
+ * (the workspace_bytes of vp_batch_layout) exceeds VP_NOALLOC_PLAN_BYTES;
+ * this and every other argument check happens before any HIP call.
+ */
+#define VP_NOALLOC_PLAN_BYTES (16 * 1024 * 1024)
+int32_t vp_preprocess_batch_noalloc(const vp_item* items, int32_t n_items, const float* mean,
+                                    const float* std, int32_t out_dtype, void* out_rows,
+                                    int64_t out_rows_capacity, int32_t* grid_thw,
+                                    int32_t* cu_seqlens, hipStream_t stream);
+
+/*
  * Normalise and patchify frames that are already at the target size: the
  * cached path of Section 3.1.1, where sampling and resizing were done once
  * offline and every RL stage still rescales, normalises and patchifies.

@@ -29,6 +29,7 @@ VP_SAMPLE_UNIFORM, VP_SAMPLE_FPS = 0, 1
 VP_OUT_F32, VP_OUT_BF16 = 0, 1
 VP_ROW = 1536
 VP_PATCH = 16
+VP_NOALLOC_PLAN_BYTES = 16 * 1024 * 1024
 
 
 def row_width(patch: int = VP_PATCH) -> int:
@@ -38,7 +39,8 @@ def row_width(patch: int = VP_PATCH) -> int:
 VP_FACTOR = 32
 
 EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
-            "vp_filter_table_fixed", "vp_batch_layout", "vp_preprocess_batch", "vp_patchify_batch",
+            "vp_filter_table_fixed", "vp_batch_layout", "vp_preprocess_batch",
+            "vp_preprocess_batch_noalloc", "vp_patchify_batch",
             "vp_resize_layout", "vp_resize_batch", "vp_position_ids", "vp_status_string",
             "vp_last_error_message", "vp_set_kernel_events")
 
@@ -83,6 +85,8 @@ def lib() -> ctypes.CDLL:
         L.vp_preprocess_batch.argtypes = [itemp, i32, f32p, f32p, i32, ctypes.c_void_p, i64,
                                           i32p, i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
         L.vp_patchify_batch.argtypes = L.vp_preprocess_batch.argtypes
+        L.vp_preprocess_batch_noalloc.argtypes = [itemp, i32, f32p, f32p, i32, ctypes.c_void_p, i64,
+                                                  i32p, i32p, ctypes.c_void_p]
         L.vp_filter_table_fixed.argtypes = [i32, i32, i32, i32p, i32p, i32p]
         L.vp_position_ids.argtypes = [itemp, i32, ctypes.c_void_p, ctypes.c_void_p, i64, i32p, i32,
                                       i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
@@ -240,6 +244,31 @@ def vp_preprocess_batch(items: Sequence, mean, std, out_dtype: int, out_rows, wo
     bfloat16 matching out_dtype; workspace: device uint8 tensor of at least
     the layout's workspace_bytes.  Returns (grid_thw, cu_seqlens)."""
     return _run("vp_preprocess_batch", items, mean, std, out_dtype, out_rows, workspace, stream)
+
+
+def vp_preprocess_batch_noalloc(items: Sequence, mean, std, out_dtype: int, out_rows, stream=None):
+    """As vp_preprocess_batch with no workspace: the plan goes to the library's
+    fixed device memory (at most VP_NOALLOC_PLAN_BYTES), and nothing is
+    allocated.  Calls whose work can overlap on one device race; calls on one
+    stream are ordered.  Returns (grid_thw, cu_seqlens)."""
+    import torch
+    want = torch.bfloat16 if out_dtype == VP_OUT_BF16 else torch.float32
+    width = row_width(getattr(items[0], "patch", VP_PATCH)) if len(items) else VP_ROW
+    if out_rows.dtype != want or out_rows.dim() != 2 or out_rows.shape[1] != width \
+            or not out_rows.is_contiguous() or not out_rows.is_cuda:
+        raise VPError(VP_ERR_ARG, f"out_rows must be a contiguous CUDA [rows, {width}] {want} tensor")
+    b = _Batch(items)
+    B = len(b)
+    m = np.ascontiguousarray(np.asarray(mean, np.float32).reshape(3))
+    s = np.ascontiguousarray(np.asarray(std, np.float32).reshape(3))
+    grid = np.zeros((B, 3), np.int32)
+    cu = np.zeros(B + 1, np.int32)
+    _check(lib().vp_preprocess_batch_noalloc(
+        b.arr, B, _ptr(m, ctypes.c_float), _ptr(s, ctypes.c_float), out_dtype,
+        ctypes.c_void_p(out_rows.data_ptr()), out_rows.shape[0], _ptr(grid, ctypes.c_int32),
+        _ptr(cu, ctypes.c_int32), ctypes.c_void_p(_stream_handle(stream))),
+        "vp_preprocess_batch_noalloc")
+    return grid, cu
 
 
 def vp_patchify_batch(items: Sequence, mean, std, out_dtype: int, out_rows, workspace,

@@ -1189,6 +1189,25 @@ int32_t hip_fail(hipError_t e, const char* what) {
     return fail(VP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Writes the plan blob (p.bytes bytes, the layout of vp_plan.h) to `base`:
+// each section, then zeros up to the next one (the gaps are never read;
+// zeroing them keeps the blob deterministic).
+void pack_plan(const Plan& p, uint8_t* base) {
+    auto put = [&](size_t off, const void* src, size_t n, size_t next) {
+        if (n != 0) std::memcpy(base + off, src, n);
+        std::memset(base + off + n, 0, next - off - n);
+    };
+    put(p.off_items, p.items.data(), sizeof(vp::DevItem) * p.items.size(), p.off_prefix);
+    put(p.off_prefix, p.prefix.data(), sizeof(int32_t) * p.prefix.size(), p.off_indices);
+    put(p.off_indices, p.indices.data(), sizeof(int32_t) * p.indices.size(), p.off_tables);
+    for (const auto& part : p.tables)
+        std::memcpy(base + p.off_tables + sizeof(int32_t) * part.first, part.second->data(),
+                    sizeof(int32_t) * part.second->size());
+    put(p.off_tables + sizeof(int32_t) * p.table_words, nullptr, 0, p.off_units);
+    put(p.off_units, p.units.data(), sizeof(vp::StreamUnit) * p.units.size(), p.off_wgs);
+    put(p.off_wgs, p.wgs.data(), sizeof(uint32_t) * p.wgs.size(), p.bytes);
+}
+
 int32_t upload_plan(const Plan& p, void* workspace, hipStream_t stream) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -1215,22 +1234,7 @@ int32_t upload_plan(const Plan& p, void* workspace, hipStream_t stream) {
         if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
         s.cap = cap;
     }
-    auto* base = static_cast<uint8_t*>(s.host);
-    // each section, then zeros up to the next one (the gaps are never read;
-    // zeroing them keeps the blob deterministic)
-    auto put = [&](size_t off, const void* src, size_t n, size_t next) {
-        if (n != 0) std::memcpy(base + off, src, n);
-        std::memset(base + off + n, 0, next - off - n);
-    };
-    put(p.off_items, p.items.data(), sizeof(vp::DevItem) * p.items.size(), p.off_prefix);
-    put(p.off_prefix, p.prefix.data(), sizeof(int32_t) * p.prefix.size(), p.off_indices);
-    put(p.off_indices, p.indices.data(), sizeof(int32_t) * p.indices.size(), p.off_tables);
-    for (const auto& part : p.tables)
-        std::memcpy(base + p.off_tables + sizeof(int32_t) * part.first, part.second->data(),
-                    sizeof(int32_t) * part.second->size());
-    put(p.off_tables + sizeof(int32_t) * p.table_words, nullptr, 0, p.off_units);
-    put(p.off_units, p.units.data(), sizeof(vp::StreamUnit) * p.units.size(), p.off_wgs);
-    put(p.off_wgs, p.wgs.data(), sizeof(uint32_t) * p.wgs.size(), p.bytes);
+    pack_plan(p, static_cast<uint8_t*>(s.host));
     e = hipMemcpyAsync(workspace, s.host, p.bytes, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
     e = hipEventRecord(s.done, stream);
@@ -1294,8 +1298,11 @@ int32_t side_for_device(int dev, Side** out) {
 // streaming shape), spread over the caller's stream and the side streams by
 // estimated cost.  `resize`: the uint8 writer's kernels instead of the float
 // path's (out_dtype and norm unused).
+// With `one_stream` every launch goes to the caller's stream, one after
+// another (no side streams, nothing created).
 int32_t run_launches(const Plan& p, const vp::PlanView& view, void* out_rows, int32_t out_dtype,
-                     const vp::Norm& norm, hipStream_t stream, bool resize = false) {
+                     const vp::Norm& norm, hipStream_t stream, bool resize = false,
+                     bool one_stream = false) {
     struct Job {
         int32_t launch;   // index into p.launches, or -1 for the general kernel
         int64_t cost;
@@ -1319,6 +1326,11 @@ int32_t run_launches(const Plan& p, const vp::PlanView& view, void* out_rows, in
         return VP_OK;
     };
     if (jobs.size() <= 1) return jobs.empty() ? VP_OK : launch(jobs[0], stream);
+    if (one_stream) {
+        for (const Job& j : jobs)
+            if (const int32_t st = launch(j, stream); st != VP_OK) return st;
+        return VP_OK;
+    }
 
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -1357,19 +1369,23 @@ int32_t run_launches(const Plan& p, const vp::PlanView& view, void* out_rows, in
     return st;
 }
 
-// Shared body of vp_preprocess_batch (resample + normalise + patchify) and
-// vp_patchify_batch (frames already at the target size).
+// Shared body of vp_preprocess_batch (resample + normalise + patchify),
+// vp_patchify_batch (frames already at the target size) and
+// vp_preprocess_batch_noalloc (no_alloc: the plan goes to the library's
+// fixed device array instead of a workspace, copied from pageable host
+// memory, and every launch runs on the caller's stream).
 int32_t run_batch(bool patch_only, const vp_item* items, int32_t n_items, const float* mean,
                   const float* std, int32_t out_dtype, void* out_rows, int64_t out_rows_capacity,
                   int32_t* grid_thw, int32_t* cu_seqlens, void* workspace, int64_t workspace_bytes,
-                  hipStream_t stream) {
-    if (mean == nullptr || std == nullptr || out_rows == nullptr || workspace == nullptr)
-        return fail(VP_ERR_NULL, "mean, std, out_rows and workspace must be non-NULL");
+                  hipStream_t stream, bool no_alloc = false) {
+    if (mean == nullptr || std == nullptr || out_rows == nullptr || (!no_alloc && workspace == nullptr))
+        return fail(VP_ERR_NULL, no_alloc ? "mean, std and out_rows must be non-NULL"
+                                          : "mean, std, out_rows and workspace must be non-NULL");
     if (out_dtype != VP_OUT_F32 && out_dtype != VP_OUT_BF16)
         return fail(VP_ERR_ARG, "out_dtype must be VP_OUT_F32 or VP_OUT_BF16");
     if (reinterpret_cast<uintptr_t>(out_rows) % 16 != 0)
         return fail(VP_ERR_ARG, "out_rows must be 16-byte aligned");
-    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+    if (!no_alloc && reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
         return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
     vp::Norm norm;
     for (int c = 0; c < 3; ++c) {
@@ -1385,11 +1401,26 @@ int32_t run_batch(bool patch_only, const vp_item* items, int32_t n_items, const 
     if (out_rows_capacity < p.total_rows)
         return fail(VP_ERR_CAPACITY, "out_rows holds " + std::to_string(out_rows_capacity) +
                                          " rows, batch needs " + std::to_string(p.total_rows));
-    if (workspace_bytes < static_cast<int64_t>(p.bytes))
-        return fail(VP_ERR_CAPACITY, "workspace holds " + std::to_string(workspace_bytes) +
-                                         " bytes, plan needs " + std::to_string(p.bytes));
-    st = upload_plan(p, workspace, stream);
-    if (st != VP_OK) return st;
+    if (no_alloc) {
+        if (p.bytes > static_cast<size_t>(vp::kNoAllocPlanBytes))
+            return fail(VP_ERR_CAPACITY, "the plan needs " + std::to_string(p.bytes) +
+                                             " bytes; the library's fixed plan memory holds " +
+                                             std::to_string(vp::kNoAllocPlanBytes));
+        const int err = vp::noalloc_plan_memory(&workspace);
+        if (err != 0) return hip_fail(static_cast<hipError_t>(err), "hipGetSymbolAddress (plan memory)");
+        // pageable host memory: the copy has read it when hipMemcpyAsync returns
+        thread_local std::vector<uint8_t> blob;
+        if (blob.size() < p.bytes) blob.resize(p.bytes);
+        pack_plan(p, blob.data());
+        const hipError_t e = hipMemcpyAsync(workspace, blob.data(), p.bytes, hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (plan)");
+    } else {
+        if (workspace_bytes < static_cast<int64_t>(p.bytes))
+            return fail(VP_ERR_CAPACITY, "workspace holds " + std::to_string(workspace_bytes) +
+                                             " bytes, plan needs " + std::to_string(p.bytes));
+        st = upload_plan(p, workspace, stream);
+        if (st != VP_OK) return st;
+    }
     hipEvent_t t_start = g_timing_start, t_stop = g_timing_stop;
     g_timing_start = g_timing_stop = nullptr;
     if (t_start != nullptr) {
@@ -1410,7 +1441,7 @@ int32_t run_batch(bool patch_only, const vp_item* items, int32_t n_items, const 
         const int err = vp::launch_patchify(view, out_rows, out_dtype, norm, p.items[0].patch, stream);
         if (err != 0) return hip_fail(static_cast<hipError_t>(err), "patchify kernel launch");
     } else {
-        st = run_launches(p, view, out_rows, out_dtype, norm, stream);
+        st = run_launches(p, view, out_rows, out_dtype, norm, stream, false, no_alloc);
         if (st != VP_OK) return st;
     }
     if (t_stop != nullptr) {
@@ -1552,6 +1583,14 @@ int32_t vp_preprocess_batch(const vp_item* items, int32_t n_items, const float* 
                             void* workspace, int64_t workspace_bytes, hipStream_t stream) {
     return run_batch(false, items, n_items, mean, std, out_dtype, out_rows, out_rows_capacity,
                      grid_thw, cu_seqlens, workspace, workspace_bytes, stream);
+}
+
+int32_t vp_preprocess_batch_noalloc(const vp_item* items, int32_t n_items, const float* mean,
+                                    const float* std, int32_t out_dtype, void* out_rows,
+                                    int64_t out_rows_capacity, int32_t* grid_thw,
+                                    int32_t* cu_seqlens, hipStream_t stream) {
+    return run_batch(false, items, n_items, mean, std, out_dtype, out_rows, out_rows_capacity,
+                     grid_thw, cu_seqlens, nullptr, 0, stream, true);
 }
 
 int32_t vp_patchify_batch(const vp_item* items, int32_t n_items, const float* mean,

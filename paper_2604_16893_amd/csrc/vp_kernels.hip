@@ -36,6 +36,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <map>
+#include <mutex>
 #include <type_traits>
 
 #include "vp_plan.h"
@@ -1581,6 +1583,32 @@ const ResizePartFn kResizeParts[VP_PARTS] = {
 #endif
 };
 }  // namespace
+
+// The plan memory of vp_preprocess_batch_noalloc: a file-scope device
+// array, so that a caller that cannot allocate device memory needs no
+// workspace.  Every device the library runs on holds its own copy until the
+// process ends.  In host code the array's name is not a device address: the
+// address of the current device's copy is looked up with
+// hipGetSymbolAddress, once per device, and only that address is used.
+__device__ __align__(256) unsigned char scratch[kNoAllocPlanBytes];
+
+int noalloc_plan_memory(void** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return static_cast<int>(e);
+    static std::mutex mu;
+    static std::map<int, void*> by_device;
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = by_device.find(dev);
+    if (it == by_device.end()) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return static_cast<int>(e);
+        it = by_device.emplace(dev, p).first;
+    }
+    *ptr = it->second;
+    return 0;
+}
 
 int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t rows,
                      hipStream_t stream) {

@@ -156,6 +156,13 @@ struct StreamLaunch {
     int64_t cost;            // host only: estimated work (source pixels read)
 };
 
+// Fixed device memory for the plan of vp_preprocess_batch_noalloc, one array
+// per device (vp_kernels.hip), and its size.  noalloc_plan_memory() gives the
+// current device's copy of the array, looked up once per device; it returns
+// a hipError_t value.
+constexpr int64_t kNoAllocPlanBytes = int64_t(16) << 20;
+int noalloc_plan_memory(void** ptr);
+
 // Kernel launchers (vp_kernels.hip).  Return a hipError_t value.
 int launch_generic(const PlanView& plan, void* out, int out_dtype, const Norm& norm,
                    hipStream_t stream);

@@ -194,6 +194,38 @@ def test_preprocess_errors_before_any_gpu_work():
     assert b"outside [0, 4)" in vp.lib().vp_last_error_message()
 
 
+def _raw_noalloc(items, mean=(0.5, 0.5, 0.5), std=(0.5, 0.5, 0.5), dtype=vp.VP_OUT_BF16,
+                 out=0x100000, cap=1 << 40):
+    b = vp._Batch(items)
+    m = (ctypes.c_float * 3)(*mean)
+    s = (ctypes.c_float * 3)(*std)
+    return vp.lib().vp_preprocess_batch_noalloc(b.arr, len(b), m, s, dtype, ctypes.c_void_p(out), cap,
+                                                None, None, None)
+
+
+def test_noalloc_errors_before_any_gpu_work():
+    """The no-allocation entry checks everything on the host first, including
+    that the plan fits the library's fixed plan memory (16 MiB), so these
+    calls make no HIP call at all (none is possible here)."""
+    ok = vp.Item((0x10000, 4, 100, 100), [0, 3], 64, 64)
+    _, _, rows, _ = vp.vp_batch_layout([ok])
+    assert _raw_noalloc([ok], std=(0.5, 0.0, 0.5)) == vp.VP_ERR_ARG
+    assert _raw_noalloc([ok], dtype=5) == vp.VP_ERR_ARG
+    assert _raw_noalloc([ok], out=0x100004) == vp.VP_ERR_ARG
+    assert _raw_noalloc([ok], out=0) == vp.VP_ERR_NULL
+    assert _raw_noalloc([ok], cap=rows - 1) == vp.VP_ERR_CAPACITY
+    assert _raw_noalloc([vp.Item((0x10000, 4, 100, 100), [4], 64, 64)]) == vp.VP_ERR_INDEX
+    # 262,144 frames of 720x1280 -> 256x448: one work unit and seven
+    # workgroup entries per frame, a plan of about 11.5 MB -- within the limit;
+    # twice as many frames need about 23 MB and are refused
+    frames = (0x10000, 2, 720, 1280)
+    small = [vp.Item(frames, [0, 1] * 2048, 256, 448) for _ in range(64)]
+    big = small + small
+    assert vp.vp_batch_layout(small)[3] <= vp.VP_NOALLOC_PLAN_BYTES < vp.vp_batch_layout(big)[3]
+    assert _raw_noalloc(big) == vp.VP_ERR_CAPACITY
+    assert b"fixed plan memory" in vp.lib().vp_last_error_message()
+
+
 def _raw_patchify(items, mean=(0.5, 0.5, 0.5), std=(0.5, 0.5, 0.5), dtype=vp.VP_OUT_BF16,
                   out=0x100000, cap=1 << 30, ws=0x200000, ws_bytes=1 << 30):
     b = vp._Batch(items)
