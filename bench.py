@@ -1,28 +1,37 @@
 #!/usr/bin/env python3
 """Throughput of the video-frame preprocessing path on one MI355X.
 
-Workload (default, the rollout-sized batch): 64 videos x 256 decoded frames of
-720x1280 uint8 RGB, resident in HBM (45.3 GB), each frame resampled to
-256x448 (smart_resize under 122880 px), normalised with per-channel
-mean/std (0.481, 0.458, 0.408)/(0.269, 0.261, 0.276) and patchified into
-3,670,016 merge-window rows of 1536 bfloat16 values, on one stream.
+Headline workload (default): the rollout-sized batch, 64 videos x 256
+decoded frames of 720x1280 uint8 RGB resident in HBM (45.3 GB), each frame
+resampled to 256x448 (smart_resize under 122880 px), normalised with
+per-channel mean/std (0.481, 0.458, 0.408)/(0.269, 0.261, 0.276) and
+patchified into 3,670,016 merge-window rows of 1536 bfloat16 values, on one
+stream.
 
 One step is one pass of the whole path over the batch: per item the target
 size (vp_smart_resize_dims) and the frame indices (vp_sample_indices) on the
-host, then vp_preprocess_batch (host plan and filter tables, one plan upload,
-the resampling/normalise/patchify kernel) on the stream.  W untimed warm-up
+host, then vp_preprocess_batch (host plan, one plan upload, the
+resampling/normalise/patchify kernels) on the stream.  W untimed warm-up
 steps, then K steps timed with a synchronize on both sides.  Prints one JSON
 line on stdout; progress goes to stderr.
 
-value      = sampled source frames per second over the K timed steps.
-roofline   = algorithmic HBM bytes of one call (every sampled u8 frame read
-             once + every output row written once) / the mean device time of
-             the call's kernels, from HIP events that the library records on
-             the stream the kernels run on (vp_set_kernel_events).
+value        = sampled source frames per second over the K timed steps.
+roofline     = algorithmic HBM bytes of one call (every sampled u8 frame read
+               once + every output row written once) / the mean device time
+               of the call's kernels, from HIP events that the library
+               records on the stream the kernels run on.
+per_config   = the same figures for the four other workloads (the 240x320,
+               480x854 and 1080x1920 videos and the mixed image/video
+               batch), measured in the same run after the headline steps.
+ceiling      = a plain device-to-device copy (torch copy_) in the same run:
+               the bandwidth a simple streaming kernel reaches on this GPU.
 cpu_baseline = the CPU oracle (double precision, unmodified) on a bounded
-             sample of the same workload, on this host's cores.
+               sample of the headline workload, on this host's cores, with a
+               single-thread figure; its output is compared with the GPU's
+               rows of the same frames (parity of the sample).
 """
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -33,6 +42,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+CPU_SHARE = 16   # host threads a one-GPU share of the machine offers
 
 
 def log(msg):
@@ -60,46 +70,218 @@ def counter_traffic(workload_tag: str, sha: str):
     return d.get("hbm_bytes_per_call")
 
 
-def cpu_baseline(wl, frames_dev, planned, patch_only=False, resize_only=False, budget_s=12.0):
-    """The oracle, item by item in workload order, until `budget_s` seconds of
-    oracle time have been spent (or the workload is done).  Each item's frame
-    pairs are copied to the host and spread over a thread pool (ctypes
-    releases the GIL); only the oracle calls are timed."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+class Run:
+    """One workload on the device: its frames, planned items, output and workspace."""
+
+    def __init__(self, vp, workloads, torch, wl, dev, mode="preprocess"):
+        self.vp, self.torch, self.wl, self.mode = vp, torch, wl, mode
+        self.frames = [workloads.frames_torch(it, dev, chunk=32) for it in wl.items]
+        self.vitems, self.planned = self.plan_items()
+        code = vp.VP_OUT_BF16 if wl.out_dtype == "bf16" else vp.VP_OUT_F32
+        self.code = code
+        if mode == "resize":
+            frame_off, ws = vp.vp_resize_layout(self.vitems)
+            self.rows = 0
+            self.out = torch.empty(int(frame_off[-1]), dtype=torch.uint8, device=dev)
+        elif mode == "positions":
+            _, _, self.rows, ws = vp.vp_batch_layout(self.vitems)
+            self.out = torch.empty((self.rows, 3), dtype=torch.int32, device=dev)
+            self.out_llm = torch.empty((self.rows // 4, 3), dtype=torch.int32, device=dev)
+        else:
+            _, _, self.rows, ws = vp.vp_batch_layout(self.vitems)
+            self.out = torch.empty((self.rows, vp.row_width(wl.items[0].patch)),
+                                   dtype=torch.bfloat16 if code == vp.VP_OUT_BF16 else torch.float32,
+                                   device=dev)
+        self.work = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
+        self.n_frames = sum(len(p[2]) for p in self.planned)
+        in_bytes = sum(len(p[2]) * it.frame_bytes for p, it in zip(self.planned, wl.items))
+        out_bytes = self.out.numel() * self.out.element_size()
+        if mode == "positions":   # no frame is read; both tables are written
+            in_bytes = 0
+            out_bytes += self.out_llm.numel() * self.out_llm.element_size()
+        self.in_bytes, self.out_bytes = in_bytes, out_bytes
+        self.alg_bytes = in_bytes + out_bytes
+
+    def plan_items(self):
+        vp = self.vp
+        vitems, planned = [], []
+        for it, fr in zip(self.wl.items, self.frames):
+            if it.dims is not None:
+                h, w = it.dims
+            else:
+                h, w = vp.vp_smart_resize_dims(it.H, it.W, 2 * it.patch, it.min_pixels, it.max_pixels)
+            s = it.sample
+            if s["mode"] == "uniform":
+                idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_UNIFORM, s["n"])
+            else:
+                idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_FPS, 0, s["video_fps"], s["fps"],
+                                           s["min_frames"], s["max_frames"])
+            vitems.append(vp.Item(fr, idx, h, w, it.patch))
+            planned.append((h, w, idx))
+        return vitems, planned
+
+    def step(self, stream):
+        """One pass of the whole path: host sizes and indices, then the call."""
+        vp = self.vp
+        items, _ = self.plan_items()
+        if self.mode == "resize":
+            vp.vp_resize_batch(items, self.out, self.work, stream)
+        elif self.mode == "positions":
+            vp.vp_position_ids(items, self.out, self.out_llm, self.work, stream)
+        elif self.mode == "patchify":
+            vp.vp_patchify_batch(items, self.wl.mean, self.wl.std, self.code, self.out, self.work, stream)
+        else:
+            vp.vp_preprocess_batch(items, self.wl.mean, self.wl.std, self.code, self.out, self.work, stream)
+
+    def timed(self, stream, steps):
+        """Time `steps` steps: (wall seconds, per-step kernel ms, per-step call
+        ms, per-step device time from the call's start to its first kernel,
+        per-step host ms)."""
+        torch = self.torch
+        pair = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        call_evs = [pair() for _ in range(steps)]
+        kern_evs = [pair() for _ in range(steps)]
+        for a, b in kern_evs + call_evs:   # HIP events exist once recorded
+            a.record(stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        host = []
+        t0 = time.perf_counter()
+        for k in range(steps):
+            h0 = time.perf_counter()
+            call_evs[k][0].record(stream)
+            self.vp.vp_set_kernel_events(*kern_evs[k])
+            self.step(stream)
+            call_evs[k][1].record(stream)
+            host.append((time.perf_counter() - h0) * 1e3)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return (wall, [a.elapsed_time(b) for a, b in kern_evs], [a.elapsed_time(b) for a, b in call_evs],
+                [c[0].elapsed_time(k[0]) for c, k in zip(call_evs, kern_evs)], host)
+
+
+def copy_ceiling(torch, dev, nbytes=4 << 30, reps=12):
+    """Plain device-to-device copies: (best GB/s counting read + write bytes,
+    ms of the best copy).  Run before the steps, this also brings the GPU
+    out of its idle clocks."""
+    src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    best = 1e30
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        torch.cuda.synchronize()
+        best = min(best, a.elapsed_time(b))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * nbytes / (best * 1e-3) / 1e9, best
+
+
+def cpu_baseline(run, budget_s=10.0, single_s=2.5, patch_only=False, resize_only=False):
+    """The oracle on the first items of the workload, in order, until about
+    `budget_s` seconds of oracle time on a thread pool (frame pairs spread
+    over the threads; ctypes releases the GIL), then about `single_s` seconds
+    on one thread.  The oracle's rows of the sampled items are compared with
+    the GPU's rows of the same items (the last timed step's output)."""
     import concurrent.futures as cf
 
     import numpy as np
 
     import oracle
+    from oracle import compare
     oracle.lib()
-    cores = min(16, os.cpu_count() or 1)
+    wl, vp, torch = run.wl, run.vp, run.torch
+    threads = max(1, min(CPU_SHARE, os.cpu_count() or 1))
+    patch = wl.items[0].patch
+    results = []
+
+    def jobs_of(b):
+        h, w, idx = run.planned[b]
+        padded = list(idx) + ([idx[-1]] if len(idx) % 2 else [])
+        host = run.frames[b].cpu().numpy()
+        if resize_only:
+            return [(np.ascontiguousarray(host[list(idx)]), h, w, None)]
+        return [(np.ascontiguousarray(host[[padded[2 * tt], padded[2 * tt + 1]]]), h, w, tt)
+                for tt in range(len(padded) // 2)]
+
+    def oracle_call(j):
+        frames, h, w, tt = j
+        if resize_only:
+            return oracle.resize_u8_item(frames, list(range(len(frames))), h, w)
+        if patch_only:
+            return oracle.patchify_item(frames, [0, 1], wl.mean, wl.std, patch=patch)
+        return oracle.preprocess_item(frames, [0, 1], h, w, wl.mean, wl.std, patch=patch)
+
+    def check(b, jobs, refs):
+        if resize_only:
+            return None
+        h, w, _ = run.planned[b]
+        per_t = (h // patch) * (w // patch)
+        cu = np.concatenate([[0], np.cumsum([((len(p[2]) + 1) // 2) * (p[0] // patch) * (p[1] // patch)
+                                            for p in run.planned])])
+        res = []
+        for j, ref in zip(jobs, refs):
+            r0 = int(cu[b]) + j[3] * per_t
+            t = run.out[r0:r0 + per_t]
+            if run.code == vp.VP_OUT_BF16:
+                res.append(compare.check_bf16(t.view(torch.int16).cpu().numpy().view(np.uint16), ref))
+            else:
+                res.append(compare.check_f32(t.cpu().numpy(), ref))
+        return compare.merge(res)
+
     frames_count = pairs = items = 0
     spent = 0.0
-    with cf.ThreadPoolExecutor(max_workers=cores) as ex:
-        for b in range(len(frames_dev)):
-            h, w, idx = planned[b]
-            padded = list(idx) + ([idx[-1]] if len(idx) % 2 else [])
-            host = frames_dev[b].cpu().numpy()
-            jobs = [(np.ascontiguousarray(host[[padded[2 * tt], padded[2 * tt + 1]]]), h, w)
-                    for tt in range(len(padded) // 2)]
-            del host
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        for b in range(len(run.frames)):
+            jobs = jobs_of(b)
             t0 = time.perf_counter()
-            if resize_only:
-                list(ex.map(lambda j: oracle.resize_u8_item(j[0], [0, 1], j[1], j[2]), jobs))
-            elif patch_only:
-                list(ex.map(lambda j: oracle.patchify_item(j[0], [0, 1], wl.mean, wl.std), jobs))
-            else:
-                list(ex.map(lambda j: oracle.preprocess_item(j[0], [0, 1], j[1], j[2], wl.mean,
-                                                             wl.std, patch=wl.items[0].patch), jobs))
+            refs = list(ex.map(oracle_call, jobs))
             spent += time.perf_counter() - t0
-            frames_count += len(idx)
+            r = check(b, jobs, refs)
+            if r is not None:
+                results.append(r)
+            frames_count += len(run.planned[b][2])
             pairs += len(jobs)
             items += 1
             if spent >= budget_s:
                 break
-    return dict(value=round(frames_count / spent, 1), unit="frames/s", cores=cores, kind="oracle",
-                sample=f"first {items} of {len(frames_dev)} items of the same workload "
-                       f"({frames_count} sampled frames, {pairs} frame pairs), fp64 C oracle, "
-                       f"{spent:.1f} s of oracle wall time on {cores} threads")
+    # one thread: oracle calls on the first item, until single_s seconds
+    jobs = jobs_of(0)
+    per_job = len(run.planned[0][2]) / len(jobs)   # sampled frames per oracle call
+    done, one_spent = 0, 0.0
+    for j in jobs:
+        t0 = time.perf_counter()
+        oracle_call(j)
+        one_spent += time.perf_counter() - t0
+        done += 1
+        if one_spent >= single_s:
+            break
+    one_frames = done * per_job
+    parity = compare.merge(results) if results else None
+    return dict(value=round(frames_count / spent, 1), unit="frames/s", cores=threads, kind="oracle",
+                sample=f"first {items} of {len(run.frames)} items of the same workload "
+                       f"({frames_count} sampled frames, {pairs} oracle calls), fp64 C oracle, "
+                       f"{spent:.1f} s of oracle wall time on {threads} threads",
+                single_thread=dict(value=round(one_frames / one_spent, 1), unit="frames/s",
+                                   sample=f"{one_frames:.0f} sampled frames of item 0, "
+                                          f"{one_spent:.1f} s on one thread"),
+                cpu_model=cpu_model(), host_cpus=os.cpu_count(),
+                threads_note=f"threads = min({CPU_SHARE}, host CPUs): the CPU share of one GPU on a "
+                             f"shared 8-GPU host",
+                parity_of_sample=parity)
 
 
 def main():
@@ -108,7 +290,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", type=int, default=4, choices=range(5),
-                    help="workload configuration (4 = 64x256 frames 720x1280, the default)")
+                    help="headline workload configuration (4 = 64x256 frames 720x1280, the default)")
     ap.add_argument("--patchify", action="store_true",
                     help="time the normalise+patchify-only entry on the cached counterpart of "
                          "workload 4 (64 x 256 frames already at 256x448) instead")
@@ -119,6 +301,10 @@ def main():
     ap.add_argument("--patch", type=int, default=16, choices=(14, 16),
                     help="14: the Qwen2/2.5-VL geometry on workload 4's frames (252x448, rows of 1176)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="skip the other workloads' figures")
+    ap.add_argument("--config-steps", type=int, default=30,
+                    help="timed calls per other workload (after 20 warm-up calls)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run plain 1 GiB device-to-device copies (twice) before the steps, "
                          "to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -143,60 +329,22 @@ def main():
     log(f"device {props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count} "
         f"mem={props.total_memory / 2**30:.0f} GiB")
 
+    special = args.patchify or args.resize or args.positions or args.patch == 14
     if args.patch == 14:
         wl = workloads.patch14_config()
     else:
         wl = workloads.patchify_config() if args.patchify else workloads.config(args.workload)
-    entry = vp.vp_patchify_batch if args.patchify else vp.vp_preprocess_batch
+    mode = "patchify" if args.patchify else ("resize" if args.resize else
+                                              ("positions" if args.positions else "preprocess"))
     log(f"workload {wl.name}")
     t0 = time.perf_counter()
-    frames = [workloads.frames_torch(it, dev, chunk=32) for it in wl.items]
+    run = Run(vp, workloads, torch, wl, dev, mode)
     torch.cuda.synchronize()
     log(f"input generated in {time.perf_counter() - t0:.1f} s "
-        f"({sum(f.numel() for f in frames) / 1e9:.2f} GB)")
-
-    def plan_items():
-        vitems, planned = [], []
-        for it, fr in zip(wl.items, frames):
-            if it.dims is not None:
-                h, w = it.dims
-            else:
-                h, w = vp.vp_smart_resize_dims(it.H, it.W, 2 * it.patch, it.min_pixels, it.max_pixels)
-            s = it.sample
-            if s["mode"] == "uniform":
-                idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_UNIFORM, s["n"])
-            else:
-                idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_FPS, 0, s["video_fps"], s["fps"],
-                                           s["min_frames"], s["max_frames"])
-            vitems.append(vp.Item(fr, idx, h, w, it.patch))
-            planned.append((h, w, idx))
-        return vitems, planned
-
-    vitems, planned = plan_items()
-    code = vp.VP_OUT_BF16 if wl.out_dtype == "bf16" else vp.VP_OUT_F32
-    if args.resize:
-        frame_off, ws_bytes = vp.vp_resize_layout(vitems)
-        rows = 0
-        out = torch.empty(int(frame_off[-1]), dtype=torch.uint8, device=dev)
-    elif args.positions:
-        grid, cu, rows, ws_bytes = vp.vp_batch_layout(vitems)
-        out = torch.empty((rows, 3), dtype=torch.int32, device=dev)
-        out_llm = torch.empty((rows // 4, 3), dtype=torch.int32, device=dev)
-    else:
-        grid, cu, rows, ws_bytes = vp.vp_batch_layout(vitems)
-        out = torch.empty((rows, vp.row_width(wl.items[0].patch)),
-                          dtype=torch.bfloat16 if code == vp.VP_OUT_BF16 else torch.float32, device=dev)
-    work = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        f"({sum(f.numel() for f in run.frames) / 1e9:.2f} GB)")
+    log(f"{run.n_frames} frames, {run.rows} rows, algorithmic bytes {run.alg_bytes / 1e9:.3f} GB "
+        f"(in {run.in_bytes / 1e9:.3f}, out {run.out_bytes / 1e9:.3f})")
     stream = torch.cuda.current_stream(dev)
-    n_frames = sum(len(p[2]) for p in planned)
-    in_bytes = sum(len(p[2]) * it.frame_bytes for p, it in zip(planned, wl.items))
-    out_bytes = out.numel() * out.element_size()
-    if args.positions:   # no frame is read; both tables are written
-        in_bytes = 0
-        out_bytes += out_llm.numel() * out_llm.element_size()
-    alg_bytes = in_bytes + out_bytes
-    log(f"{n_frames} frames, {rows} rows, algorithmic bytes {alg_bytes / 1e9:.3f} GB "
-        f"(in {in_bytes / 1e9:.3f}, out {out_bytes / 1e9:.3f})")
 
     if args.copy_probe:
         src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
@@ -208,62 +356,83 @@ def main():
         log("copy probe: 2 x (1 GiB copy_ + 1 GiB bitwise_not), each reads and writes 2^30 bytes")
         del src, dst
 
-    def step():
-        items, _ = plan_items()
-        if args.resize:
-            vp.vp_resize_batch(items, out, work, stream)
-        elif args.positions:
-            vp.vp_position_ids(items, out, out_llm, work, stream)
-        else:
-            entry(items, wl.mean, wl.std, code, out, work, stream)
+    copy_gbps, copy_ms = copy_ceiling(torch, dev)
+    log(f"copy ceiling: {copy_gbps:,.0f} GB/s ({copy_gbps / HBM_PEAK_GBPS:.1%} of 8 TB/s; "
+        f"4 GiB copy in {copy_ms:.3f} ms)")
 
+    # Python's cyclic garbage collector pauses the host for 30-55 ms on this
+    # heap (torch, numpy, ctypes objects) at unpredictable steps, and the GPU
+    # idles meanwhile: collect now and keep it off while steps are timed,
+    # as the standard library's timeit does.
+    gc.collect()
+    gc.disable()
     for _ in range(args.warmup):
-        step()
+        run.step(stream)
     torch.cuda.synchronize()
     log(f"warm-up done ({args.warmup} steps)")
-
-    # Per timed step: events around the whole call (plan + upload + kernels)
-    # and, recorded by the library itself, around its kernels alone.
-    def pair():
-        return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-    call_evs = [pair() for _ in range(args.steps)]
-    kern_evs = [pair() for _ in range(args.steps)]
-    for a, b in kern_evs:          # HIP events exist once recorded
-        a.record(stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        call_evs[k][0].record(stream)
-        vp.vp_set_kernel_events(*kern_evs[k])
-        step()
-        call_evs[k][1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    call_ms = [a.elapsed_time(b) for a, b in call_evs]
-    kern_ms = [a.elapsed_time(b) for a, b in kern_evs]
+    wall, kern_ms, call_ms, pre_ms, host_ms = run.timed(stream, args.steps)
+    gc.enable()
     mean_kern_ms = sum(kern_ms) / len(kern_ms)
     ms_per_step = wall * 1e3 / args.steps
-    value = n_frames * args.steps / wall
-    achieved = alg_bytes / (mean_kern_ms * 1e-3) / 1e9
+    value = run.n_frames * args.steps / wall
+    achieved = run.alg_bytes / (mean_kern_ms * 1e-3) / 1e9
     log(f"{ms_per_step:.3f} ms/step wall; call {sum(call_ms) / len(call_ms):.3f} ms mean; "
         f"kernels {mean_kern_ms:.3f} ms mean (min {min(kern_ms):.3f}, max {max(kern_ms):.3f}); "
         f"{value:,.0f} frames/s; {achieved:,.0f} GB/s algorithmic "
         f"({achieved / HBM_PEAK_GBPS:.1%} of 8 TB/s)")
     log("kernel ms per step: " + " ".join(f"{t:.3f}" for t in kern_ms))
+    log("call ms per step:   " + " ".join(f"{t:.3f}" for t in call_ms))
+    log("call start to first kernel, ms: " + " ".join(f"{t:.3f}" for t in pre_ms))
+    log("host ms per step:   " + " ".join(f"{t:.3f}" for t in host_ms))
 
-    tag = "q4" if args.patch == 14 else (
-        "p4" if args.patchify else (f"r{args.workload}" if args.resize else
-                                    (f"i{args.workload}" if args.positions else f"c{args.workload}")))
+    if args.patch == 14:
+        tag = "q4"
+    elif args.patchify:
+        tag = "p4"
+    elif args.resize:
+        tag = f"r{args.workload}"
+    elif args.positions:
+        tag = f"i{args.workload}"
+    else:
+        tag = f"c{args.workload}"
     sha = kernel_source_sha()
     traffic = counter_traffic(tag, sha)
 
     baseline = None
     if not args.no_cpu_baseline and not args.positions:
         log("timing the CPU oracle on a bounded sample")
-        baseline = cpu_baseline(wl, frames, planned, patch_only=args.patchify, resize_only=args.resize)
+        baseline = cpu_baseline(run, patch_only=args.patchify, resize_only=args.resize)
         log(f"cpu baseline {baseline}")
+
+    per_config = None
+    if not special and not args.no_per_config:
+        per_config = {}
+        for k in range(5):
+            if k == args.workload:
+                continue
+            wk = workloads.config(k)
+            r = Run(vp, workloads, torch, wk, dev)
+            gc.collect()
+            gc.disable()
+            for _ in range(20):
+                r.step(stream)
+            w_s, kms, cms, _, _ = r.timed(stream, args.config_steps)
+            gc.enable()
+            mk = sum(kms) / len(kms)
+            gbps = r.alg_bytes / (mk * 1e-3) / 1e9
+            per_config[f"c{k}"] = dict(
+                workload=wk.name, frames=r.n_frames, rows=r.rows, out_dtype=wk.out_dtype,
+                algorithmic_bytes=r.alg_bytes, kernel_ms=round(mk, 4),
+                kernel_ms_median=round(sorted(kms)[len(kms) // 2], 4),
+                frames_per_s=round(r.n_frames / (mk * 1e-3), 1),
+                frames_per_s_wall=round(r.n_frames * args.config_steps / w_s, 1),
+                achieved_gbps=round(gbps, 1), frac=round(gbps / HBM_PEAK_GBPS, 4),
+                traffic=counter_traffic(f"c{k}", sha), steps=args.config_steps)
+            log(f"c{k}: kernels {mk:.4f} ms mean, {gbps:,.0f} GB/s ({gbps / HBM_PEAK_GBPS:.1%}), "
+                f"{r.n_frames / (mk * 1e-3):,.0f} frames/s")
+            del r
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
 
     rec = {
         "metric": "preprocessed frames/s and achieved HBM GB/s (% of MI355X peak) per config",
@@ -276,18 +445,19 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
+        # the arithmetic type of the path: fp32 sums (bf16 is only the output format)
         "dtype": "i32" if (args.resize or args.positions) else "f32",
         "data": "synthetic (seeded SplitMix64 frames resident in HBM)",
         "config": {
             "workload": wl.name + ("; uint8 cache writer (fixed-point resize only)" if args.resize else
                                    "; position tables only" if args.positions else ""),
             "items": len(wl.items),
-            "frames": n_frames,
-            "rows": rows,
+            "frames": run.n_frames,
+            "rows": run.rows,
             "out_dtype": "u8" if args.resize else ("i32" if args.positions else wl.out_dtype),
             "mean": list(wl.mean),
             "std": list(wl.std),
-            "algorithmic_bytes": alg_bytes,
+            "algorithmic_bytes": run.alg_bytes,
             "kernel_sha": sha,
         },
         "roofline": {
@@ -298,7 +468,14 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
             "kernel_ms": round(mean_kern_ms, 4),
+            "kernel_ms_median": round(sorted(kern_ms)[len(kern_ms) // 2], 4),
         },
+        "ceiling": {
+            "kind": "device-to-device copy (torch copy_, 4 GiB, best of 12)",
+            "gbps": round(copy_gbps, 1),
+            "frac": round(copy_gbps / HBM_PEAK_GBPS, 4),
+        },
+        "per_config": per_config,
         "cpu_baseline": baseline,
     }
     print(json.dumps(rec), flush=True)

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <algorithm>
+#include <list>
 #include <map>
 #include <memory>
 #include <tuple>
@@ -1157,6 +1158,74 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
 }
 
 // ---------------------------------------------------------------------------
+// Plan cache.  An RL loop or a serving loop hands the library the same batch
+// (the same frame buffers, sizes and index lists) call after call; its plan
+// is a pure function of those, so the last few plans are kept and reused
+// when every field and every index matches.  Entries are immutable and
+// shared by pointer; a cache holds kPlanCacheMax plans, the most recently
+// used first.
+// ---------------------------------------------------------------------------
+
+enum class PlanKind : int64_t { kBatch = 1, kPatch = 2, kResize = 3, kRows = 4 };
+
+constexpr size_t kPlanCacheMax = 8;
+std::mutex g_plan_mu;
+std::list<std::pair<std::vector<int64_t>, std::shared_ptr<const Plan>>> g_plans;
+
+int32_t build_kind(PlanKind kind, const vp_item* items, int32_t n, Plan* p) {
+    switch (kind) {
+        case PlanKind::kBatch: return build_plan(items, n, p);
+        case PlanKind::kPatch: return build_patch_plan(items, n, p);
+        case PlanKind::kResize: return build_resize_plan(items, n, p);
+        case PlanKind::kRows: return build_rows_plan(items, n, p);
+    }
+    return fail(VP_ERR_ARG, "unknown plan kind");
+}
+
+// The plan of `items` for `kind`: from the cache if an identical batch was
+// planned recently, else built (and cached if valid).  Errors are those of
+// the builder; nothing invalid is cached.
+int32_t get_plan(PlanKind kind, const vp_item* items, int32_t n, std::shared_ptr<const Plan>* out) {
+    bool cacheable = items != nullptr && n >= 1;
+    for (int32_t b = 0; cacheable && b < n; ++b)
+        cacheable = items[b].indices != nullptr && items[b].n_idx >= 1;
+    if (!cacheable) {   // the builder reports the error
+        Plan p;
+        const int32_t st = build_kind(kind, items, n, &p);
+        if (st == VP_OK) *out = std::make_shared<const Plan>(std::move(p));
+        return st;
+    }
+    std::vector<int64_t> key;
+    key.reserve(2 + size_t(n) * 8);
+    key.push_back(static_cast<int64_t>(kind));
+    key.push_back(n);
+    for (int32_t b = 0; b < n; ++b) {
+        const vp_item& it = items[b];
+        key.insert(key.end(), {static_cast<int64_t>(reinterpret_cast<uintptr_t>(it.frames)), it.n_src,
+                               it.src_h, it.src_w, it.n_idx, it.dst_h, it.dst_w, it.patch});
+        key.insert(key.end(), it.indices, it.indices + it.n_idx);
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_plan_mu);
+        for (auto e = g_plans.begin(); e != g_plans.end(); ++e)
+            if (e->first == key) {
+                g_plans.splice(g_plans.begin(), g_plans, e);   // most recent first
+                *out = e->second;
+                return VP_OK;
+            }
+    }
+    Plan p;
+    const int32_t st = build_kind(kind, items, n, &p);
+    if (st != VP_OK) return st;
+    auto plan = std::make_shared<const Plan>(std::move(p));
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    g_plans.emplace_front(std::move(key), plan);
+    if (g_plans.size() > kPlanCacheMax) g_plans.pop_back();
+    *out = std::move(plan);
+    return VP_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Pinned staging ring: the plan blob is written into pinned host memory and
 // copied asynchronously; a slot is reused only after the copy that read it
 // has completed.
@@ -1395,9 +1464,10 @@ int32_t run_batch(bool patch_only, const vp_item* items, int32_t n_items, const 
         norm.b[c] = static_cast<float>(-static_cast<double>(mean[c]) / static_cast<double>(std[c]));
         norm.z[c] = static_cast<float>(-255.0 * static_cast<double>(mean[c]));
     }
-    Plan p;
-    int32_t st = patch_only ? build_patch_plan(items, n_items, &p) : build_plan(items, n_items, &p);
+    std::shared_ptr<const Plan> plan;
+    int32_t st = get_plan(patch_only ? PlanKind::kPatch : PlanKind::kBatch, items, n_items, &plan);
     if (st != VP_OK) return st;
+    const Plan& p = *plan;
     if (out_rows_capacity < p.total_rows)
         return fail(VP_ERR_CAPACITY, "out_rows holds " + std::to_string(out_rows_capacity) +
                                          " rows, batch needs " + std::to_string(p.total_rows));
@@ -1567,9 +1637,10 @@ int32_t vp_filter_table_fixed(int32_t n_in, int32_t n_out, int32_t taps, int32_t
 
 int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw,
                         int32_t* cu_seqlens, int64_t* total_rows, int64_t* workspace_bytes) {
-    Plan p;
-    const int32_t st = build_plan(items, n_items, &p);
+    std::shared_ptr<const Plan> plan;
+    const int32_t st = get_plan(PlanKind::kBatch, items, n_items, &plan);
     if (st != VP_OK) return st;
+    const Plan& p = *plan;
     if (grid_thw) std::memcpy(grid_thw, p.grid.data(), sizeof(int32_t) * p.grid.size());
     if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
     if (total_rows) *total_rows = p.total_rows;
@@ -1602,9 +1673,10 @@ int32_t vp_patchify_batch(const vp_item* items, int32_t n_items, const float* me
 }
 int32_t vp_resize_layout(const vp_item* items, int32_t n_items, int64_t* frame_off,
                          int64_t* workspace_bytes) {
-    Plan p;
-    const int32_t st = build_resize_plan(items, n_items, &p);
+    std::shared_ptr<const Plan> plan;
+    const int32_t st = get_plan(PlanKind::kResize, items, n_items, &plan);
     if (st != VP_OK) return st;
+    const Plan& p = *plan;
     if (frame_off) std::memcpy(frame_off, p.byte_off.data(), sizeof(int64_t) * p.byte_off.size());
     if (workspace_bytes) *workspace_bytes = static_cast<int64_t>(p.bytes);
     g_last_error.clear();
@@ -1620,9 +1692,10 @@ int32_t vp_resize_batch(const vp_item* items, int32_t n_items, void* out_frames,
         return fail(VP_ERR_ARG, "out_frames must be 4-byte aligned");
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
         return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
-    Plan p;
-    int32_t st = build_resize_plan(items, n_items, &p);
+    std::shared_ptr<const Plan> plan;
+    int32_t st = get_plan(PlanKind::kResize, items, n_items, &plan);
     if (st != VP_OK) return st;
+    const Plan& p = *plan;
     if (out_capacity < p.byte_off[n_items])
         return fail(VP_ERR_CAPACITY, "out_frames holds " + std::to_string(out_capacity) +
                                          " bytes, batch needs " + std::to_string(p.byte_off[n_items]));
@@ -1667,9 +1740,10 @@ int32_t vp_position_ids(const vp_item* items, int32_t n_items, int32_t* vit_pos,
         return fail(VP_ERR_ARG, "workspace must be 256-byte aligned");
     if (reinterpret_cast<uintptr_t>(vit_pos) % 4 != 0 || reinterpret_cast<uintptr_t>(llm_pos) % 4 != 0)
         return fail(VP_ERR_ARG, "vit_pos and llm_pos must be 4-byte aligned");
-    Plan p;
-    int32_t st = build_rows_plan(items, n_items, &p);
+    std::shared_ptr<const Plan> plan;
+    int32_t st = get_plan(PlanKind::kRows, items, n_items, &plan);
     if (st != VP_OK) return st;
+    const Plan& p = *plan;
     if ((vit_pos != nullptr || llm_pos != nullptr) && rows_capacity < p.total_rows)
         return fail(VP_ERR_CAPACITY, "position tables hold " + std::to_string(rows_capacity) +
                                          " rows, batch needs " + std::to_string(p.total_rows));

@@ -143,6 +143,35 @@ def test_batch_layout_random_ragged_vs_oracle():
         assert grid.tolist() == og.tolist() and cu.tolist() == ocu.tolist() and rows == ocu[-1]
 
 
+def test_plan_cache_follows_every_field_and_index():
+    """The library reuses the plan of an identical batch; any change of a
+    field or an index (same frame buffer, same index array object mutated in
+    place) must give that batch's own layout, including after eviction of
+    older plans (more distinct batches than the cache holds)."""
+    frames = (0x10000, 300, 720, 1280)
+    idx = np.arange(0, 300, 2, dtype=np.int32)[:150]
+    items = [vp.Item(frames, idx, 256, 448)]
+    g1, cu1, r1, ws1 = vp.vp_batch_layout(items)
+    idx[-1] = 299                          # same array, new content: same layout, new plan
+    g2, cu2, r2, ws2 = vp.vp_batch_layout(items)
+    assert (g1.tolist(), r1) == (g2.tolist(), r2)
+    for k in range(12):                    # more distinct batches than the cache keeps
+        n = 2 + 2 * k
+        it = [vp.Item(frames, np.arange(n, dtype=np.int32), 256 - 32 * (k % 3), 448), items[0]]
+        g, cu, rows, ws = vp.vp_batch_layout(it)
+        og, ocu = oracle.layout([n, len(idx)], [256 - 32 * (k % 3), 256], [448, 448])
+        assert g.tolist() == og.tolist() and cu.tolist() == ocu.tolist() and rows == ocu[-1]
+    odd = [vp.Item(frames, idx[:149], 256, 448)]   # one index fewer: t = 75 either way
+    g3, cu3, r3, _ = vp.vp_batch_layout(odd)
+    assert g3.tolist() == [[75, 16, 28]] and r3 == r1
+    # a bad index in a batch whose good twin was planned before is still reported
+    bad = idx.copy()
+    bad[5] = 300
+    with pytest.raises(vp.VPError) as e:
+        vp.vp_batch_layout([vp.Item(frames, bad, 256, 448)])
+    assert e.value.status == vp.VP_ERR_INDEX
+
+
 def test_layout_errors():
     ok = vp.Item((0x10000, 4, 100, 100), [0, 3], 64, 64)
     cases = [
