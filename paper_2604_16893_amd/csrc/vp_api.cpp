@@ -473,6 +473,34 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t pa
     return best >= 0;
 }
 
+// The x-first streaming kernel (patch 16) for an item, if it can take it:
+// bands of 64 output columns (the last one narrower where the width is not a
+// multiple of 64), an even tap count from 4 to 12 (the window's taps rounded
+// up), M slots.
+// Its shape is recorded with px = kPxXFirst.
+bool xfirst_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
+    const int32_t kx = round_up(std::max<int32_t>(fx.taps, 4), 2);
+    if (!vp::xfirst_shape_supported(m, kx)) return false;
+    // every load of a frame row (a window of up to 3 kx + 4 bytes past its
+    // start, up to kSlotMax + 8 rows past the last one) stays below 4 GiB
+    if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 3 * kx + 64 >= (int64_t(1) << 32)) return false;
+    const int32_t band = 64;
+    const int32_t waves = (it.dst_w + band - 1) / band;
+    if (waves > vp::kWgBandMax) return false;
+    sh->m = m;
+    sh->kx = kx;
+    sh->px = vp::kPxXFirst;
+    sh->band = band;
+    sh->bands = waves;
+    return true;
+}
+
+// Vertical scales up to this one (source rows per output row) take the
+// x-first kernel where it fits: an output row closes on almost every source
+// row there, and the y-first kernel's gathers of each closed row from LDS
+// bound it.
+constexpr double kXFirstMaxScale = 1.6;
+
 // Process-wide cache of per-axis tables.  The same axes recur from call to
 // call (an RL loop preprocesses batches of the same shapes every step), and
 // building them is most of the host's work for a batch of many shapes.
@@ -540,12 +568,17 @@ struct Keyed {
 // Output rows per streaming unit of an item: at most about max_src_rows
 // source rows, at least ten windows of source rows, a multiple of `group`
 // rows (the kernel's store group), and at least 16 rows (28 for groups of 14).
+// A frame's rows are then cut into that many units of nearly equal length:
+// units of one frame are neighbours in the workgroup list, and a long unit
+// followed by a short remainder would load the XCDs unevenly.
 int64_t unit_row_band(const vp::DevItem& d, int64_t max_src_rows, int64_t group) {
     int64_t band = max_src_rows * d.h / d.H;
     const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
     band = std::max(band, min_band);
     band = std::max<int64_t>((band + group - 1) / group * group, group == 4 ? 16 : 2 * group);
-    return std::min<int64_t>(band, d.h);   // h is a multiple of 2P: every band ends on a whole group
+    if (band >= d.h) return d.h;   // h is a multiple of 2P: every band ends on a whole group
+    const int64_t n = (d.h + band - 1) / band;
+    return ((d.h + n - 1) / n + group - 1) / group * group;   // at most band, more than band (n - 1) / n
 }
 
 // Lays out the streaming units as launches and their workgroup lists.
@@ -558,7 +591,10 @@ int32_t assemble_launches(const std::vector<Keyed>& keyed, int32_t P, Plan* p) {
     // that all bands of one unit run on one XCD and share the source pixels
     // of neighbouring bands through its L2; a unit with fewer bands than the
     // others of its eight leaves empty entries.  Units are sorted by band
-    // count first, which keeps those rare.
+    // count first, which keeps those rare.  The XCD of the x-th unit of the
+    // g-th eight is (x + g) mod 8: a pattern in the units' lengths that
+    // repeats every few units (the units of one frame) then spreads over all
+    // eight XCDs instead of loading some more than others.
     if (keyed.size() > vp::kWgUnitMask + 1)
         return fail(VP_ERR_CAPACITY, "batch has more than 2^20 streaming work units");
     // order: by shape, then band count, then as generated (a grouping: the
@@ -588,7 +624,7 @@ int32_t assemble_launches(const std::vector<Keyed>& keyed, int32_t P, Plan* p) {
         L.kx = std::get<1>(key0);
         L.px = std::get<2>(key0);
         L.patch = P;
-        for (size_t c0 = k0; c0 < k1; c0 += 8) {
+        for (size_t c0 = k0, g = 0; c0 < k1; c0 += 8, ++g) {
             const size_t c1 = std::min(c0 + 8, k1);
             int32_t rounds = 0;
             for (size_t k = c0; k < c1; ++k) rounds = std::max(rounds, keyed[order[k]].bands);
@@ -599,7 +635,8 @@ int32_t assemble_launches(const std::vector<Keyed>& keyed, int32_t P, Plan* p) {
                 L.cost += e.cost * e.bands;
             }
             for (int32_t r = 0; r < rounds; ++r)
-                for (size_t x = 0; x < 8; ++x) {
+                for (size_t col = 0; col < 8; ++col) {
+                    const size_t x = (col + 8 - g % 8) % 8;   // the unit on XCD col
                     const size_t k = c0 + x;
                     p->wgs.push_back(k < c1 && r < keyed[order[k]].bands
                                          ? (u0 + static_cast<uint32_t>(x)) | (static_cast<uint32_t>(r) << vp::kWgBandShift)
@@ -707,10 +744,12 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         d.route = vp::kRouteGeneric;
         int32_t m = 0;
         StreamShape sh;
-        if (slots_for(*fy, &d.sy_off, &m) && stream_shape(it, *fx, m, P, &sh)) {
+        const bool slots = slots_for(*fy, &d.sy_off, &m);
+        const bool near_one = P == 16 && double(it.src_h) <= kXFirstMaxScale * double(it.dst_h);
+        if (slots && ((near_one && xfirst_shape(it, *fx, m, &sh)) || stream_shape(it, *fx, m, P, &sh))) {
             d.route = vp::kRouteStream;
             d.band = sh.band;
-            d.row_px = 64 * sh.px;
+            d.row_px = sh.px > 0 ? 64 * sh.px : it.src_w + sh.kx;
             d.sx_off = columns_for(*fx, sh.kx, sh.band, d.row_px);
             shapes[b] = sh;
         } else if (!generic_subtile(*fx, 2 * P, &d.rh, &d.cw)) {

@@ -1008,6 +1008,300 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 
 
 // ===========================================================================
+// x-first streaming kernel (patch 16): vertical scales near 1
+// ===========================================================================
+//
+// The streaming kernel above resamples y first and gathers each closed
+// output row's x windows from LDS, 16 bytes per tap and lane.  Where the
+// vertical scale is near 1 -- upscales, and downscales up to about 1.6x --
+// an output row closes on almost every source row, and those gathers bound
+// the kernel.  This one resamples x first and keeps LDS for the stage only:
+//   * lane j (output column j0 + j) loads its own window of each source row
+//     straight from the frame: the dwords holding its 3 KXE bytes (ND of
+//     them, dword aligned, four rows ahead); neighbouring lanes' windows
+//     overlap, and the overlap is served by the L1 cache, not HBM;
+//   * the lane shifts the window to its first byte (v_alignbyte by the
+//     window's byte misalignment) and moves the bytes of taps 2m and 2m + 1
+//     of each channel into the two 16-bit halves of a register with zero high
+//     bytes (one v_perm with a fixed selector): byte value b reads as the f16
+//     denormal b * 2^-24, as in the y-first kernel, so the x sums are
+//     mixed-precision FMAs with no conversion (exact products);
+//   * the three channel sums go into M rotating accumulator slots with the
+//     slot table's wave-uniform weights, which carry the factor 2^24; a slot
+//     starts at z_c = -255 mean_c, so a closed slot holds R + z_c;
+//   * a closing output row is multiplied by a_c = 1/(255 std_c), converted
+//     and staged; every four rows the stage leaves as 16-byte stores, eight
+//     lanes per 128-byte run, as in the y-first kernel.
+// Window bytes past the end of a row are the next row's (or zeros past the
+// frame, from the buffer range check); they meet only zero weights.
+template <int M, int KXE, int OUT_BF16>
+__global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void* out, Norm norm) {
+    using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
+    static_assert(KXE % 2 == 0 && KXE >= 4 && KXE <= 12, "even tap counts from 4 to 12");
+    constexpr int NA = (3 * KXE + 3) / 4;          // dwords of the window from its first byte
+    constexpr int ND = NA + 1;                     // dwords loaded: the window at any alignment
+    constexpr int S = 16 / int(sizeof(elem_t));    // output columns per 16-byte store
+    extern __shared__ __align__(16) unsigned char smem[];
+    elem_t* const stage = reinterpret_cast<elem_t*>(smem);   // [3][4][64]
+
+    const int lane = static_cast<int>(threadIdx.x) & 63;
+    const uint32_t wg = as_const(plan.wgs)[wg0 + static_cast<int>(blockIdx.x)];
+    if (wg == kNoWork) return;
+    const int u = static_cast<int>(wg & kWgUnitMask);
+    const int wave = static_cast<int>(wg >> kWgBandShift);
+    const cptr<StreamUnit> up = as_const(plan.units) + u;
+    const int u_item = up->item, u_pf = up->p_flags, i0 = up->i0, i1 = up->i1;
+    const int u_p = u_pf & (kUnitBoth - 1);
+    const cptr<DevItem> it = as_const(plan.items) + u_item;
+    const int w = it->w;
+    const int band = it->band;
+    const int j0 = wave * band;                    // first output column of this wave
+    const int nbw = min(band, w - j0);             // its columns
+    const int tt = u_p >> 1;
+    const int dt_self = u_p & 1;
+    int64_t it_row_off = it->row_off;
+    int it_hm = it->hm, it_wm = it->wm;
+    asm volatile("" : "+s"(it_row_off), "+s"(it_hm), "+s"(it_wm));
+    const bool both = (u_pf & kUnitBoth) != 0;
+
+    // Column table: window start relative to the band's first source pixel,
+    // then KXE weights (zero past the window).  Lanes past the band's last
+    // column take its first column's entry (valid reads) with zero weights.
+    const cptr<int32_t> tables = as_const(plan.tables);
+    const cptr<int32_t> sx_start = tables + it->sx_off;
+    const cptr<float> sx_w = (cptr<float>)(sx_start + w);
+    const bool xlane = lane < nbw;
+    const int jx = xlane ? j0 + lane : j0;
+    const int sj = sx_start[jx];
+    float wx[KXE];
+    {
+        const cptr<float> src = sx_w + int64_t(jx) * KXE;
+#pragma unroll
+        for (int k = 0; k < KXE; ++k) wx[k] = xlane ? src[k] : 0.f;
+    }
+    const cptr<int32_t> xs = tables + it->tx_off;
+    const int x0 = xs[j0];                         // first source pixel of the band
+    const cptr<int32_t> ys = tables + it->ty_off;
+    const cptr<float> slot_w = (cptr<float>)(tables + it->sy_off);
+    const cptr<int32_t> close_row = tables + it->sy_off + (it->H + kSlotMax) * kSlotWords;
+
+    // Source frame through buffer resources, as in the y-first kernel: row
+    // blocks of four start at a multiple of 4 rows, so each block's offset
+    // (a multiple of 4 bytes) goes into its resource, and the lane's window
+    // in row phase k sits at the fixed dword offset voff[k], byte sh[k].
+    const int f = as_const(plan.indices)[it->idx_off + u_p];
+    const uintptr_t fa = reinterpret_cast<uintptr_t>(it->frames + int64_t(f) * it->frame_bytes);
+    const uint32_t lead = static_cast<uint32_t>(fa & 3u);
+    const uint32_t range = static_cast<uint32_t>((it->frame_bytes + lead + 3) & ~int64_t(3));
+    const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
+    uint32_t voff[kPrefetch], sh[kPrefetch];
+#pragma unroll
+    for (int k = 0; k < kPrefetch; ++k) {
+        const uint32_t c = lead + static_cast<uint32_t>(k) * row_bytes + 3u * static_cast<uint32_t>(x0 + sj);
+        voff[k] = c & ~3u;
+        sh[k] = c & 3u;
+    }
+    struct Win {
+        uint32_t d[ND];
+    };
+    auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> Win {
+        const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
+        const uint32_t n = __builtin_amdgcn_readfirstlane(range > o ? range - o : 0u);
+        const uintptr_t bp = fa - lead + o;
+        const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
+        const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
+        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+            reinterpret_cast<void*>((uintptr_t(b_hi) << 32) | b_lo), (short)0, static_cast<int>(n), 0x00020000);
+        Win r;
+#pragma unroll
+        for (int i = 0; i < ND; i += 4) {
+            const uint32_t vo = voff[k] + 4u * static_cast<uint32_t>(i);
+            if (ND - i >= 4) {
+                const auto v = __builtin_amdgcn_raw_buffer_load_b128(rb, vo, 0, 0);
+                r.d[i] = v[0];
+                r.d[i + 1] = v[1];
+                r.d[i + 2] = v[2];
+                r.d[i + 3] = v[3];
+            } else if (ND - i == 3) {
+                const auto v = __builtin_amdgcn_raw_buffer_load_b96(rb, vo, 0, 0);
+                r.d[i] = v[0];
+                r.d[i + 1] = v[1];
+                r.d[i + 2] = v[2];
+            } else if (ND - i == 2) {
+                const auto v = __builtin_amdgcn_raw_buffer_load_b64(rb, vo, 0, 0);
+                r.d[i] = v[0];
+                r.d[i + 1] = v[1];
+            } else {
+                r.d[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, vo, 0, 0);
+            }
+        }
+        return r;
+    };
+
+    const float a0 = norm.a[0], a1 = norm.a[1], a2 = norm.a[2];
+    const float z0 = norm.z[0], z1 = norm.z[1], z2 = norm.z[2];
+    float acc[M][3];
+#pragma unroll
+    for (int s = 0; s < M; ++s) {
+        acc[s][0] = z0;
+        acc[s][1] = z1;
+        acc[s][2] = z2;
+    }
+
+    const int y0 = ys[i0];
+    const int y1 = close_row[i1 - 1] + 1;
+    int base = i0;
+    while (base > 0 && close_row[base - 1] >= y0) --base;
+    int slot = base % M;
+    int next_close = close_row[base];
+    int after_close = close_row[base + 1];
+
+    // store-out pieces, as in the y-first kernel (patch 16)
+    constexpr int kPieces = 16 / S;
+    constexpr int kPerPatch = 3 * 4 * kPieces;
+    constexpr int kStoreIter = (4 * kPerPatch + 63) / 64;
+    int st_off[kStoreIter], dst_off[kStoreIter];
+    {
+        const int n_seg = (nbw >> 4) * kPerPatch;
+#pragma unroll
+        for (int r = 0; r < kStoreIter; ++r) {
+            const int e = lane + 64 * r;
+            const int q = e / kPerPatch;
+            const int rr = e - q * kPerPatch;
+            const int c = rr / (4 * kPieces);
+            const int ry = (rr / kPieces) & 3;
+            const int piece = rr % kPieces;
+            const int qa = (j0 >> 4) + q;
+            st_off[r] = e < n_seg ? (c * 4 + ry) * 64 + q * 16 + piece * S : -1;
+            dst_off[r] = ((qa >> 1) * 4 + (qa & 1)) * kRow + (c * 2) * 256 + ry * 16 + piece * S;
+        }
+    }
+    auto store_out = [&](int i) __attribute__((always_inline)) {   // rows i-3 .. i
+        wave_lds_fence();
+        const int yq = (i & 15) >> 2;
+        const int bh = i >> 5;
+        const int mh = (i >> 4) & 1;
+        const int64_t win_row0 = it_row_off + (int64_t(tt) * it_hm + bh) * it_wm * 4 + mh * 2;
+        elem_t* const obase = static_cast<elem_t*>(out) + win_row0 * kRow + yq * 64;
+        using u4v = unsigned __attribute__((ext_vector_type(4)));
+#pragma unroll
+        for (int r = 0; r < kStoreIter; ++r) {
+            if (st_off[r] >= 0) {
+                const uint4 val = *reinterpret_cast<const uint4*>(stage + st_off[r]);
+                elem_t* dst = obase + dst_off[r];
+                const u4v vv = {val.x, val.y, val.z, val.w};
+                if (both) {
+                    __builtin_nontemporal_store(vv, reinterpret_cast<u4v*>(dst));
+                    __builtin_nontemporal_store(vv, reinterpret_cast<u4v*>(dst + 256));
+                } else {
+                    __builtin_nontemporal_store(vv, reinterpret_cast<u4v*>(dst + dt_self * 256));
+                }
+            }
+        }
+        wave_lds_fence();
+    };
+
+    // Row y: the window sums, the slots, then the output rows that close on y.
+    auto process_row = [&](int y, const Win& raw, uint32_t shk, const float (&wr)[M]) __attribute__((always_inline)) {
+        // the window from its first byte: byte t of a[] is window byte t
+        uint32_t a[NA];
+#pragma unroll
+        for (int k = 0; k < NA; ++k) a[k] = __builtin_amdgcn_alignbyte(raw.d[k + 1], raw.d[k], shk);
+        float tsum[3];
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            float t = 0.f;
+#pragma unroll
+            for (int m = 0; m < KXE / 2; ++m) {
+                // channel c of taps 2m and 2m + 1: window bytes p and p + 3
+                constexpr int kZero = 0x0c;   // v_perm selector of a zero byte
+                const int p = 6 * m + c;
+                const int lo = p >> 2;
+                const int hi = lo + 1 < NA ? lo + 1 : lo;   // p + 3 stays in a[lo] when lo is the last
+                const uint32_t sel = static_cast<uint32_t>((p & 3) | (kZero << 8) | ((p + 3 - 4 * lo) << 16) |
+                                                           (kZero << 24));
+                const h2 pr = __builtin_bit_cast(h2, __builtin_amdgcn_perm(a[hi], a[lo], sel));
+                t = fmaf(wx[2 * m], static_cast<float>(pr.x), t);
+                t = fmaf(wx[2 * m + 1], static_cast<float>(pr.y), t);
+            }
+            tsum[c] = t;
+        }
+#pragma unroll
+        for (int s = 0; s < M; ++s) {
+            const float ws = wr[s];
+            acc[s][0] = fmaf(ws, tsum[0], acc[s][0]);
+            acc[s][1] = fmaf(ws, tsum[1], acc[s][1]);
+            acc[s][2] = fmaf(ws, tsum[2], acc[s][2]);
+        }
+        while (y == next_close && base < i1) {   // wave-uniform
+            const bool keep = base >= i0;
+            const int yy = base & 3;
+#pragma unroll
+            for (int s = 0; s < M; ++s) {
+                if (slot == s) {
+                    if (keep) {
+                        const float v0 = acc[s][0] * a0, v1 = acc[s][1] * a1, v2 = acc[s][2] * a2;
+                        elem_t* st = stage + yy * 64 + lane;
+                        if constexpr (OUT_BF16 != 0) {
+                            st[0] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v0));
+                            st[256] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
+                            st[512] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
+                        } else {
+                            st[0] = v0;
+                            st[256] = v1;
+                            st[512] = v2;
+                        }
+                    }
+                    acc[s][0] = z0;
+                    acc[s][1] = z1;
+                    acc[s][2] = z2;
+                }
+            }
+            if (keep && yy == 3) store_out(base);
+            ++base;
+            slot = slot + 1 == M ? 0 : slot + 1;
+            next_close = after_close;
+            after_close = close_row[base + 1];
+        }
+    };
+
+    const int yb0 = y0 & ~3;
+    Win pf[kPrefetch];
+#pragma unroll
+    for (int k = 0; k < kPrefetch; ++k) {
+        pf[k] = load_row(yb0, k);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int yb = yb0; yb < y1; yb += kPrefetch) {
+        const cptr<float> wblk = slot_w + yb * kSlotWords;
+        float wk[kPrefetch][M];
+#pragma unroll
+        for (int k = 0; k < kPrefetch; ++k)
+#pragma unroll
+            for (int s = 0; s < M; ++s) wk[k][s] = wblk[k * kSlotWords + s];
+#pragma unroll
+        for (int k = 0; k < kPrefetch; ++k) {
+            const int y = yb + k;
+            const Win cur = pf[k];
+            pf[k] = load_row(yb + kPrefetch, k);
+            if (y >= y0 && y < y1) process_row(y, cur, sh[k], wk[k]);
+        }
+    }
+}
+
+template <int M, int KXE>
+int launch_xfirst_shape(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
+                        const Norm& norm, hipStream_t stream) {
+    const int lds = xfirst_wave_bytes(out_dtype == 1 ? 2 : 4);
+    dim3 grid(static_cast<unsigned>(L.count)), block(64);
+    if (out_dtype == 1)
+        hipLaunchKernelGGL((xfirst_kernel<M, KXE, 1>), grid, block, lds, stream, plan, L.first, out, norm);
+    else
+        hipLaunchKernelGGL((xfirst_kernel<M, KXE, 0>), grid, block, lds, stream, plan, L.first, out, norm);
+    return static_cast<int>(hipGetLastError());
+}
+
+// ===========================================================================
 // uint8 streaming writer
 // ===========================================================================
 
@@ -1469,6 +1763,16 @@ int stream_case(const PlanView& plan, const StreamLaunch& L, void* out, int out_
 }
 
 template <int MM, int KK, int ID>
+int xfirst_case(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
+                const Norm& norm, hipStream_t stream) {
+    if constexpr (ID % VP_PARTS == VP_PART) {
+        if (L.m == MM && L.kx == KK && L.px == kPxXFirst)
+            return launch_xfirst_shape<MM, KK>(plan, L, out, out_dtype, norm, stream);
+    }
+    return -1;
+}
+
+template <int MM, int KK, int ID>
 int resize_case(const PlanView& plan, const StreamLaunch& L, void* out, hipStream_t stream) {
     if constexpr (ID % VP_PARTS == VP_PART) {
         if (L.m == MM && L.kx == KK) {
@@ -1506,6 +1810,14 @@ int VP_CAT(launch_stream_part, VP_PART)(const PlanView& plan, const StreamLaunch
 #undef VP_STREAM_LONG
 #undef VP_STREAM_KX
 #undef VP_STREAM_CASE
+#define VP_XF_CASE(MM, KK)                                                                    \
+    if (const int r = xfirst_case<MM, KK, __COUNTER__>(plan, L, out, out_dtype, norm, stream); \
+        r != -1)                                                                             \
+        return r;
+#define VP_XF_KX(MM) VP_XF_CASE(MM, 4) VP_XF_CASE(MM, 6) VP_XF_CASE(MM, 8) VP_XF_CASE(MM, 10) VP_XF_CASE(MM, 12)
+    VP_XF_KX(4) VP_XF_KX(5) VP_XF_KX(6) VP_XF_KX(7) VP_XF_KX(8)
+#undef VP_XF_KX
+#undef VP_XF_CASE
     return -1;
 }
 
@@ -1680,10 +1992,16 @@ bool stream_shape_supported(int m, int kx, int px) {
     return px == 2 || (px == 3 && m <= 5 && kx <= 24);
 }
 
+bool xfirst_shape_supported(int m, int kx) {
+    return m >= 4 && m <= kSlotWords && kx >= 4 && kx <= 12 && kx % 2 == 0;
+}
+
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream) {
     if (L.count <= 0) return 0;
-    if (!stream_shape_supported(L.m, L.kx, L.px) || stream_wave_bytes(L.px, L.kx, 4, L.patch) > kStreamLdsBudget)
+    if (L.px == kPxXFirst ? (!xfirst_shape_supported(L.m, L.kx) || L.patch != 16)
+                 : (!stream_shape_supported(L.m, L.kx, L.px) ||
+                    stream_wave_bytes(L.px, L.kx, 4, L.patch) > kStreamLdsBudget))
         return static_cast<int>(hipErrorInvalidConfiguration);
     for (const StreamPartFn part : kStreamParts)
         if (const int r = part(plan, L, out, out_dtype, norm, stream); r != -1) return r;

@@ -29,8 +29,10 @@
 //            (an upscaled axis, the bottom border)
 //   fixed-point window table (uint8 writer): as the window table, with int32
 //       weights in units of 2^-22
-//   column table of an x axis (streaming kernel), KX taps, for output bands
-//   of `band` columns whose source pixels fit an LDS row of `row_px` pixels:
+//   column table of an x axis (streaming kernels), KX taps, for output bands
+//   of `band` columns whose source pixels fit a row of `row_px` pixels (the
+//   y-first kernel's LDS row; the x-first kernel passes W + KX, a bound no
+//   window reaches):
 //       int32 start[n_out]; float weight[n_out][KX]
 //     -- start is relative to the first source pixel of the output's band
 //        (the window start of the band's first column) and start + KX never
@@ -62,6 +64,10 @@ constexpr int stream_wave_bytes(int px, int kx, int elem_bytes, int patch = 16) 
     return (void)kx, patch == 16 ? 64 * px * 16 + 3 * 4 * 64 * elem_bytes
                                  : 4 * 64 * px * 16 + 8 * 6 * patch * patch * elem_bytes;
 }
+
+// LDS of one x-first streaming workgroup (one wave): the stage of four
+// output rows (its lanes load their source windows from memory).
+constexpr int xfirst_wave_bytes(int elem_bytes) { return 3 * 4 * 64 * elem_bytes; }
 
 // uint8 streaming writer: pixels per lane (a band's source span is at most
 // 64 * kRsPx pixels), and the LDS of one workgroup (one wave): its source
@@ -104,7 +110,7 @@ struct DevItem {
     int32_t route;
     int32_t band;            // streaming kernel: output columns per wave (16, 32, 48 or 64)
     int32_t sy_off, sx_off;  // streaming kernel: slot and column tables
-    int32_t row_px;          // streaming kernel: source pixels per wave row (64 * px)
+    int32_t row_px;          // streaming kernels: the column table's row bound (64 * px; x-first W + kx)
     int32_t patch;           // patch edge P (16 or 14): rows of 6 P^2 values, windows of 2P
 };
 static_assert(sizeof(DevItem) == 104, "DevItem layout");
@@ -148,10 +154,11 @@ constexpr int kWgBandMax = (1 << (32 - kWgBandShift)) - 2;   // keeps entries be
 constexpr uint32_t kNoWork = 0xffffffffu;
 
 // One launch of the streaming kernel: workgroups wgs[first, first + count),
-// all with the same template shape.
+// all with the same template shape.  px == kPxXFirst marks the x-first kernel.
+constexpr int32_t kPxXFirst = -1;
 struct StreamLaunch {
     int32_t first, count;
-    int32_t m, kx, px;       // accumulator slots, column taps, pixels per lane
+    int32_t m, kx, px;       // accumulator slots, column taps, pixels per lane (or kPxXFirst)
     int32_t patch;           // patch edge of the batch (16 or 14)
     int64_t cost;            // host only: estimated work (source pixels read)
 };
@@ -184,5 +191,7 @@ int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t r
                      hipStream_t stream);
 // Whether a (m, kx, px) shape has a compiled streaming kernel.
 bool stream_shape_supported(int m, int kx, int px);
+// Whether an (m, kx) shape has a compiled x-first kernel.
+bool xfirst_shape_supported(int m, int kx);
 
 }  // namespace vp

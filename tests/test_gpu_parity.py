@@ -162,6 +162,17 @@ SMALL = [
     ("taps9_px2", [(2, 180, 640, [1, 0], 96, 288)], "f32"),
     ("taps10_px3", [(3, 90, 300, [2, 0], 32, 128)], "bf16"),
     ("taps7_bf16", [(2, 120, 854, [1, 0], 64, 512)], "bf16"),
+    # the x-first kernel (vertical scales up to 1.6): 12, 10 and 8 taps,
+    # a last band of 32 columns, odd frame sizes (windows at every byte
+    # alignment), a scale just under the limit; one just over it and a
+    # near-1 vertical scale whose x window is too long for x-first stay on
+    # the y-first kernel
+    ("xfirst_taps12_ragged_band", [(2, 100, 691, [1, 0], 96, 288)], "f32"),
+    ("xfirst_taps10_bf16", [(3, 90, 512, [2, 0, 1], 96, 256)], "bf16"),
+    ("xfirst_taps8_odd_sizes", [(2, 121, 451, [0, 1], 96, 320)], "f32"),
+    ("xfirst_scale_1p55", [(2, 149, 300, [1, 0], 96, 192)], "bf16"),
+    ("yfirst_scale_1p65", [(2, 158, 300, [1, 0], 96, 192)], "bf16"),
+    ("yfirst_near1_long_x", [(2, 64, 900, [0, 1], 64, 256)], "f32"),
 ]
 
 
