@@ -475,11 +475,11 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t pa
 
 // The x-first streaming kernel (patch 16) for an item, if it can take it:
 // bands of 64 output columns (the last one narrower where the width is not a
-// multiple of 64), an even tap count from 4 to 12 (the window's taps rounded
-// up), M slots.
+// multiple of 64), 4 to 12 taps (the window's own count, at least 4), M
+// slots.
 // Its shape is recorded with px = kPxXFirst.
 bool xfirst_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
-    const int32_t kx = round_up(std::max<int32_t>(fx.taps, 4), 2);
+    const int32_t kx = std::max<int32_t>(fx.taps, 4);
     if (!vp::xfirst_shape_supported(m, kx)) return false;
     // every load of a frame row (a window of up to 3 kx + 4 bytes past its
     // start, up to kSlotMax + 8 rows past the last one) stays below 4 GiB

@@ -1022,10 +1022,11 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 //     overlap, and the overlap is served by the L1 cache, not HBM;
 //   * the lane shifts the window to its first byte (v_alignbyte by the
 //     window's byte misalignment) and moves the bytes of taps 2m and 2m + 1
-//     of each channel into the two 16-bit halves of a register with zero high
-//     bytes (one v_perm with a fixed selector): byte value b reads as the f16
-//     denormal b * 2^-24, as in the y-first kernel, so the x sums are
-//     mixed-precision FMAs with no conversion (exact products);
+//     of each channel (an odd count's last tap alone) into the two 16-bit
+//     halves of a register with zero high bytes (one v_perm with a fixed
+//     selector): byte value b reads as the f16 denormal b * 2^-24, as in
+//     the y-first kernel, so the x sums are mixed-precision FMAs with no
+//     conversion (exact products);
 //   * the three channel sums go into M rotating accumulator slots with the
 //     slot table's wave-uniform weights, which carry the factor 2^24; a slot
 //     starts at z_c = -255 mean_c, so a closed slot holds R + z_c;
@@ -1037,7 +1038,7 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 template <int M, int KXE, int OUT_BF16>
 __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
-    static_assert(KXE % 2 == 0 && KXE >= 4 && KXE <= 12, "even tap counts from 4 to 12");
+    static_assert(KXE >= 4 && KXE <= 12, "tap counts from 4 to 12");
     constexpr int NA = (3 * KXE + 3) / 4;          // dwords of the window from its first byte
     constexpr int ND = NA + 1;                     // dwords loaded: the window at any alignment
     constexpr int S = 16 / int(sizeof(elem_t));    // output columns per 16-byte store
@@ -1212,17 +1213,19 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
         for (int c = 0; c < 3; ++c) {
             float t = 0.f;
 #pragma unroll
-            for (int m = 0; m < KXE / 2; ++m) {
+            for (int m = 0; m < (KXE + 1) / 2; ++m) {
                 // channel c of taps 2m and 2m + 1: window bytes p and p + 3
+                // (an odd count's last tap alone, its high half zero)
                 constexpr int kZero = 0x0c;   // v_perm selector of a zero byte
+                const bool pair = 2 * m + 1 < KXE;
                 const int p = 6 * m + c;
                 const int lo = p >> 2;
                 const int hi = lo + 1 < NA ? lo + 1 : lo;   // p + 3 stays in a[lo] when lo is the last
-                const uint32_t sel = static_cast<uint32_t>((p & 3) | (kZero << 8) | ((p + 3 - 4 * lo) << 16) |
-                                                           (kZero << 24));
+                const uint32_t sel = static_cast<uint32_t>((p & 3) | (kZero << 8) |
+                                                           ((pair ? p + 3 - 4 * lo : kZero) << 16) | (kZero << 24));
                 const h2 pr = __builtin_bit_cast(h2, __builtin_amdgcn_perm(a[hi], a[lo], sel));
                 t = fmaf(wx[2 * m], static_cast<float>(pr.x), t);
-                t = fmaf(wx[2 * m + 1], static_cast<float>(pr.y), t);
+                if (pair) t = fmaf(wx[2 * m + 1], static_cast<float>(pr.y), t);
             }
             tsum[c] = t;
         }
@@ -1814,7 +1817,8 @@ int VP_CAT(launch_stream_part, VP_PART)(const PlanView& plan, const StreamLaunch
     if (const int r = xfirst_case<MM, KK, __COUNTER__>(plan, L, out, out_dtype, norm, stream); \
         r != -1)                                                                             \
         return r;
-#define VP_XF_KX(MM) VP_XF_CASE(MM, 4) VP_XF_CASE(MM, 6) VP_XF_CASE(MM, 8) VP_XF_CASE(MM, 10) VP_XF_CASE(MM, 12)
+#define VP_XF_KX(MM) VP_XF_CASE(MM, 4) VP_XF_CASE(MM, 5) VP_XF_CASE(MM, 6) VP_XF_CASE(MM, 7) VP_XF_CASE(MM, 8) \
+    VP_XF_CASE(MM, 9) VP_XF_CASE(MM, 10) VP_XF_CASE(MM, 11) VP_XF_CASE(MM, 12)
     VP_XF_KX(4) VP_XF_KX(5) VP_XF_KX(6) VP_XF_KX(7) VP_XF_KX(8)
 #undef VP_XF_KX
 #undef VP_XF_CASE
@@ -1993,7 +1997,7 @@ bool stream_shape_supported(int m, int kx, int px) {
 }
 
 bool xfirst_shape_supported(int m, int kx) {
-    return m >= 4 && m <= kSlotWords && kx >= 4 && kx <= 12 && kx % 2 == 0;
+    return m >= 4 && m <= kSlotWords && kx >= 4 && kx <= 12;
 }
 
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
