@@ -1095,11 +1095,14 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     const uint32_t lead = static_cast<uint32_t>(fa & 3u);
     const uint32_t range = static_cast<uint32_t>((it->frame_bytes + lead + 3) & ~int64_t(3));
     const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
-    uint32_t voff[kPrefetch], sh[kPrefetch];
+    // (one offset per 16-byte chunk of the window, so that no row adds them)
+    constexpr int NC = (ND + 3) / 4;
+    uint32_t voff[kPrefetch][NC], sh[kPrefetch];
 #pragma unroll
     for (int k = 0; k < kPrefetch; ++k) {
         const uint32_t c = lead + static_cast<uint32_t>(k) * row_bytes + 3u * static_cast<uint32_t>(x0 + sj);
-        voff[k] = c & ~3u;
+#pragma unroll
+        for (int i = 0; i < NC; ++i) voff[k][i] = (c & ~3u) + 16u * static_cast<uint32_t>(i);
         sh[k] = c & 3u;
     }
     struct Win {
@@ -1116,7 +1119,7 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
         Win r;
 #pragma unroll
         for (int i = 0; i < ND; i += 4) {
-            const uint32_t vo = voff[k] + 4u * static_cast<uint32_t>(i);
+            const uint32_t vo = voff[k][i / 4];
             if (ND - i >= 4) {
                 const auto v = __builtin_amdgcn_raw_buffer_load_b128(rb, vo, 0, 0);
                 r.d[i] = v[0];
@@ -1202,12 +1205,9 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
         wave_lds_fence();
     };
 
-    // Row y: the window sums, the slots, then the output rows that close on y.
-    auto process_row = [&](int y, const Win& raw, uint32_t shk, const float (&wr)[M]) __attribute__((always_inline)) {
-        // the window from its first byte: byte t of a[] is window byte t
-        uint32_t a[NA];
-#pragma unroll
-        for (int k = 0; k < NA; ++k) a[k] = __builtin_amdgcn_alignbyte(raw.d[k + 1], raw.d[k], shk);
+    // Row y (its window from the first byte: byte t of a[] is window byte t):
+    // the window sums, the slots, then the output rows that close on y.
+    auto process_row = [&](int y, const uint32_t (&a)[NA], const float (&wr)[M]) __attribute__((always_inline)) {
         float tsum[3];
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
@@ -1285,9 +1285,15 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
 #pragma unroll
         for (int k = 0; k < kPrefetch; ++k) {
             const int y = yb + k;
-            const Win cur = pf[k];
+            // align first: the next load then reuses pf[k]'s registers
+            // instead of copying them while it is in flight
+            uint32_t a[NA];
+#pragma unroll
+            for (int q = 0; q < NA; ++q) a[q] = __builtin_amdgcn_alignbyte(pf[k].d[q + 1], pf[k].d[q], sh[k]);
+#pragma unroll
+            for (int q = 0; q < NA; ++q) asm volatile("" : : "v"(a[q]));
             pf[k] = load_row(yb + kPrefetch, k);
-            if (y >= y0 && y < y1) process_row(y, cur, sh[k], wk[k]);
+            if (y >= y0 && y < y1) process_row(y, a, wk[k]);
         }
     }
 }
