@@ -568,18 +568,28 @@ struct Keyed {
 // Output rows per streaming unit of an item: at most about max_src_rows
 // source rows, at least ten windows of source rows, a multiple of `group`
 // rows (the kernel's store group), and at least 16 rows (28 for groups of 14).
-// A frame's rows are then cut into that many units of nearly equal length:
-// units of one frame are neighbours in the workgroup list, and a long unit
-// followed by a short remainder would load the XCDs unevenly.
 int64_t unit_row_band(const vp::DevItem& d, int64_t max_src_rows, int64_t group) {
     int64_t band = max_src_rows * d.h / d.H;
     const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
     band = std::max(band, min_band);
     band = std::max<int64_t>((band + group - 1) / group * group, group == 4 ? 16 : 2 * group);
-    if (band >= d.h) return d.h;   // h is a multiple of 2P: every band ends on a whole group
-    const int64_t n = (d.h + band - 1) / band;
-    return ((d.h + n - 1) / n + group - 1) / group * group;   // at most band, more than band (n - 1) / n
+    return std::min<int64_t>(band, d.h);
 }
+
+// A frame's h output rows cut into n = ceil(h / band) units whose boundaries
+// fall on whole store groups of `group` rows, as evenly as that allows:
+// lengths differ by at most one group, and the last unit also takes the rows
+// past the last whole group.  Units of one frame are neighbours in the
+// workgroup list, and a long unit followed by a short remainder (a 320-row
+// frame at a 296-row cap: 296 + 24) would load the XCDs unevenly.
+struct UnitSplit {
+    int64_t h, group, groups, n;
+    UnitSplit(int64_t h_, int64_t band, int64_t group_) : h(h_), group(group_), groups(h_ / group_) {
+        n = std::max<int64_t>(1, std::min<int64_t>((h + band - 1) / band, groups));
+    }
+    int32_t begin(int64_t u) const { return static_cast<int32_t>(group * (groups * u / n)); }
+    int32_t end(int64_t u) const { return static_cast<int32_t>(u + 1 == n ? h : group * (groups * (u + 1) / n)); }
+};
 
 // Lays out the streaming units as launches and their workgroup lists.
 int32_t assemble_launches(const std::vector<Keyed>& keyed, int32_t P, Plan* p) {
@@ -805,13 +815,14 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         const StreamShape& sh = shapes[b];
         // whole store groups: multiples of 4 rows for patch 16, whole
         // patch rows (14 output rows, stored at once) for patch 14
-        const int64_t band = unit_row_band(d, max_src_rows, d.patch == 16 ? 4 : d.patch);
+        const int64_t group = d.patch == 16 ? 4 : d.patch;
+        const UnitSplit split(d.h, unit_row_band(d, max_src_rows, group), group);
         for (int32_t tt = 0; tt < d.t; ++tt) {
             const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
             const bool pair_units = d.patch == 14;   // both frames in one unit
             for (int32_t dt = 0; dt < (same || pair_units ? 1 : 2); ++dt) {
-                for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
-                    const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
+                for (int64_t u = 0; u < split.n; ++u) {
+                    const int32_t i0 = split.begin(u), i1 = split.end(u);
                     Keyed k;
                     k.key = std::make_tuple(sh.m, sh.kx, sh.px);
                     k.bands = d.patch == 14 ? (sh.bands + 1) / 2 : sh.bands;   // patch 14: bands in pairs
@@ -1168,10 +1179,10 @@ int32_t build_resize_plan(const vp_item* items, int32_t n, Plan* p) {
         const vp::DevItem& d = p->items[b];
         if (d.route != vp::kRouteStream) continue;
         const StreamShape& sh = shapes[b];
-        const int64_t band = unit_row_band(d, max_src_rows, 4);
+        const UnitSplit split(d.h, unit_row_band(d, max_src_rows, 4), 4);
         for (int32_t k = 0; k < d.t; ++k) {
-            for (int32_t i0 = 0; i0 < d.h; i0 += static_cast<int32_t>(band)) {
-                const int32_t i1 = static_cast<int32_t>(i0 + band < d.h ? i0 + band : d.h);
+            for (int64_t u = 0; u < split.n; ++u) {
+                const int32_t i0 = split.begin(u), i1 = split.end(u);
                 Keyed e;
                 e.key = std::make_tuple(sh.m, sh.kx, sh.px);
                 e.bands = sh.bands;
