@@ -1,11 +1,12 @@
 // vp_kernels.hip -- gfx950 kernels of the preprocessing path.
 //
-// Two kernels compute the same result (the resampled, normalised,
+// Three kernels compute the same result (the resampled, normalised,
 // merge-window rows of Section 3.1.1 of arXiv 2604.16893, laid out per the
 // grid the host reports); the host routes each item to one of them.
 //
-// Streaming kernel (the fast path; items whose frames are not upscaled
-// vertically and whose filters are short enough).  One workgroup streams
+// Streaming kernel, y first (the fast path for vertical downscales: items
+// with at most 8 output rows open on a source row and x windows of at most
+// 32 taps that the x-first kernel below does not take).  One workgroup streams
 // one source frame -- or a band of its output rows -- top to bottom, one
 // wave per band of up to 64 output columns; the waves never wait for each
 // other:
@@ -27,6 +28,11 @@
 //   * patch 14 is the exception to independent waves: a workgroup is four
 //     waves (two neighbouring bands x a pair's two frames) that meet at a
 //     barrier once per patch row, to write whole output rows.
+//
+// Streaming kernel, x first (patch 16, vertical scales up to 1.6, x windows
+// of 4 to 12 taps): the same units, slots and store, but each lane x-filters
+// its own window of every source row, loaded straight from the frame, before
+// the y pass into the slots; LDS holds only the stage.
 //
 // General kernel (any scale factor): one workgroup per merge window of one
 // frame pair; y pass from global memory into an LDS column tile, x pass,
