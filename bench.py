@@ -70,6 +70,16 @@ def counter_traffic(workload_tag: str, sha: str):
     return d.get("hbm_bytes_per_call")
 
 
+def counter_fields(traffic, alg_bytes, kernel_ms):
+    """Counter-based GB/s (the metric as named) and the ratio of counter to
+    algorithmic bytes, flagged above 1.10 (halo or intermediate traffic)."""
+    if traffic is None:
+        return dict(counter_gbps=None, traffic_ratio=None, halo_flag=None)
+    ratio = traffic / alg_bytes
+    return dict(counter_gbps=round(traffic / (kernel_ms * 1e-3) / 1e9, 1), traffic_ratio=round(ratio, 4),
+                halo_flag=ratio > 1.10)
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -190,6 +200,72 @@ def copy_ceiling(torch, dev, nbytes=4 << 30, reps=12):
     return 2 * nbytes / (best * 1e-3) / 1e9, best
 
 
+def oracle_jobs(run, b, resize_only=False):
+    """The oracle calls of item b: one per frame pair (or one per item for
+    the uint8 writer), with host copies of the frames they read."""
+    import numpy as np
+    h, w, idx = run.planned[b]
+    padded = list(idx) + ([idx[-1]] if len(idx) % 2 else [])
+    host = run.frames[b].cpu().numpy()
+    if resize_only:
+        return [(np.ascontiguousarray(host[list(idx)]), h, w, None)]
+    return [(np.ascontiguousarray(host[[padded[2 * tt], padded[2 * tt + 1]]]), h, w, tt)
+            for tt in range(len(padded) // 2)]
+
+
+def oracle_call(run, j, patch_only=False, resize_only=False):
+    import oracle
+    wl = run.wl
+    frames, h, w, tt = j
+    patch = wl.items[0].patch
+    if resize_only:
+        return oracle.resize_u8_item(frames, list(range(len(frames))), h, w)
+    if patch_only:
+        return oracle.patchify_item(frames, [0, 1], wl.mean, wl.std, patch=patch)
+    return oracle.preprocess_item(frames, [0, 1], h, w, wl.mean, wl.std, patch=patch)
+
+
+def check_item(run, b, jobs, refs):
+    """The GPU's rows of item b (the last call's output) against the oracle's."""
+    import numpy as np
+    from oracle import compare
+    vp, torch = run.vp, run.torch
+    patch = run.wl.items[0].patch
+    h, w, _ = run.planned[b]
+    per_t = (h // patch) * (w // patch)
+    cu = np.concatenate([[0], np.cumsum([((len(p[2]) + 1) // 2) * (p[0] // patch) * (p[1] // patch)
+                                        for p in run.planned])])
+    res = []
+    for j, ref in zip(jobs, refs):
+        r0 = int(cu[b]) + j[3] * per_t
+        t = run.out[r0:r0 + per_t]
+        if run.code == vp.VP_OUT_BF16:
+            res.append(compare.check_bf16(t.view(torch.int16).cpu().numpy().view(np.uint16), ref))
+        else:
+            res.append(compare.check_f32(t.cpu().numpy(), ref))
+    return compare.merge(res)
+
+
+def parity_every_row(run):
+    """Every row of the run's last call against the oracle (frame pairs over
+    the host's threads), as the measurement protocol asks for C0-C3."""
+    import concurrent.futures as cf
+    import oracle
+    from oracle import compare
+    oracle.lib()
+    threads = max(1, min(CPU_SHARE, os.cpu_count() or 1))
+    t0 = time.perf_counter()
+    res = []
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        for b in range(len(run.frames)):
+            jobs = oracle_jobs(run, b)
+            res.append(check_item(run, b, jobs, list(ex.map(lambda j: oracle_call(run, j), jobs))))
+    out = compare.merge(res)
+    out["rows_checked"] = run.rows
+    out["seconds"] = round(time.perf_counter() - t0, 2)
+    return out
+
+
 def cpu_baseline(run, budget_s=10.0, single_s=2.5, patch_only=False, resize_only=False):
     """The oracle on the first items of the workload, in order, until about
     `budget_s` seconds of oracle time on a thread pool (frame pairs spread
@@ -198,49 +274,20 @@ def cpu_baseline(run, budget_s=10.0, single_s=2.5, patch_only=False, resize_only
     the GPU's rows of the same items (the last timed step's output)."""
     import concurrent.futures as cf
 
-    import numpy as np
-
     import oracle
     from oracle import compare
     oracle.lib()
-    wl, vp, torch = run.wl, run.vp, run.torch
     threads = max(1, min(CPU_SHARE, os.cpu_count() or 1))
-    patch = wl.items[0].patch
     results = []
 
     def jobs_of(b):
-        h, w, idx = run.planned[b]
-        padded = list(idx) + ([idx[-1]] if len(idx) % 2 else [])
-        host = run.frames[b].cpu().numpy()
-        if resize_only:
-            return [(np.ascontiguousarray(host[list(idx)]), h, w, None)]
-        return [(np.ascontiguousarray(host[[padded[2 * tt], padded[2 * tt + 1]]]), h, w, tt)
-                for tt in range(len(padded) // 2)]
+        return oracle_jobs(run, b, resize_only)
 
-    def oracle_call(j):
-        frames, h, w, tt = j
-        if resize_only:
-            return oracle.resize_u8_item(frames, list(range(len(frames))), h, w)
-        if patch_only:
-            return oracle.patchify_item(frames, [0, 1], wl.mean, wl.std, patch=patch)
-        return oracle.preprocess_item(frames, [0, 1], h, w, wl.mean, wl.std, patch=patch)
+    def call(j):
+        return oracle_call(run, j, patch_only, resize_only)
 
     def check(b, jobs, refs):
-        if resize_only:
-            return None
-        h, w, _ = run.planned[b]
-        per_t = (h // patch) * (w // patch)
-        cu = np.concatenate([[0], np.cumsum([((len(p[2]) + 1) // 2) * (p[0] // patch) * (p[1] // patch)
-                                            for p in run.planned])])
-        res = []
-        for j, ref in zip(jobs, refs):
-            r0 = int(cu[b]) + j[3] * per_t
-            t = run.out[r0:r0 + per_t]
-            if run.code == vp.VP_OUT_BF16:
-                res.append(compare.check_bf16(t.view(torch.int16).cpu().numpy().view(np.uint16), ref))
-            else:
-                res.append(compare.check_f32(t.cpu().numpy(), ref))
-        return compare.merge(res)
+        return None if resize_only else check_item(run, b, jobs, refs)
 
     frames_count = pairs = items = 0
     spent = 0.0
@@ -248,7 +295,7 @@ def cpu_baseline(run, budget_s=10.0, single_s=2.5, patch_only=False, resize_only
         for b in range(len(run.frames)):
             jobs = jobs_of(b)
             t0 = time.perf_counter()
-            refs = list(ex.map(oracle_call, jobs))
+            refs = list(ex.map(call, jobs))
             spent += time.perf_counter() - t0
             r = check(b, jobs, refs)
             if r is not None:
@@ -264,7 +311,7 @@ def cpu_baseline(run, budget_s=10.0, single_s=2.5, patch_only=False, resize_only
     done, one_spent = 0, 0.0
     for j in jobs:
         t0 = time.perf_counter()
-        oracle_call(j)
+        call(j)
         one_spent += time.perf_counter() - t0
         done += 1
         if one_spent >= single_s:
@@ -420,6 +467,8 @@ def main():
             gc.enable()
             mk = sum(kms) / len(kms)
             gbps = r.alg_bytes / (mk * 1e-3) / 1e9
+            tr = counter_traffic(f"c{k}", sha)
+            par = None if args.no_cpu_baseline else parity_every_row(r)
             per_config[f"c{k}"] = dict(
                 workload=wk.name, frames=r.n_frames, rows=r.rows, out_dtype=wk.out_dtype,
                 algorithmic_bytes=r.alg_bytes, kernel_ms=round(mk, 4),
@@ -427,9 +476,10 @@ def main():
                 frames_per_s=round(r.n_frames / (mk * 1e-3), 1),
                 frames_per_s_wall=round(r.n_frames * args.config_steps / w_s, 1),
                 achieved_gbps=round(gbps, 1), frac=round(gbps / HBM_PEAK_GBPS, 4),
-                traffic=counter_traffic(f"c{k}", sha), steps=args.config_steps)
+                traffic=tr, **counter_fields(tr, r.alg_bytes, mk), steps=args.config_steps,
+                parity_every_row=par)
             log(f"c{k}: kernels {mk:.4f} ms mean, {gbps:,.0f} GB/s ({gbps / HBM_PEAK_GBPS:.1%}), "
-                f"{r.n_frames / (mk * 1e-3):,.0f} frames/s")
+                f"{r.n_frames / (mk * 1e-3):,.0f} frames/s; every row against the oracle: {par}")
             del r
             torch.cuda.synchronize()
             torch.cuda.empty_cache()
@@ -467,6 +517,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
+            **counter_fields(traffic, run.alg_bytes, mean_kern_ms),
             "kernel_ms": round(mean_kern_ms, 4),
             "kernel_ms_median": round(sorted(kern_ms)[len(kern_ms) // 2], 4),
         },
