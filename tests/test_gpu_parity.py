@@ -173,6 +173,13 @@ SMALL = [
     ("xfirst_scale_1p55", [(2, 149, 300, [1, 0], 96, 192)], "bf16"),
     ("yfirst_scale_1p65", [(2, 158, 300, [1, 0], 96, 192)], "bf16"),
     ("yfirst_near1_long_x", [(2, 64, 900, [0, 1], 64, 256)], "f32"),
+    # x-first edges: a 5-pixel-wide source (windows run past the row into
+    # the next row and past the frame's end), a source just wider than one
+    # band, and eight open rows (2x vertical upscale) in fp32 with an odd
+    # tap count
+    ("xfirst_width5_source", [(3, 30, 5, [2, 0, 1], 32, 32)], "bf16"),
+    ("xfirst_one_band_plus", [(2, 70, 67, [1, 0], 64, 64)], "f32"),
+    ("xfirst_eight_slots_odd_taps", [(2, 48, 150, [0, 1], 96, 96)], "f32"),
 ]
 
 
