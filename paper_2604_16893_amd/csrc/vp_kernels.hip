@@ -988,7 +988,11 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
             // below and pf[k] has to be copied while its load is in flight)
 #pragma unroll
             for (int q = 0; q < kPairs; ++q) asm volatile("" : : "v"(hv[q]));
+            // (issued at raised wave priority, so that the load leaves ahead
+            // of other waves' arithmetic and the memory stream stays full)
+            __builtin_amdgcn_s_setprio(2);
             pf[k] = load_row(yb + kPrefetch, k);
+            __builtin_amdgcn_s_setprio(0);
             if (y >= y0 && y < y1) process_row(y, hv, wk[k]);
         }
     }
@@ -1298,7 +1302,11 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
             for (int q = 0; q < NA; ++q) a[q] = __builtin_amdgcn_alignbyte(pf[k].d[q + 1], pf[k].d[q], sh[k]);
 #pragma unroll
             for (int q = 0; q < NA; ++q) asm volatile("" : : "v"(a[q]));
+            // (issued at raised wave priority, so that the load leaves ahead
+            // of other waves' arithmetic and the memory stream stays full)
+            __builtin_amdgcn_s_setprio(2);
             pf[k] = load_row(yb + kPrefetch, k);
+            __builtin_amdgcn_s_setprio(0);
             if (y >= y0 && y < y1) process_row(y, a, wk[k]);
         }
     }
