@@ -51,7 +51,7 @@ def log(msg):
 
 def kernel_source_sha() -> str:
     h = hashlib.sha256()
-    for name in ("vp_kernels.hip", "vp_plan.h"):
+    for name in ("vp_kernels.hip", "vp_plan.h", "vp_api.cpp"):
         with open(os.path.join(ROOT, "paper_2604_16893_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]

@@ -566,11 +566,12 @@ struct Keyed {
 };
 
 // Output rows per streaming unit of an item: at most about max_src_rows
-// source rows, at least ten windows of source rows, a multiple of `group`
-// rows (the kernel's store group), and at least 16 rows (28 for groups of 14).
-int64_t unit_row_band(const vp::DevItem& d, int64_t max_src_rows, int64_t group) {
+// source rows, at least min_windows windows of source rows, a multiple of
+// `group` rows (the kernel's store group), and at least 16 rows (28 for
+// groups of 14).
+int64_t unit_row_band(const vp::DevItem& d, int64_t max_src_rows, int64_t group, int64_t min_windows = 10) {
     int64_t band = max_src_rows * d.h / d.H;
-    const int64_t min_band = (int64_t(10) * d.ky * d.h + d.H - 1) / d.H;
+    const int64_t min_band = (min_windows * d.ky * d.h + d.H - 1) / d.H;
     band = std::max(band, min_band);
     band = std::max<int64_t>((band + group - 1) / group * group, group == 4 ? 16 : 2 * group);
     return std::min<int64_t>(band, d.h);
@@ -793,7 +794,10 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     // bands of output rows that are multiples of 4 (one 64-value run per
     // store).  A band re-reads the source rows that its first window shares
     // with the band above, so none spans fewer than ten windows of source
-    // rows.
+    // rows, or fifteen where the batch still gives every wave slot two
+    // workgroups at that length (a small batch of large frames -- one 1080p
+    // video of 128 frames -- otherwise gets units of ten windows that
+    // re-read about a tenth of their rows).
     constexpr int64_t kWaveSlots = 256 * 20;
     int64_t wave_rows = 0;   // source rows that all workgroups stream, whole frames
     int64_t stream_frames = 0;
@@ -807,6 +811,23 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         }
     }
     const int64_t max_src_rows = wave_rows / (kWaveSlots * 8);
+    auto workgroup_waves = [&](int64_t min_windows) {
+        int64_t waves = 0;
+        for (int32_t b = 0; b < n; ++b) {
+            const vp::DevItem& d = p->items[b];
+            if (d.route != vp::kRouteStream) continue;
+            const int64_t group = d.patch == 16 ? 4 : d.patch;
+            const int64_t units = UnitSplit(d.h, unit_row_band(d, max_src_rows, group, min_windows), group).n;
+            int64_t frames = 0;   // units per row band: one per distinct frame (patch 14: per pair)
+            for (int32_t tt = 0; tt < d.t; ++tt)
+                frames += d.patch == 14 || p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1]
+                              ? 1 : 2;
+            const int64_t per_unit = d.patch == 14 ? 4 * ((shapes[b].bands + 1) / 2) : shapes[b].bands;
+            waves += frames * units * per_unit;
+        }
+        return waves;
+    };
+    const int64_t min_windows = workgroup_waves(15) >= 2 * kWaveSlots ? 15 : 10;
     std::vector<Keyed> keyed;
     keyed.reserve(static_cast<size_t>(stream_frames));
     for (int32_t b = 0; b < n; ++b) {
@@ -816,7 +837,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         // whole store groups: multiples of 4 rows for patch 16, whole
         // patch rows (14 output rows, stored at once) for patch 14
         const int64_t group = d.patch == 16 ? 4 : d.patch;
-        const UnitSplit split(d.h, unit_row_band(d, max_src_rows, group), group);
+        const UnitSplit split(d.h, unit_row_band(d, max_src_rows, group, min_windows), group);
         for (int32_t tt = 0; tt < d.t; ++tt) {
             const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
             const bool pair_units = d.patch == 14;   // both frames in one unit
