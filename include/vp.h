@@ -191,6 +191,30 @@ int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw
                         int32_t* cu_seqlens, int64_t* total_rows, int64_t* workspace_bytes);
 
 /*
+ * Diagnostic: the kernel launches that vp_preprocess_batch makes for a
+ * batch, without running them (no device memory is touched): which form of
+ * the resampling (Section 3.2: resize, normalise and patchify fused into one
+ * pass per frame) each group of items takes.  For tests and tuning.
+ * launches: HOST int32[capacity][6], or NULL with capacity 0.  Row i:
+ *   kind: VP_KERNEL_GENERIC, VP_KERNEL_YFIRST or VP_KERNEL_XFIRST;
+ *   M, the accumulator slots (output rows open at one source row; 0 for
+ *   the generic kernel);
+ *   the column taps of the x windows (0 for the generic kernel);
+ *   y-first: source pixels per lane; else 0;
+ *   x-first: output columns per lane (1, or 2 for column pairs); else 0;
+ *   workgroups (the generic kernel: output tiles).
+ *   Rows past `capacity` are not written.
+ * n_launches: HOST, receives the number of launches.
+ * Errors: as vp_batch_layout; VP_ERR_NULL (n_launches), VP_ERR_ARG
+ * (capacity < 0, or launches NULL with capacity > 0).
+ */
+#define VP_KERNEL_GENERIC 0
+#define VP_KERNEL_YFIRST 1
+#define VP_KERNEL_XFIRST 2
+int32_t vp_batch_kernels(const vp_item* items, int32_t n_items, int32_t* launches,
+                         int32_t capacity, int32_t* n_launches);
+
+/*
  * Preprocess a batch on the GPU: for every item, every sampled frame is
  * resampled from (src_h, src_w) to (dst_h, dst_w) with the filter of
  * vp_filter_table along x then y (no clamping, no rounding in between),

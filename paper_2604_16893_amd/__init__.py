@@ -39,7 +39,7 @@ def row_width(patch: int = VP_PATCH) -> int:
 VP_FACTOR = 32
 
 EXPORTED = ("vp_smart_resize_dims", "vp_sample_indices", "vp_filter_taps", "vp_filter_table",
-            "vp_filter_table_fixed", "vp_batch_layout", "vp_preprocess_batch",
+            "vp_filter_table_fixed", "vp_batch_layout", "vp_batch_kernels", "vp_preprocess_batch",
             "vp_preprocess_batch_noalloc", "vp_patchify_batch",
             "vp_resize_layout", "vp_resize_batch", "vp_position_ids", "vp_status_string",
             "vp_last_error_message", "vp_set_kernel_events")
@@ -82,6 +82,7 @@ def lib() -> ctypes.CDLL:
         L.vp_filter_taps.argtypes = [i32, i32, i32p]
         L.vp_filter_table.argtypes = [i32, i32, i32, i32p, i32p, f32p]
         L.vp_batch_layout.argtypes = [itemp, i32, i32p, i32p, i64p, i64p]
+        L.vp_batch_kernels.argtypes = [itemp, i32, i32p, i32, i32p]
         L.vp_preprocess_batch.argtypes = [itemp, i32, f32p, f32p, i32, ctypes.c_void_p, i64,
                                           i32p, i32p, ctypes.c_void_p, i64, ctypes.c_void_p]
         L.vp_patchify_batch.argtypes = L.vp_preprocess_batch.argtypes
@@ -226,6 +227,22 @@ def vp_batch_layout(items: Sequence):
     _check(lib().vp_batch_layout(b.arr, B, _ptr(grid, ctypes.c_int32), _ptr(cu, ctypes.c_int32),
                                  ctypes.byref(rows), ctypes.byref(ws)), "vp_batch_layout")
     return grid, cu, rows.value, ws.value
+
+
+VP_KERNEL_GENERIC, VP_KERNEL_YFIRST, VP_KERNEL_XFIRST = 0, 1, 2
+
+
+def vp_batch_kernels(items: Sequence):
+    """The launches vp_preprocess_batch makes for the batch, as int32 rows
+    (kind, slots M, column taps, y-first pixels per lane, x-first columns per
+    lane, workgroups); no kernel runs."""
+    b = _Batch(items)
+    n = ctypes.c_int32()
+    _check(lib().vp_batch_kernels(b.arr, len(b), None, 0, ctypes.byref(n)), "vp_batch_kernels")
+    rows = np.zeros((max(n.value, 1), 6), np.int32)
+    _check(lib().vp_batch_kernels(b.arr, len(b), _ptr(rows, ctypes.c_int32), n.value, ctypes.byref(n)),
+           "vp_batch_kernels")
+    return rows[:n.value]
 
 
 def _stream_handle(stream) -> int:

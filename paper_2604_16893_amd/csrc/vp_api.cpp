@@ -11,6 +11,7 @@
 #include <cstring>
 #include <algorithm>
 #include <list>
+#include <array>
 #include <map>
 #include <memory>
 #include <tuple>
@@ -474,22 +475,33 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t pa
 }
 
 // The x-first streaming kernel (patch 16) for an item, if it can take it:
-// bands of 64 output columns (the last one narrower where the width is not a
-// multiple of 64), 4 to 12 taps (the window's own count, at least 4), M
-// slots.
-// Its shape is recorded with px = kPxXFirst.
-bool xfirst_shape(const vp_item& it, const AxisFilter& fx, int32_t m, StreamShape* sh) {
+// 4 to 12 taps (the window's own count, at least 4), M slots.  With
+// `pairs`, windows of 6 to 8 taps -- x scales of about 1.3 to 2 -- whose
+// starts in each pair of columns (2i, 2i + 1) lie 0 to 2 pixels apart take
+// one column pair per lane and 128 columns per wave; else a lane takes one
+// column and a wave 64.  (A single column's window of 6 or more taps takes a
+// second load of 8 bytes or more per row, which pairs save; shorter windows
+// ran slower in pairs, at the lower occupancy of their larger register set.)
+// The last band is narrower where the width is not a multiple of the band.
+// Its shape is recorded with px = xfirst_px(0), or xfirst_px(2) for pairs.
+bool xfirst_shape(const vp_item& it, const AxisFilter& fx, int32_t m, bool pairs_ok, StreamShape* sh) {
     const int32_t kx = std::max<int32_t>(fx.taps, 4);
-    if (!vp::xfirst_shape_supported(m, kx)) return false;
-    // every load of a frame row (a window of up to 3 kx + 4 bytes past its
-    // start, up to kSlotMax + 8 rows past the last one) stays below 4 GiB
+    bool pairs = pairs_ok && vp::xfirst_shape_supported(m, kx, 2) && fx.n_out % 2 == 0;
+    for (int32_t j = 0; pairs && j + 1 < fx.n_out; j += 2) {
+        const int32_t d = fx.start[j + 1] - fx.start[j];
+        pairs = d >= 0 && d <= 2;
+    }
+    const int32_t db = pairs ? 2 : 0;
+    if (!vp::xfirst_shape_supported(m, kx, db)) return false;
+    // every load of a frame row (a window of up to 3 (kx + db) + 6 bytes past
+    // its start, up to kSlotMax + 8 rows past the last one) stays below 4 GiB
     if (int64_t(it.src_h + vp::kSlotMax + 8) * it.src_w * 3 + 3 * kx + 64 >= (int64_t(1) << 32)) return false;
-    const int32_t band = 64;
+    const int32_t band = db > 0 ? 128 : 64;
     const int32_t waves = (it.dst_w + band - 1) / band;
     if (waves > vp::kWgBandMax) return false;
     sh->m = m;
     sh->kx = kx;
-    sh->px = vp::kPxXFirst;
+    sh->px = vp::xfirst_px(db);
     sh->band = band;
     sh->bands = waves;
     return true;
@@ -728,6 +740,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         return found->second;
     };
     std::vector<StreamShape> shapes(n);
+    std::vector<const AxisFilter*> x_axes(n, nullptr);
 
     int64_t rows = 0, tiles = 0;
     for (int32_t b = 0; b < n; ++b) {
@@ -757,12 +770,10 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         StreamShape sh;
         const bool slots = slots_for(*fy, &d.sy_off, &m);
         const bool near_one = P == 16 && double(it.src_h) <= kXFirstMaxScale * double(it.dst_h);
-        if (slots && ((near_one && xfirst_shape(it, *fx, m, &sh)) || stream_shape(it, *fx, m, P, &sh))) {
-            d.route = vp::kRouteStream;
-            d.band = sh.band;
-            d.row_px = sh.px > 0 ? 64 * sh.px : it.src_w + sh.kx;
-            d.sx_off = columns_for(*fx, sh.kx, sh.band, d.row_px);
+        if (slots && ((near_one && xfirst_shape(it, *fx, m, false, &sh)) || stream_shape(it, *fx, m, P, &sh))) {
+            d.route = vp::kRouteStream;   // (band and column table below, once the shape is final)
             shapes[b] = sh;
+            x_axes[b] = fx;
         } else if (!generic_subtile(*fx, 2 * P, &d.rh, &d.cw)) {
             return fail(VP_ERR_CAPACITY, "item " + std::to_string(b) +
                                              ": horizontal filter window too long (downscale too large)");
@@ -799,19 +810,22 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     // video of 128 frames -- otherwise gets units of ten windows that
     // re-read about a tenth of their rows).
     constexpr int64_t kWaveSlots = 256 * 20;
-    int64_t wave_rows = 0;   // source rows that all workgroups stream, whole frames
     int64_t stream_frames = 0;
-    for (int32_t b = 0; b < n; ++b) {
-        const vp::DevItem& d = p->items[b];
-        if (d.route != vp::kRouteStream) continue;
-        for (int32_t tt = 0; tt < d.t; ++tt) {
-            const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
-            wave_rows += int64_t(same ? 1 : 2) * shapes[b].bands * d.H;
-            stream_frames += same ? 1 : 2;
+    auto source_row_cap = [&] {
+        int64_t wave_rows = 0;   // source rows that all workgroups stream, whole frames
+        stream_frames = 0;
+        for (int32_t b = 0; b < n; ++b) {
+            const vp::DevItem& d = p->items[b];
+            if (d.route != vp::kRouteStream) continue;
+            for (int32_t tt = 0; tt < d.t; ++tt) {
+                const bool same = p->indices[d.idx_off + 2 * tt] == p->indices[d.idx_off + 2 * tt + 1];
+                wave_rows += int64_t(same ? 1 : 2) * shapes[b].bands * d.H;
+                stream_frames += same ? 1 : 2;
+            }
         }
-    }
-    const int64_t max_src_rows = wave_rows / (kWaveSlots * 8);
-    auto workgroup_waves = [&](int64_t min_windows) {
+        return wave_rows / (kWaveSlots * 8);
+    };
+    auto workgroup_waves = [&](int64_t min_windows, int64_t max_src_rows) {
         int64_t waves = 0;
         for (int32_t b = 0; b < n; ++b) {
             const vp::DevItem& d = p->items[b];
@@ -827,7 +841,26 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         }
         return waves;
     };
-    const int64_t min_windows = workgroup_waves(15) >= 2 * kWaveSlots ? 15 : 10;
+    // Column pairs halve an x-first item's workgroups: taken only where the
+    // batch gives every wave slot four workgroups with single columns.
+    if (workgroup_waves(10, source_row_cap()) >= 4 * kWaveSlots) {
+        for (int32_t b = 0; b < n; ++b) {
+            StreamShape sh;
+            if (p->items[b].route == vp::kRouteStream && shapes[b].px < 0 &&
+                xfirst_shape(items[b], *x_axes[b], shapes[b].m, true, &sh))
+                shapes[b] = sh;
+        }
+    }
+    for (int32_t b = 0; b < n; ++b) {
+        vp::DevItem& d = p->items[b];
+        if (d.route != vp::kRouteStream) continue;
+        const StreamShape& sh = shapes[b];
+        d.band = sh.band;
+        d.row_px = sh.px > 0 ? 64 * sh.px : d.W + sh.kx;
+        d.sx_off = columns_for(*x_axes[b], sh.kx, sh.band, d.row_px);
+    }
+    const int64_t max_src_rows = source_row_cap();
+    const int64_t min_windows = workgroup_waves(15, max_src_rows) >= 2 * kWaveSlots ? 15 : 10;
     std::vector<Keyed> keyed;
     keyed.reserve(static_cast<size_t>(stream_frames));
     for (int32_t b = 0; b < n; ++b) {
@@ -1716,6 +1749,29 @@ int32_t vp_batch_layout(const vp_item* items, int32_t n_items, int32_t* grid_thw
     if (cu_seqlens) std::memcpy(cu_seqlens, p.cu.data(), sizeof(int32_t) * p.cu.size());
     if (total_rows) *total_rows = p.total_rows;
     if (workspace_bytes) *workspace_bytes = static_cast<int64_t>(p.bytes);
+    return VP_OK;
+}
+
+int32_t vp_batch_kernels(const vp_item* items, int32_t n_items, int32_t* launches,
+                         int32_t capacity, int32_t* n_launches) {
+    if (n_launches == nullptr) return fail(VP_ERR_NULL, "n_launches is NULL");
+    if (capacity < 0 || (launches == nullptr && capacity > 0))
+        return fail(VP_ERR_ARG, "launches must hold capacity rows of 6 int32");
+    std::shared_ptr<const Plan> plan;
+    const int32_t st = get_plan(PlanKind::kBatch, items, n_items, &plan);
+    if (st != VP_OK) return st;
+    const Plan& p = *plan;
+    std::vector<std::array<int32_t, 6>> rows;
+    if (p.prefix[n_items] > 0) rows.push_back({VP_KERNEL_GENERIC, 0, 0, 0, 0, p.prefix[n_items]});
+    for (const vp::StreamLaunch& L : p.launches) {
+        if (L.px < 0)
+            rows.push_back({VP_KERNEL_XFIRST, L.m, L.kx, 0, vp::xfirst_db(L.px) > 0 ? 2 : 1, L.count});
+        else
+            rows.push_back({VP_KERNEL_YFIRST, L.m, L.kx, L.px, 0, L.count});
+    }
+    for (size_t i = 0; i < rows.size() && i < size_t(capacity); ++i)
+        std::memcpy(launches + 6 * i, rows[i].data(), sizeof(int32_t) * 6);
+    *n_launches = static_cast<int32_t>(rows.size());
     return VP_OK;
 }
 

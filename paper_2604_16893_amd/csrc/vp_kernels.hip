@@ -1030,6 +1030,13 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 //     straight from the frame: the dwords holding its 3 KXE bytes (ND of
 //     them, dword aligned, four rows ahead); neighbouring lanes' windows
 //     overlap, and the overlap is served by the L1 cache, not HBM;
+//   * with DB > 0 a lane takes two neighbouring columns, j0 + 2j and
+//     j0 + 2j + 1 (a wave covers 128): it loads the pair's window, which is
+//     the first column's window extended by DB pixels, and the second column
+//     gets its KXE weights at their place in it (its window starts 0 to DB
+//     pixels after the first's) with zeros elsewhere.  A pair reads about
+//     half the bytes that two single columns read, and its tap bytes are
+//     extracted once for both columns;
 //   * the lane shifts the window to its first byte (v_alignbyte by the
 //     window's byte misalignment) and moves the bytes of taps 2m and 2m + 1
 //     of each channel (an odd count's last tap alone) into the two 16-bit
@@ -1045,15 +1052,18 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 //     lanes per 128-byte run, as in the y-first kernel.
 // Window bytes past the end of a row are the next row's (or zeros past the
 // frame, from the buffer range check); they meet only zero weights.
-template <int M, int KXE, int OUT_BF16>
+template <int M, int KXE, int DB, int OUT_BF16>
 __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     using elem_t = typename std::conditional<OUT_BF16 != 0, uint16_t, float>::type;
-    static_assert(KXE >= 4 && KXE <= 12, "tap counts from 4 to 12");
-    constexpr int NA = (3 * KXE + 3) / 4;          // dwords of the window from its first byte
-    constexpr int ND = NA + 1;                     // dwords loaded: the window at any alignment
+    static_assert(KXE >= 4 && KXE <= 12 && DB >= 0 && DB <= 2, "tap counts from 4 to 12, pair offsets to 2");
+    constexpr int CPL = DB > 0 ? 2 : 1;            // output columns per lane
+    constexpr int BW = 64 * CPL;                   // output columns per wave
+    constexpr int KW = KXE + DB;                   // window taps from the lane's window start
+    constexpr int NA = (3 * KW + 3) / 4;           // dwords of the window from its first byte
+    constexpr int ND = (3 * KW + 6) / 4;           // dwords loaded: the window at any alignment
     constexpr int S = 16 / int(sizeof(elem_t));    // output columns per 16-byte store
     extern __shared__ __align__(16) unsigned char smem[];
-    elem_t* const stage = reinterpret_cast<elem_t*>(smem);   // [3][4][64]
+    elem_t* const stage = reinterpret_cast<elem_t*>(smem);   // [3][4][BW]
 
     const int lane = static_cast<int>(threadIdx.x) & 63;
     const uint32_t wg = as_const(plan.wgs)[wg0 + static_cast<int>(blockIdx.x)];
@@ -1078,17 +1088,35 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     // Column table: window start relative to the band's first source pixel,
     // then KXE weights (zero past the window).  Lanes past the band's last
     // column take its first column's entry (valid reads) with zero weights.
+    // A pair's second column (widths are multiples of 32, so it is in the
+    // band with the first) takes its weights at its offset in the window.
     const cptr<int32_t> tables = as_const(plan.tables);
     const cptr<int32_t> sx_start = tables + it->sx_off;
     const cptr<float> sx_w = (cptr<float>)(sx_start + w);
-    const bool xlane = lane < nbw;
-    const int jx = xlane ? j0 + lane : j0;
+    const bool xlane = CPL * lane < nbw;
+    const int jx = xlane ? j0 + CPL * lane : j0;
     const int sj = sx_start[jx];
     float wx[KXE];
     {
         const cptr<float> src = sx_w + int64_t(jx) * KXE;
 #pragma unroll
         for (int k = 0; k < KXE; ++k) wx[k] = xlane ? src[k] : 0.f;
+    }
+    float wb[DB > 0 ? KW : 1];
+    if constexpr (DB > 0) {
+        const int db = sx_start[jx + 1] - sj;     // 0 .. DB
+        const cptr<float> src = sx_w + int64_t(jx + 1) * KXE;
+        float t[KXE];
+#pragma unroll
+        for (int k = 0; k < KXE; ++k) t[k] = src[k];
+#pragma unroll
+        for (int k = 0; k < KW; ++k) {
+            float v = 0.f;
+#pragma unroll
+            for (int d = 0; d <= DB; ++d)
+                if (k - d >= 0 && k - d < KXE) v = db == d ? t[k - d] : v;
+            wb[k] = xlane ? v : 0.f;
+        }
     }
     const cptr<int32_t> xs = tables + it->tx_off;
     const int x0 = xs[j0];                         // first source pixel of the band
@@ -1107,14 +1135,33 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
     // (one offset per 16-byte chunk of the window, so that no row adds them)
     constexpr int NC = (ND + 3) / 4;
-    uint32_t voff[kPrefetch][NC], sh[kPrefetch];
+#ifndef XF_LIVE_OFF
+#define XF_LIVE_OFF 1
+#endif
+    constexpr bool kLive = DB > 0 && XF_LIVE_OFF;   // pairs: offsets formed per row (fewer registers)
+    const uint32_t c0 = lead + 3u * static_cast<uint32_t>(x0 + sj);
+    uint32_t voff[kLive ? 1 : 4][NC], sh[kLive ? 1 : 4];
+    if constexpr (!kLive) {
 #pragma unroll
-    for (int k = 0; k < kPrefetch; ++k) {
-        const uint32_t c = lead + static_cast<uint32_t>(k) * row_bytes + 3u * static_cast<uint32_t>(x0 + sj);
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t c = c0 + static_cast<uint32_t>(k) * row_bytes;
 #pragma unroll
-        for (int i = 0; i < NC; ++i) voff[k][i] = (c & ~3u) + 16u * static_cast<uint32_t>(i);
-        sh[k] = c & 3u;
+            for (int i = 0; i < NC; ++i) voff[k][i] = (c & ~3u) + 16u * static_cast<uint32_t>(i);
+            sh[k] = c & 3u;
+        }
     }
+    auto phase_off = [&](int k, int i) __attribute__((always_inline)) -> uint32_t {
+        if constexpr (kLive)
+            return ((c0 + static_cast<uint32_t>(k) * row_bytes) & ~3u) + 16u * static_cast<uint32_t>(i);
+        else
+            return voff[k][i];
+    };
+    auto phase_sh = [&](int k) __attribute__((always_inline)) -> uint32_t {
+        if constexpr (kLive)
+            return (c0 + static_cast<uint32_t>(k) * row_bytes) & 3u;
+        else
+            return sh[k];
+    };
     struct Win {
         uint32_t d[ND];
     };
@@ -1129,7 +1176,7 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
         Win r;
 #pragma unroll
         for (int i = 0; i < ND; i += 4) {
-            const uint32_t vo = voff[k][i / 4];
+            const uint32_t vo = phase_off(k, i / 4);
             if (ND - i >= 4) {
                 const auto v = __builtin_amdgcn_raw_buffer_load_b128(rb, vo, 0, 0);
                 r.d[i] = v[0];
@@ -1154,13 +1201,15 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
 
     const float a0 = norm.a[0], a1 = norm.a[1], a2 = norm.a[2];
     const float z0 = norm.z[0], z1 = norm.z[1], z2 = norm.z[2];
-    float acc[M][3];
+    float acc[M][3 * CPL];   // channels of the lane's first column, then its second's
 #pragma unroll
-    for (int s = 0; s < M; ++s) {
-        acc[s][0] = z0;
-        acc[s][1] = z1;
-        acc[s][2] = z2;
-    }
+    for (int s = 0; s < M; ++s)
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) {
+            acc[s][3 * q + 0] = z0;
+            acc[s][3 * q + 1] = z1;
+            acc[s][3 * q + 2] = z2;
+        }
 
     const int y0 = ys[i0];
     const int y1 = close_row[i1 - 1] + 1;
@@ -1173,7 +1222,7 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     // store-out pieces, as in the y-first kernel (patch 16)
     constexpr int kPieces = 16 / S;
     constexpr int kPerPatch = 3 * 4 * kPieces;
-    constexpr int kStoreIter = (4 * kPerPatch + 63) / 64;
+    constexpr int kStoreIter = (BW / 16 * kPerPatch + 63) / 64;
     int st_off[kStoreIter], dst_off[kStoreIter];
     {
         const int n_seg = (nbw >> 4) * kPerPatch;
@@ -1186,7 +1235,7 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
             const int ry = (rr / kPieces) & 3;
             const int piece = rr % kPieces;
             const int qa = (j0 >> 4) + q;
-            st_off[r] = e < n_seg ? (c * 4 + ry) * 64 + q * 16 + piece * S : -1;
+            st_off[r] = e < n_seg ? (c * 4 + ry) * BW + q * 16 + piece * S : -1;
             dst_off[r] = ((qa >> 1) * 4 + (qa & 1)) * kRow + (c * 2) * 256 + ry * 16 + piece * S;
         }
     }
@@ -1218,33 +1267,37 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     // Row y (its window from the first byte: byte t of a[] is window byte t):
     // the window sums, the slots, then the output rows that close on y.
     auto process_row = [&](int y, const uint32_t (&a)[NA], const float (&wr)[M]) __attribute__((always_inline)) {
-        float tsum[3];
+        float tsum[3 * CPL];
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
-            float t = 0.f;
+            float t = 0.f, tb = 0.f;
 #pragma unroll
-            for (int m = 0; m < (KXE + 1) / 2; ++m) {
+            for (int m = 0; m < (KW + 1) / 2; ++m) {
                 // channel c of taps 2m and 2m + 1: window bytes p and p + 3
                 // (an odd count's last tap alone, its high half zero)
                 constexpr int kZero = 0x0c;   // v_perm selector of a zero byte
-                const bool pair = 2 * m + 1 < KXE;
+                const bool pair = 2 * m + 1 < KW;
                 const int p = 6 * m + c;
                 const int lo = p >> 2;
                 const int hi = lo + 1 < NA ? lo + 1 : lo;   // p + 3 stays in a[lo] when lo is the last
                 const uint32_t sel = static_cast<uint32_t>((p & 3) | (kZero << 8) |
                                                            ((pair ? p + 3 - 4 * lo : kZero) << 16) | (kZero << 24));
                 const h2 pr = __builtin_bit_cast(h2, __builtin_amdgcn_perm(a[hi], a[lo], sel));
-                t = fmaf(wx[2 * m], static_cast<float>(pr.x), t);
-                if (pair) t = fmaf(wx[2 * m + 1], static_cast<float>(pr.y), t);
+                if (2 * m < KXE) t = fmaf(wx[2 * m], static_cast<float>(pr.x), t);
+                if (2 * m + 1 < KXE) t = fmaf(wx[2 * m + 1], static_cast<float>(pr.y), t);
+                if constexpr (DB > 0) {
+                    tb = fmaf(wb[2 * m], static_cast<float>(pr.x), tb);
+                    if (pair) tb = fmaf(wb[2 * m + 1], static_cast<float>(pr.y), tb);
+                }
             }
             tsum[c] = t;
+            if constexpr (DB > 0) tsum[3 + c] = tb;
         }
 #pragma unroll
         for (int s = 0; s < M; ++s) {
             const float ws = wr[s];
-            acc[s][0] = fmaf(ws, tsum[0], acc[s][0]);
-            acc[s][1] = fmaf(ws, tsum[1], acc[s][1]);
-            acc[s][2] = fmaf(ws, tsum[2], acc[s][2]);
+#pragma unroll
+            for (int q = 0; q < 3 * CPL; ++q) acc[s][q] = fmaf(ws, tsum[q], acc[s][q]);
         }
         while (y == next_close && base < i1) {   // wave-uniform
             const bool keep = base >= i0;
@@ -1253,21 +1306,33 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
             for (int s = 0; s < M; ++s) {
                 if (slot == s) {
                     if (keep) {
-                        const float v0 = acc[s][0] * a0, v1 = acc[s][1] * a1, v2 = acc[s][2] * a2;
-                        elem_t* st = stage + yy * 64 + lane;
-                        if constexpr (OUT_BF16 != 0) {
-                            st[0] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v0));
-                            st[256] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v1));
-                            st[512] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v2));
-                        } else {
-                            st[0] = v0;
-                            st[256] = v1;
-                            st[512] = v2;
+                        elem_t* st = stage + yy * BW + CPL * lane;
+#pragma unroll
+                        for (int c = 0; c < 3; ++c) {
+                            const float sc = c == 0 ? a0 : (c == 1 ? a1 : a2);
+                            const float v = acc[s][c] * sc;
+                            if constexpr (DB > 0) {   // the pair's two columns as one store
+                                const float vb = acc[s][3 + c] * sc;
+                                if constexpr (OUT_BF16 != 0)
+                                    *reinterpret_cast<uint32_t*>(st + c * 4 * BW) =
+                                        uint32_t(__builtin_bit_cast(uint16_t, static_cast<__bf16>(v))) |
+                                        (uint32_t(__builtin_bit_cast(uint16_t, static_cast<__bf16>(vb))) << 16);
+                                else
+                                    *reinterpret_cast<float2*>(st + c * 4 * BW) = make_float2(v, vb);
+                            } else {
+                                if constexpr (OUT_BF16 != 0)
+                                    st[c * 4 * BW] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
+                                else
+                                    st[c * 4 * BW] = v;
+                            }
                         }
                     }
-                    acc[s][0] = z0;
-                    acc[s][1] = z1;
-                    acc[s][2] = z2;
+#pragma unroll
+                    for (int q = 0; q < CPL; ++q) {
+                        acc[s][3 * q + 0] = z0;
+                        acc[s][3 * q + 1] = z1;
+                        acc[s][3 * q + 2] = z2;
+                    }
                 }
             }
             if (keep && yy == 3) store_out(base);
@@ -1278,49 +1343,61 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
         }
     };
 
+    // Rows in flight per lane: four, or two for column pairs, whose windows
+    // are twice as wide (the registers that two more would take cost more
+    // occupancy than they hide latency).  Rows go in blocks of four; row k
+    // of a block is in buffer k % PF.
+#ifndef XF_PAIR_PF
+#define XF_PAIR_PF 2
+#endif
+    constexpr int PF = DB > 0 ? XF_PAIR_PF : kPrefetch;
+    static_assert(PF == 2 || PF == 4, "rows in flight divide the block of four");
     const int yb0 = y0 & ~3;
-    Win pf[kPrefetch];
+    Win pf[PF];
 #pragma unroll
-    for (int k = 0; k < kPrefetch; ++k) {
+    for (int k = 0; k < PF; ++k) {
         pf[k] = load_row(yb0, k);
         __builtin_amdgcn_sched_barrier(0);
     }
-    for (int yb = yb0; yb < y1; yb += kPrefetch) {
+    for (int yb = yb0; yb < y1; yb += 4) {
         const cptr<float> wblk = slot_w + yb * kSlotWords;
-        float wk[kPrefetch][M];
+        float wk[4][M];
 #pragma unroll
-        for (int k = 0; k < kPrefetch; ++k)
+        for (int k = 0; k < 4; ++k)
 #pragma unroll
             for (int s = 0; s < M; ++s) wk[k][s] = wblk[k * kSlotWords + s];
 #pragma unroll
-        for (int k = 0; k < kPrefetch; ++k) {
+        for (int k = 0; k < 4; ++k) {
             const int y = yb + k;
-            // align first: the next load then reuses pf[k]'s registers
+            Win& buf = pf[k % PF];
+            // align first: the next load then reuses the buffer's registers
             // instead of copying them while it is in flight
             uint32_t a[NA];
+            const uint32_t shk = phase_sh(k);
 #pragma unroll
-            for (int q = 0; q < NA; ++q) a[q] = __builtin_amdgcn_alignbyte(pf[k].d[q + 1], pf[k].d[q], sh[k]);
+            for (int q = 0; q < NA; ++q)   // (a last dword past ND brings only bytes past the window)
+                a[q] = __builtin_amdgcn_alignbyte(buf.d[q + 1 < ND ? q + 1 : q], buf.d[q], shk);
 #pragma unroll
             for (int q = 0; q < NA; ++q) asm volatile("" : : "v"(a[q]));
             // (issued at raised wave priority, so that the load leaves ahead
             // of other waves' arithmetic and the memory stream stays full)
             __builtin_amdgcn_s_setprio(2);
-            pf[k] = load_row(yb + kPrefetch, k);
+            buf = load_row(yb + (k + PF) / 4 * 4, (k + PF) % 4);
             __builtin_amdgcn_s_setprio(0);
             if (y >= y0 && y < y1) process_row(y, a, wk[k]);
         }
     }
 }
 
-template <int M, int KXE>
+template <int M, int KXE, int DB>
 int launch_xfirst_shape(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                         const Norm& norm, hipStream_t stream) {
-    const int lds = xfirst_wave_bytes(out_dtype == 1 ? 2 : 4);
+    const int lds = xfirst_wave_bytes(out_dtype == 1 ? 2 : 4, DB > 0 ? 2 : 1);
     dim3 grid(static_cast<unsigned>(L.count)), block(64);
     if (out_dtype == 1)
-        hipLaunchKernelGGL((xfirst_kernel<M, KXE, 1>), grid, block, lds, stream, plan, L.first, out, norm);
+        hipLaunchKernelGGL((xfirst_kernel<M, KXE, DB, 1>), grid, block, lds, stream, plan, L.first, out, norm);
     else
-        hipLaunchKernelGGL((xfirst_kernel<M, KXE, 0>), grid, block, lds, stream, plan, L.first, out, norm);
+        hipLaunchKernelGGL((xfirst_kernel<M, KXE, DB, 0>), grid, block, lds, stream, plan, L.first, out, norm);
     return static_cast<int>(hipGetLastError());
 }
 
@@ -1785,12 +1862,12 @@ int stream_case(const PlanView& plan, const StreamLaunch& L, void* out, int out_
     return -1;
 }
 
-template <int MM, int KK, int ID>
+template <int MM, int KK, int DB, int ID>
 int xfirst_case(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                 const Norm& norm, hipStream_t stream) {
     if constexpr (ID % VP_PARTS == VP_PART) {
-        if (L.m == MM && L.kx == KK && L.px == kPxXFirst)
-            return launch_xfirst_shape<MM, KK>(plan, L, out, out_dtype, norm, stream);
+        if (L.m == MM && L.kx == KK && L.px == xfirst_px(DB))
+            return launch_xfirst_shape<MM, KK, DB>(plan, L, out, out_dtype, norm, stream);
     }
     return -1;
 }
@@ -1833,13 +1910,16 @@ int VP_CAT(launch_stream_part, VP_PART)(const PlanView& plan, const StreamLaunch
 #undef VP_STREAM_LONG
 #undef VP_STREAM_KX
 #undef VP_STREAM_CASE
-#define VP_XF_CASE(MM, KK)                                                                    \
-    if (const int r = xfirst_case<MM, KK, __COUNTER__>(plan, L, out, out_dtype, norm, stream); \
-        r != -1)                                                                             \
+#define VP_XF_CASE(MM, KK, DB)                                                                    \
+    if (const int r = xfirst_case<MM, KK, DB, __COUNTER__>(plan, L, out, out_dtype, norm, stream); \
+        r != -1)                                                                                 \
         return r;
-#define VP_XF_KX(MM) VP_XF_CASE(MM, 4) VP_XF_CASE(MM, 5) VP_XF_CASE(MM, 6) VP_XF_CASE(MM, 7) VP_XF_CASE(MM, 8) \
-    VP_XF_CASE(MM, 9) VP_XF_CASE(MM, 10) VP_XF_CASE(MM, 11) VP_XF_CASE(MM, 12)
+#define VP_XF_KX(MM) VP_XF_CASE(MM, 4, 0) VP_XF_CASE(MM, 5, 0) VP_XF_CASE(MM, 6, 0) VP_XF_CASE(MM, 7, 0) \
+    VP_XF_CASE(MM, 8, 0) VP_XF_CASE(MM, 9, 0) VP_XF_CASE(MM, 10, 0) VP_XF_CASE(MM, 11, 0) VP_XF_CASE(MM, 12, 0)
+#define VP_XF_PAIR(MM, DB) VP_XF_CASE(MM, 6, DB) VP_XF_CASE(MM, 7, DB) VP_XF_CASE(MM, 8, DB)
     VP_XF_KX(4) VP_XF_KX(5) VP_XF_KX(6) VP_XF_KX(7) VP_XF_KX(8)
+    VP_XF_PAIR(4, 2) VP_XF_PAIR(5, 2) VP_XF_PAIR(6, 2) VP_XF_PAIR(7, 2) VP_XF_PAIR(8, 2)
+#undef VP_XF_PAIR
 #undef VP_XF_KX
 #undef VP_XF_CASE
     return -1;
@@ -2016,14 +2096,14 @@ bool stream_shape_supported(int m, int kx, int px) {
     return px == 2 || (px == 3 && m <= 5 && kx <= 24);
 }
 
-bool xfirst_shape_supported(int m, int kx) {
-    return m >= 4 && m <= kSlotWords && kx >= 4 && kx <= 12;
+bool xfirst_shape_supported(int m, int kx, int db) {
+    return m >= 4 && m <= kSlotWords && kx >= 4 && (db == 0 ? kx <= 12 : db == 2 && kx >= 6 && kx <= 8);
 }
 
 int launch_stream(const PlanView& plan, const StreamLaunch& L, void* out, int out_dtype,
                   const Norm& norm, hipStream_t stream) {
     if (L.count <= 0) return 0;
-    if (L.px == kPxXFirst ? (!xfirst_shape_supported(L.m, L.kx) || L.patch != 16)
+    if (L.px < 0 ? (L.px < xfirst_px(2) || !xfirst_shape_supported(L.m, L.kx, xfirst_db(L.px)) || L.patch != 16)
                  : (!stream_shape_supported(L.m, L.kx, L.px) ||
                     stream_wave_bytes(L.px, L.kx, 4, L.patch) > kStreamLdsBudget))
         return static_cast<int>(hipErrorInvalidConfiguration);

@@ -65,9 +65,10 @@ constexpr int stream_wave_bytes(int px, int kx, int elem_bytes, int patch = 16) 
                                  : 4 * 64 * px * 16 + 8 * 6 * patch * patch * elem_bytes;
 }
 
-// LDS of one x-first streaming workgroup (one wave): the stage of four
-// output rows (its lanes load their source windows from memory).
-constexpr int xfirst_wave_bytes(int elem_bytes) { return 3 * 4 * 64 * elem_bytes; }
+// LDS of one x-first streaming workgroup (one wave of cpl columns per lane):
+// the stage of four output rows (its lanes load their source windows from
+// memory).
+constexpr int xfirst_wave_bytes(int elem_bytes, int cpl) { return 3 * 4 * 64 * cpl * elem_bytes; }
 
 // uint8 streaming writer: pixels per lane (a band's source span is at most
 // 64 * kRsPx pixels), and the LDS of one workgroup (one wave): its source
@@ -154,11 +155,14 @@ constexpr int kWgBandMax = (1 << (32 - kWgBandShift)) - 2;   // keeps entries be
 constexpr uint32_t kNoWork = 0xffffffffu;
 
 // One launch of the streaming kernel: workgroups wgs[first, first + count),
-// all with the same template shape.  px == kPxXFirst marks the x-first kernel.
-constexpr int32_t kPxXFirst = -1;
+// all with the same template shape.  px < 0 marks the x-first kernel:
+// xfirst_px(0) one column per lane, xfirst_px(2) column pairs whose second
+// window starts at most 2 pixels after the first's.
+constexpr int32_t xfirst_px(int db) { return -1 - db; }
+constexpr int xfirst_db(int32_t px) { return -1 - px; }
 struct StreamLaunch {
     int32_t first, count;
-    int32_t m, kx, px;       // accumulator slots, column taps, pixels per lane (or kPxXFirst)
+    int32_t m, kx, px;       // accumulator slots, column taps, pixels per lane (or xfirst_px)
     int32_t patch;           // patch edge of the batch (16 or 14)
     int64_t cost;            // host only: estimated work (source pixels read)
 };
@@ -191,7 +195,7 @@ int launch_positions(const PlanView& plan, int32_t* vit, int32_t* llm, int64_t r
                      hipStream_t stream);
 // Whether a (m, kx, px) shape has a compiled streaming kernel.
 bool stream_shape_supported(int m, int kx, int px);
-// Whether an (m, kx) shape has a compiled x-first kernel.
-bool xfirst_shape_supported(int m, int kx);
+// Whether an (m, kx, pair offset) shape has a compiled x-first kernel.
+bool xfirst_shape_supported(int m, int kx, int db);
 
 }  // namespace vp

@@ -199,6 +199,53 @@ def test_small_cases_full(name, specs, dtype):
         assert_close(host_rows(out, cu[k], cu[k + 1], dtype), ref, dtype, f"{name} item {k}")
 
 
+# Column pairs on the x-first kernel (windows of 6 to 8 taps) are taken only
+# in batches that give every wave slot four workgroups with single columns,
+# so each case below is padded with copies of its first item (the same
+# device frames) until the plan takes them; the distinct items are compared
+# with the oracle in full, every copy with the first item's rows.
+PAIRS = [
+    # (name, [(n_src, H, W, indices, h, w)], dtype, x taps of the pair launches)
+    ("pairs_480p_ragged_band", [(2, 480, 854, [1, 0], 320, 576)], "bf16", {6}),   # last band 64 of 128
+    ("pairs_taps8_odd_sizes", [(2, 121, 611, [0, 1], 96, 320)], "f32", {8}),
+    ("pairs_upscale_eight_slots", [(2, 48, 400, [0, 1], 96, 256)], "f32", {7}),
+    # one band of 32 columns (16 lanes), windows past the row and the frame
+    ("pairs_narrow_source", [(3, 40, 45, [2, 0, 1], 32, 32)], "bf16", {6}),
+    # two pair shapes and a single-column item (5 taps) in one batch
+    ("pairs_mixed", [(2, 150, 700, [1, 0], 96, 384), (2, 100, 500, [0, 1], 64, 288),
+                     (2, 360, 640, [0, 1], 320, 576)], "bf16", {7, 8}),
+]
+
+
+@pytest.mark.parametrize("name,specs,dtype,pair_taps", PAIRS, ids=[s[0] for s in PAIRS])
+def test_xfirst_column_pairs(name, specs, dtype, pair_taps):
+    mean, std = (0.481, 0.458, 0.408), (0.269, 0.261, 0.276)
+    items, host = [], []
+    for k, (n_src, H, W, idx, h, w) in enumerate(specs):
+        it = _rand_video(300 + k, n_src, H, W)
+        items.append((workloads.frames_torch(it, DEV), np.asarray(idx, np.int32), h, w))
+        host.append(workloads.frames_np(it))
+    copies = 1
+    while True:
+        batch = items + [items[0]] * copies
+        launches = vp.vp_batch_kernels([vp.Item(f, idx, h, w) for f, idx, h, w in batch])
+        paired = {int(r[2]) for r in launches if r[0] == vp.VP_KERNEL_XFIRST and r[4] == 2}
+        if paired:
+            break
+        copies *= 2
+        assert copies <= 16384, "the plan never took column pairs"
+    assert paired == pair_taps, launches.tolist()
+    log(f"case {name}: {len(specs)} items + {copies} copies, launches {launches.tolist()} {dtype}")
+    out, grid, cu = run_gpu(batch, mean, std, dtype)
+    assert all_written(out)
+    for k, (f, idx, h, w) in enumerate(items):
+        ref = oracle.preprocess_item(host[k], idx, h, w, mean, std)
+        assert_close(host_rows(out, cu[k], cu[k + 1], dtype), ref, dtype, f"{name} item {k}")
+    first = out[cu[0]:cu[1]]
+    rest = out[cu[len(items)]:].view(copies, first.shape[0], first.shape[1])
+    assert torch.equal(rest, first.unsqueeze(0).expand_as(rest)), "a copy differs from its original"
+
+
 def test_constant_frames_exact():
     f = torch.full((2, 77, 131, 3), 255, dtype=torch.uint8, device=DEV)
     out, _, _ = run_gpu([(f, np.array([0, 1], np.int32), 64, 96)], (0.5,) * 3, (0.5,) * 3, "bf16")

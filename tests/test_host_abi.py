@@ -379,3 +379,37 @@ def test_patch14_layout_and_checks():
     assert status([vp.Item((0x10000, 2, 64, 64), [0], 64, 64),
                    vp.Item((0x10000, 2, 64, 64), [0], 56, 56, patch=14)]) == vp.VP_ERR_ARG
     assert b"share one patch size" in vp.lib().vp_last_error_message()
+
+
+def _workload_items(wl):
+    """Items of a workload for the host-only entry points (frames are not read)."""
+    out = []
+    for it in wl.items:
+        h, w = it.dims if it.dims is not None else vp.vp_smart_resize_dims(
+            it.H, it.W, 2 * it.patch, it.min_pixels, it.max_pixels)
+        s = it.sample
+        idx = vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_UNIFORM, s["n"]) if s["mode"] == "uniform" else \
+            vp.vp_sample_indices(it.n_src, vp.VP_SAMPLE_FPS, 0, s["video_fps"], s["fps"],
+                                 s["min_frames"], s["max_frames"])
+        out.append(vp.Item((1 << 20, it.n_src, it.H, it.W), idx, h, w, it.patch))
+    return out
+
+
+def test_batch_kernels_routes():
+    """The launch description: x-first with single columns for the small
+    480p batch, column pairs for the ragged batch's 6-tap (480p) videos only,
+    the y-first kernel for strong downscales, and workgroup totals that add
+    up to the plan's."""
+    k1 = vp.vp_batch_kernels(_workload_items(workloads.config(1)))
+    assert [tuple(r[:5]) for r in k1] == [(vp.VP_KERNEL_XFIRST, 5, 6, 0, 1)]
+    k3 = vp.vp_batch_kernels(_workload_items(workloads.config(3)))
+    xf = [r for r in k3 if r[0] == vp.VP_KERNEL_XFIRST]
+    assert {int(r[2]) for r in xf if r[4] == 2} == {6}
+    assert all(r[4] == 1 for r in xf if r[2] != 6)
+    assert any(r[0] == vp.VP_KERNEL_YFIRST and r[2] == 9 for r in k3)
+    k4 = vp.vp_batch_kernels(_workload_items(workloads.config(4)))
+    assert [tuple(r) for r in k4] == [(vp.VP_KERNEL_YFIRST, 4, 12, 3, 0, 64 * 128 * 2 * 7)]
+    n = ctypes.c_int32()
+    assert vp.lib().vp_batch_kernels(None, 1, None, 0, None) == vp.VP_ERR_NULL
+    assert vp.lib().vp_batch_kernels(None, 1, None, 1, ctypes.byref(n)) == vp.VP_ERR_ARG
+    assert vp.lib().vp_batch_kernels(None, 1, None, 0, ctypes.byref(n)) == vp.VP_ERR_NULL   # items
