@@ -3,8 +3,9 @@
 //
 // Drives every host path of the library's C ABI -- smart_resize, index
 // sampling, the float and fixed-point filter tables, the batch planner of
-// every entry point (through vp_batch_layout, vp_resize_layout and the host
-// part of vp_position_ids), the plan cache, and the argument checks that
+// every entry point (through vp_batch_layout, vp_batch_kernels,
+// vp_resize_layout and the host part of vp_position_ids), the plan cache,
+// column pairs of the x-first kernel in a large batch, and the checks that
 // return before any HIP call -- and every function of the oracle, over
 // seeded random shapes, degenerate sizes and the workloads' own batches.
 // A sanitizer report aborts the run; the exit status is 0 only if every
@@ -129,6 +130,13 @@ void library_host_paths() {
         const int32_t st = vp_batch_layout(b.items.data(), n, grid.data(), cu.data(), &rows, &ws);
         count(st);
         count(vp_batch_layout(b.items.data(), n, nullptr, nullptr, nullptr, nullptr));   // a cache hit
+        {
+            int32_t nl = 0;
+            std::vector<int32_t> launches(6 * 2);
+            count(vp_batch_kernels(b.items.data(), n, launches.data(), 2, &nl));   // maybe fewer rows than launches
+            launches.assign(size_t(6) * (nl > 0 ? nl : 1), 0);
+            count(vp_batch_kernels(b.items.data(), n, launches.data(), nl, &nl));
+        }
         std::vector<int64_t> off(n + 1);
         count(vp_resize_layout(b.items.data(), n, off.data(), &ws));
         int64_t slices = 0;
@@ -168,12 +176,26 @@ void library_host_paths() {
         for (auto& it : items) it.patch = 14, it.dst_h = 252;
         count(vp_batch_layout(items.data(), 64, grid.data(), cu.data(), &rows, &ws));
     }
+    // a batch large enough for column pairs: 400 copies of a 480p pair -> 320x576
+    {
+        std::vector<int32_t> idx = {1, 0};
+        std::vector<vp_item> items(400, vp_item{fake_frames(3), idx.data(), 2, 480, 854, 2, 320, 576, 16});
+        int32_t nl = 0;
+        std::vector<int32_t> launches(6 * 8);
+        count(vp_batch_kernels(items.data(), 400, launches.data(), 8, &nl));
+        int64_t rows = 0, ws = 0;
+        count(vp_batch_layout(items.data(), 400, nullptr, nullptr, &rows, &ws));
+        count(vp_batch_kernels(items.data(), 400, nullptr, 0, &nl));
+    }
     // NULLs and degenerate batches
     count(vp_batch_layout(nullptr, 1, nullptr, nullptr, nullptr, nullptr));
     int32_t one = 0;
     vp_item single{fake_frames(0), &one, 1, 1, 1, 1, 32, 32, 16};
     count(vp_batch_layout(&single, 1, nullptr, nullptr, nullptr, nullptr));
     count(vp_batch_layout(&single, 0, nullptr, nullptr, nullptr, nullptr));
+    int32_t nl = 0;
+    count(vp_batch_kernels(&single, 1, nullptr, -1, &nl));
+    count(vp_batch_kernels(&single, 1, nullptr, 0, nullptr));
     single.indices = nullptr;
     count(vp_batch_layout(&single, 1, nullptr, nullptr, nullptr, nullptr));
     for (int s = -1; s < 12; ++s) (void)vp_status_string(s);
