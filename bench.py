@@ -351,7 +351,7 @@ def main():
     ap.add_argument("--no-per-config", action="store_true",
                     help="skip the other workloads' figures")
     ap.add_argument("--config-steps", type=int, default=30,
-                    help="timed calls per other workload (after 20 warm-up calls)")
+                    help="timed calls per other workload (after at least 20 warm-up calls and 0.5 s)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run plain 1 GiB device-to-device copies (twice) before the steps, "
                          "to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -461,8 +461,15 @@ def main():
             r = Run(vp, workloads, torch, wk, dev)
             gc.collect()
             gc.disable()
-            for _ in range(20):
+            # at least 20 calls and half a second of them: the oracle's checks
+            # before leave the GPU idle for seconds, and it runs slowly for the
+            # first tens of milliseconds after that
+            t_end, n_warm = time.perf_counter() + 0.5, 0
+            while n_warm < 20 or time.perf_counter() < t_end:
                 r.step(stream)
+                n_warm += 1
+                if n_warm % 10 == 0:
+                    torch.cuda.synchronize()
             w_s, kms, cms, _, _ = r.timed(stream, args.config_steps)
             gc.enable()
             mk = sum(kms) / len(kms)
