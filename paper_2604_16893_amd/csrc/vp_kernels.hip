@@ -1135,10 +1135,9 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     const uint32_t row_bytes = static_cast<uint32_t>(it->W) * 3u;
     // (one offset per 16-byte chunk of the window, so that no row adds them)
     constexpr int NC = (ND + 3) / 4;
-#ifndef XF_LIVE_OFF
-#define XF_LIVE_OFF 1
-#endif
-    constexpr bool kLive = DB > 0 && XF_LIVE_OFF;   // pairs: offsets formed per row (fewer registers)
+    // (column pairs form each row's offsets from c0 as they go; single
+    // columns keep the four row phases' offsets)
+    constexpr bool kLive = DB > 0;
     const uint32_t c0 = lead + 3u * static_cast<uint32_t>(x0 + sj);
     uint32_t voff[kLive ? 1 : 4][NC], sh[kLive ? 1 : 4];
     if constexpr (!kLive) {
@@ -1347,10 +1346,7 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     // are twice as wide (the registers that two more would take cost more
     // occupancy than they hide latency).  Rows go in blocks of four; row k
     // of a block is in buffer k % PF.
-#ifndef XF_PAIR_PF
-#define XF_PAIR_PF 2
-#endif
-    constexpr int PF = DB > 0 ? XF_PAIR_PF : kPrefetch;
+    constexpr int PF = DB > 0 ? 2 : kPrefetch;
     static_assert(PF == 2 || PF == 4, "rows in flight divide the block of four");
     const int yb0 = y0 & ~3;
     Win pf[PF];
