@@ -180,6 +180,10 @@ SMALL = [
     ("xfirst_width5_source", [(3, 30, 5, [2, 0, 1], 32, 32)], "bf16"),
     ("xfirst_one_band_plus", [(2, 70, 67, [1, 0], 64, 64)], "f32"),
     ("xfirst_eight_slots_odd_taps", [(2, 48, 150, [0, 1], 96, 96)], "f32"),
+    # targets taller than 2^15 rows (a unit's output rows beyond 16 bits):
+    # one near 1 (x-first), one at 2x (y-first)
+    ("tall_target_xfirst", [(2, 33000, 40, [1, 0], 32800, 32)], "bf16"),
+    ("tall_target_yfirst", [(2, 66000, 48, [0, 1], 32800, 32)], "bf16"),
 ]
 
 

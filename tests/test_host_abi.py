@@ -413,3 +413,17 @@ def test_batch_kernels_routes():
     assert vp.lib().vp_batch_kernels(None, 1, None, 0, None) == vp.VP_ERR_NULL
     assert vp.lib().vp_batch_kernels(None, 1, None, 1, ctypes.byref(n)) == vp.VP_ERR_ARG
     assert vp.lib().vp_batch_kernels(None, 1, None, 0, ctypes.byref(n)) == vp.VP_ERR_NULL   # items
+
+
+def test_tall_targets_take_the_streaming_kernels():
+    """Targets of 2^15 rows and more are planned like any other: the layout
+    counts their rows, and they take the streaming kernels (their GPU parity
+    is in tests/test_gpu_parity.py)."""
+    for H, W, h, w, kind in ((33000, 40, 32800, 32, vp.VP_KERNEL_XFIRST),
+                             (66000, 48, 32800, 32, vp.VP_KERNEL_YFIRST),
+                             (131400, 48, 65600, 32, vp.VP_KERNEL_YFIRST)):
+        items = [vp.Item((0x10000, 2, H, W), [0, 1], h, w)]
+        grid, cu, rows, ws = vp.vp_batch_layout(items)
+        assert grid.tolist() == [[1, h // 16, w // 16]] and rows == h // 16 * (w // 16)
+        k = vp.vp_batch_kernels(items)
+        assert [int(r[0]) for r in k] == [kind], k.tolist()
