@@ -523,6 +523,16 @@ constexpr int kPrefetch = 4;           // source rows in flight per lane
 using f3 = float __attribute__((ext_vector_type(3)));
 using h2 = _Float16 __attribute__((ext_vector_type(2)));
 
+// range - o, or 0 where o > range, for wave-uniform operands, on the
+// scalar unit (written out: the compiler forms this saturating difference
+// with a vector instruction and a v_readfirstlane, three vector issues per
+// source row of the streaming kernels).
+__device__ __forceinline__ uint32_t uniform_sat_sub(uint32_t range, uint32_t o) {
+    uint32_t r;
+    asm("s_sub_u32 %0, %1, %2\n\ts_cselect_b32 %0, 0, %0" : "=s"(r) : "s"(range), "s"(o) : "scc");
+    return r;
+}
+
 // Orders this wave's LDS accesses before and after it.  LDS operations of
 // one wave execute in issue order, so within a wave keeping the compiler from
 // moving them across this point is all the synchronisation needed.
@@ -736,7 +746,7 @@ void stream_kernel(PlanView plan, int wg0, void* out, Norm norm) {
     auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> load_t {
         // (the block is wave-uniform; say so, or the descriptor would be built per lane)
         const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
-        const uint32_t n = __builtin_amdgcn_readfirstlane(range > o ? range - o : 0u);
+        const uint32_t n = uniform_sat_sub(range, o);
         const uintptr_t bp = fa - lead + o;
         const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
         const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
@@ -1166,7 +1176,7 @@ __global__ __launch_bounds__(64) void xfirst_kernel(PlanView plan, int wg0, void
     };
     auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> Win {
         const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
-        const uint32_t n = __builtin_amdgcn_readfirstlane(range > o ? range - o : 0u);
+        const uint32_t n = uniform_sat_sub(range, o);
         const uintptr_t bp = fa - lead + o;
         const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
         const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
@@ -1493,7 +1503,7 @@ __global__ __launch_bounds__(64) void resize_stream_kernel(PlanView plan, int wg
     }
     auto load_row = [&](int yb, int k) __attribute__((always_inline)) -> uint4 {
         const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(yb)) * row_bytes;
-        const uint32_t n = __builtin_amdgcn_readfirstlane(range > o ? range - o : 0u);
+        const uint32_t n = uniform_sat_sub(range, o);
         const uintptr_t bp = fa - lead + o;
         const uint32_t b_lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp));
         const uint32_t b_hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bp >> 32));
