@@ -1038,8 +1038,9 @@ int launch_stream_shape(const PlanView& plan, const StreamLaunch& L, void* out, 
 // the kernel.  This one resamples x first and keeps LDS for the stage only:
 //   * lane j (output column j0 + j) loads its own window of each source row
 //     straight from the frame: the dwords holding its 3 KXE bytes (ND of
-//     them, dword aligned, four rows ahead); neighbouring lanes' windows
-//     overlap, and the overlap is served by the L1 cache, not HBM;
+//     them, dword aligned, four rows ahead, or two for column pairs);
+//     neighbouring lanes' windows overlap, and the overlap is served by the
+//     L1 cache, not HBM;
 //   * with DB > 0 a lane takes two neighbouring columns, j0 + 2j and
 //     j0 + 2j + 1 (a wave covers 128): it loads the pair's window, which is
 //     the first column's window extended by DB pixels, and the second column
