@@ -203,6 +203,19 @@ def test_small_cases_full(name, specs, dtype):
         assert_close(host_rows(out, cu[k], cu[k + 1], dtype), ref, dtype, f"{name} item {k}")
 
 
+def _pairs_batch(items):
+    """items padded with copies of the first until the plan takes column
+    pairs; (batch, copies, launches)."""
+    copies = 1
+    while True:
+        batch = items + [items[0]] * copies
+        launches = vp.vp_batch_kernels([vp.Item(f, idx, h, w) for f, idx, h, w in batch])
+        if any(r[0] == vp.VP_KERNEL_XFIRST and r[4] == 2 for r in launches):
+            return batch, copies, launches
+        copies *= 2
+        assert copies <= 16384, "the plan never took column pairs"
+
+
 # Column pairs on the x-first kernel (windows of 6 to 8 taps) are taken only
 # in batches that give every wave slot four workgroups with single columns,
 # so each case below is padded with copies of its first item (the same
@@ -229,15 +242,8 @@ def test_xfirst_column_pairs(name, specs, dtype, pair_taps):
         it = _rand_video(300 + k, n_src, H, W)
         items.append((workloads.frames_torch(it, DEV), np.asarray(idx, np.int32), h, w))
         host.append(workloads.frames_np(it))
-    copies = 1
-    while True:
-        batch = items + [items[0]] * copies
-        launches = vp.vp_batch_kernels([vp.Item(f, idx, h, w) for f, idx, h, w in batch])
-        paired = {int(r[2]) for r in launches if r[0] == vp.VP_KERNEL_XFIRST and r[4] == 2}
-        if paired:
-            break
-        copies *= 2
-        assert copies <= 16384, "the plan never took column pairs"
+    batch, copies, launches = _pairs_batch(items)
+    paired = {int(r[2]) for r in launches if r[0] == vp.VP_KERNEL_XFIRST and r[4] == 2}
     assert paired == pair_taps, launches.tolist()
     log(f"case {name}: {len(specs)} items + {copies} copies, launches {launches.tolist()} {dtype}")
     out, grid, cu = run_gpu(batch, mean, std, dtype)
@@ -247,6 +253,37 @@ def test_xfirst_column_pairs(name, specs, dtype, pair_taps):
         assert_close(host_rows(out, cu[k], cu[k + 1], dtype), ref, dtype, f"{name} item {k}")
     first = out[cu[0]:cu[1]]
     rest = out[cu[len(items)]:].view(copies, first.shape[0], first.shape[1])
+    assert torch.equal(rest, first.unsqueeze(0).expand_as(rest)), "a copy differs from its original"
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_xfirst_column_pairs_random(case):
+    """Seeded random shapes for column pairs: vertical scales 0.5 to 1.6,
+    horizontal 1.3 to 2 (6- to 8-tap windows), odd source sizes, unsorted
+    indices with repeats and odd counts, fp32 and bf16."""
+    rng = np.random.default_rng(7100 + case)
+    dtype = "bf16" if case % 2 else "f32"
+    mean, std = (0.481, 0.458, 0.408), (0.269, 0.261, 0.276)
+    h = 32 * int(rng.integers(1, 8))
+    w = 32 * int(rng.integers(1, 12))
+    H = max(1, int(round(h * rng.uniform(0.5, 1.6)))) | 1
+    W = int(round(w * rng.uniform(1.32, 1.95))) | 1
+    n_src = int(rng.integers(1, 6))
+    idx = rng.integers(0, n_src, size=int(rng.integers(1, 5))).astype(np.int32)
+    it = _rand_video(500 + case, n_src, H, W)
+    item = (workloads.frames_torch(it, DEV), idx, h, w)
+    kx = vp.vp_filter_taps(W, w)
+    if not 6 <= kx <= 8 or H > 1.6 * h:
+        pytest.skip(f"drawn shape {H}x{W} -> {h}x{w} ({kx} taps) is not a column-pair shape")
+    batch, copies, launches = _pairs_batch([item])
+    log(f"pairs random {case}: {n_src}x{H}x{W} idx {idx.tolist()} -> {h}x{w} {dtype}, "
+        f"{copies} copies, launches {launches.tolist()}")
+    out, grid, cu = run_gpu(batch, mean, std, dtype)
+    assert all_written(out)
+    ref = oracle.preprocess_item(workloads.frames_np(it), idx, h, w, mean, std)
+    assert_close(host_rows(out, cu[0], cu[1], dtype), ref, dtype, f"pairs random {case}")
+    first = out[cu[0]:cu[1]]
+    rest = out[cu[1]:].view(copies, first.shape[0], first.shape[1])
     assert torch.equal(rest, first.unsqueeze(0).expand_as(rest)), "a copy differs from its original"
 
 
