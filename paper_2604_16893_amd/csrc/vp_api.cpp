@@ -458,8 +458,12 @@ bool stream_shape(const vp_item& it, const AxisFilter& fx, int32_t m, int32_t pa
             if (!vp::stream_shape_supported(mm, kx, px)) continue;
             if (span > 64 * px || kx > 64 * px) continue;
             if (vp::stream_wave_bytes(px, kx, 4, patch) > vp::kStreamLdsBudget) continue;
-            const int64_t cost = int64_t(waves) * (int64_t(it.src_h) * px * 3 * (mm + 1) +
-                                                    int64_t(it.dst_h) * (3 * kx + 12));
+            // vector instructions per wave: per source row 3 px M
+            // multiply-adds, about 2 px unpacks and 4 more; per output row
+            // the x pass (3 kx FMAs, kx LDS reads), the slot's 3 px clears
+            // and about 12 more
+            const int64_t cost = int64_t(waves) * (int64_t(it.src_h) * (3 * px * mm + 2 * px + 4) +
+                                                    int64_t(it.dst_h) * (4 * kx + 3 * px + 12));
             if (best < 0 || cost < best) {
                 best = cost;
                 sh->m = mm;
