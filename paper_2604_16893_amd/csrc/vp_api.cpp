@@ -850,7 +850,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     if (workgroup_waves(10, source_row_cap()) >= 4 * kWaveSlots) {
         for (int32_t b = 0; b < n; ++b) {
             StreamShape sh;
-            if (p->items[b].route == vp::kRouteStream && shapes[b].px < 0 &&
+            if (p->items[b].route == vp::kRouteStream && shapes[b].px == vp::xfirst_px(0) &&
                 xfirst_shape(items[b], *x_axes[b], shapes[b].m, true, &sh))
                 shapes[b] = sh;
         }
