@@ -427,3 +427,17 @@ def test_tall_targets_take_the_streaming_kernels():
         assert grid.tolist() == [[1, h // 16, w // 16]] and rows == h // 16 * (w // 16)
         k = vp.vp_batch_kernels(items)
         assert [int(r[0]) for r in k] == [kind], k.tolist()
+
+
+def test_batch_kernels_capacity_truncates():
+    """With room for fewer rows than launches, vp_batch_kernels writes the
+    first rows only and still reports the full count."""
+    items = vp._Batch(_workload_items(workloads.config(3)))
+    full = vp.vp_batch_kernels(_workload_items(workloads.config(3)))
+    assert len(full) >= 3
+    rows = np.full((3, 6), -7, np.int32)
+    n = ctypes.c_int32()
+    assert vp.lib().vp_batch_kernels(items.arr, len(items), vp._ptr(rows, ctypes.c_int32), 2,
+                                     ctypes.byref(n)) == vp.VP_OK
+    assert n.value == len(full)
+    assert rows[:2].tolist() == full[:2].tolist() and (rows[2] == -7).all()
