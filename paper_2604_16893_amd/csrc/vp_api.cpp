@@ -809,10 +809,10 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
     // bands of output rows that are multiples of 4 (one 64-value run per
     // store).  A band re-reads the source rows that its first window shares
     // with the band above, so none spans fewer than ten windows of source
-    // rows, or fifteen where the batch still gives every wave slot two
-    // workgroups at that length (a small batch of large frames -- one 1080p
-    // video of 128 frames -- otherwise gets units of ten windows that
-    // re-read about a tenth of their rows).
+    // rows, or fifteen where the batch still gives every wave slot four
+    // workgroups at that length (shorter units re-read more rows -- about a
+    // tenth at ten windows -- but in a batch of few workgroups they end it
+    // more evenly, which is worth more).
     constexpr int64_t kWaveSlots = 256 * 20;
     int64_t stream_frames = 0;
     auto source_row_cap = [&] {
@@ -864,7 +864,7 @@ int32_t build_plan(const vp_item* items, int32_t n, Plan* p) {
         d.sx_off = columns_for(*x_axes[b], sh.kx, sh.band, d.row_px);
     }
     const int64_t max_src_rows = source_row_cap();
-    const int64_t min_windows = workgroup_waves(15, max_src_rows) >= 2 * kWaveSlots ? 15 : 10;
+    const int64_t min_windows = workgroup_waves(15, max_src_rows) >= 4 * kWaveSlots ? 15 : 10;
     std::vector<Keyed> keyed;
     keyed.reserve(static_cast<size_t>(stream_frames));
     for (int32_t b = 0; b < n; ++b) {
